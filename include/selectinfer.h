@@ -1,0 +1,172 @@
+/*
+ * selectinfer.h — C ABI of the selective-computation gated FFN on MI355X (gfx950).
+ *
+ * The method (SelectInfer: selective neuron loading and computation): an FFN layer keeps only
+ * a "loaded" subset of its neurons (Selective Loading section), and each token computes only
+ * an "active" subset of the loaded neurons (Selective Computation section). Neuron n of a
+ * SwiGLU FFN is row n of gate_proj and up_proj and column n of down_proj (LLM Profiler
+ * section), so the selective FFN output is
+ *
+ *     y = sum_{j in active} SiLU(W_gate[j] . x) * (W_up[j] . x) * W_down[:, j].
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Every pointer argument is a DEVICE pointer unless stated otherwise. The caller allocates
+ *   and owns all buffers; the library keeps no pointer after a call returns.
+ * - Calls are enqueued on `hip_stream` (a hipStream_t, NULL = the null stream) and return
+ *   before the work finishes, except where a call is documented as synchronous. Buffers must
+ *   stay alive until the enqueued work completes.
+ * - Errors that can be seen from the host (NULL pointers, bad sizes, unsupported dtypes,
+ *   misaligned pointers, too small a workspace) return a nonzero status and enqueue nothing.
+ * - Kernels never read or write out of bounds whatever the CONTENT of index arrays: an out of
+ *   range slot id is skipped (contributes nothing), offsets are clamped to [0, nnz].
+ *   Index content is validated on the device only under SI_FLAG_CHECK (synchronous).
+ * - Matrices are row-major. bf16 values are IEEE bfloat16 bit patterns (2 bytes).
+ * - Index spaces: "original ids" are neuron numbers in [0, N); "slots" are positions in a
+ *   compacted layer, in [0, L). Slot s holds the loaded neuron with the s-th smallest id.
+ * - Results are deterministic: no floating-point atomics are used, every reduction has a
+ *   fixed order, and repeated calls with the same inputs give the same bits.
+ */
+#ifndef SELECTINFER_H
+#define SELECTINFER_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { SI_F32 = 0, SI_BF16 = 1 } si_dtype;
+
+typedef enum {
+    SI_OK = 0,
+    SI_ERR_INVALID = 1,     /* bad argument: NULL pointer, negative size, k > L, misalignment */
+    SI_ERR_RANGE = 2,       /* an id, slot or offset outside its range (device check)        */
+    SI_ERR_DUPLICATE = 3,   /* an id listed twice where a set is required (device check)     */
+    SI_ERR_NOT_LOADED = 4,  /* an original id whose neuron is not in the compacted layer     */
+    SI_ERR_UNSUPPORTED = 5, /* dtype or size the kernels do not handle                       */
+    SI_ERR_HIP = 6,         /* a HIP runtime call failed                                     */
+    SI_ERR_WORKSPACE = 7    /* workspace NULL or smaller than the *_workspace query says     */
+} si_status;
+
+/* Ranking key of si_select_topk. */
+enum { SI_TOPK_ABS = 0, SI_TOPK_RAW = 1 };
+
+/* Flags of si_selective_ffn and si_remap_ids. */
+enum {
+    SI_FLAG_CHECK = 1,      /* validate index content on the device, synchronise, report     */
+    SI_FLAG_PER_TOKEN = 2,  /* B > 1: use the per-token path even when the union path applies */
+    SI_FLAG_FAST_H = 4      /* union path: feed SiLU(g)*u to the second MFMA GEMM as one bf16
+                               value instead of a bf16 hi + lo pair (faster, ~1e-3 rel. err) */
+};
+
+/* Library version (major * 10000 + minor * 100 + patch). */
+int si_version(void);
+
+/* Static string naming a status code. Never NULL. */
+const char* si_status_string(int status);
+
+/*
+ * Selective loading (Selective Loading section): keep only the loaded neurons of one FFN
+ * layer, laid out neuron-major for row gathers.
+ *
+ *   w_gate, w_up  [N][d]  gate_proj / up_proj weights (PyTorch [out, in] storage), dtype wdt
+ *   w_down        [d][N]  down_proj weights, dtype wdt
+ *   loaded        [L]     int32 original ids, any order, unique, each in [0, N)
+ *   gate_up_c     [L][2][d] out: slot s holds (W_gate[n], W_up[n]) for its neuron n
+ *   down_c        [L][d]  out: slot s holds column n of W_down, contiguous
+ *   slot_to_orig  [L]     out: ascending original ids
+ *   orig_to_slot  [N]     out: slot of each neuron, -1 when not loaded
+ *
+ * A pure copy: outputs are bit-identical to the inputs' values. Compacted size is 3*d*L*s
+ * bytes and the memory left out is 3*d*(N-L)*s bytes (s = element size), per Eq. 2.
+ * SYNCHRONOUS: waits for the stream, so that it can report SI_ERR_RANGE (an id outside
+ * [0, N)) and SI_ERR_DUPLICATE. On such an error the outputs are unspecified.
+ * Requires 1 <= L <= N, d >= 1. Calls that overlap on one device are serialised internally.
+ */
+int si_compact_ffn(const void* w_gate, const void* w_up, const void* w_down,
+                   int64_t N, int64_t d, si_dtype wdt,
+                   const int32_t* loaded, int64_t L,
+                   void* gate_up_c, void* down_c,
+                   int32_t* slot_to_orig, int32_t* orig_to_slot,
+                   void* hip_stream);
+
+/*
+ * Original ids -> slots (Selective Computation section: only loaded neurons are computed).
+ *
+ *   orig_to_slot [N] int32 map from si_compact_ffn;  ids [n] int32;  slots [n] int32 out.
+ *
+ * slots[i] = orig_to_slot[ids[i]], or -1 when ids[i] is outside [0, N) or not loaded.
+ * With SI_FLAG_CHECK the call synchronises and returns SI_ERR_RANGE or SI_ERR_NOT_LOADED if
+ * any entry maps to -1 (the output is still written). n = 0 is allowed.
+ */
+int si_remap_ids(const int32_t* orig_to_slot, int64_t N,
+                 const int32_t* ids, int64_t n, int32_t* slots,
+                 int flags, void* hip_stream);
+
+/*
+ * Per-token top-k over loaded neurons (dynamic-neuron selection, Selective Computation
+ * section: rank a token's activations over the loaded neurons, descending, keep the top).
+ *
+ *   scores  [B][L] float32;  out_idx [B][k] int32 out, each row ascending.
+ *
+ * Row b selects the k slots with the largest key: key = |score| (SI_TOPK_ABS) or score
+ * (SI_TOPK_RAW). Equal keys go to the lower index; -0 and +0 are equal; NaN ranks below every
+ * number. The selected set is therefore unique. Requires 0 <= k <= L (k > L is
+ * SI_ERR_INVALID), L <= 2^24. B = 0 or k = 0 enqueue nothing.
+ */
+int si_select_topk(const float* scores, int64_t B, int64_t L, int64_t k, int mode,
+                   int32_t* out_idx, void* hip_stream);
+
+/*
+ * Workspace bytes si_selective_ffn needs for these sizes and flags (0 means none needed but a
+ * NULL workspace is still accepted only when 0 is returned). The value depends on B, nnz, L,
+ * d, the dtypes and flags only.
+ */
+size_t si_selective_ffn_workspace(int64_t B, int64_t nnz, int64_t L, int64_t d,
+                                  si_dtype xdt, si_dtype wdt, int flags);
+
+/*
+ * Selective computation (Selective Computation section) of one compacted SwiGLU FFN layer
+ * for B tokens:
+ *
+ *   y[b] = sum_{j in A_b} SiLU(gate_c[j] . x[b]) * (up_c[j] . x[b]) * down_c[j]
+ *
+ *   x         [B][d]   token activations, dtype xdt (SI_F32 or SI_BF16)
+ *   offsets   [B+1]    int32: token b's active slots are idx[offsets[b] .. offsets[b+1])
+ *   idx       [nnz]    int32 slot ids in [0, L), any order, no duplicates within a token
+ *   gate_up_c [L][2][d], down_c [L][d]  compacted layer from si_compact_ffn, dtype wdt
+ *   y         [B][d]   float32 out
+ *   ws                 workspace of at least si_selective_ffn_workspace(...) bytes
+ *
+ * Accumulation is float32. An empty active set gives y[b] = 0 exactly. Paths:
+ *   - per-token (B == 1, fp32 weights or x, or SI_FLAG_PER_TOKEN): a gather-GEMV streams only
+ *     the active rows with 16-byte loads and a fused SiLU*up epilogue, then accumulates the
+ *     down rows into float32 partial sums that a second kernel adds in a fixed order;
+ *   - union (B >= 2, bf16 weights and x): the union of the B active sets is built on the
+ *     device and both projections run as bf16 MFMA gather-GEMMs over the union rows, with
+ *     each token's h masked to its own set. Each union row is read from HBM once per call.
+ * Requirements: d % 8 == 0 for bf16 data, d % 4 == 0 for f32; d <= 32768 (bf16) or 16384
+ * (f32); 16-byte aligned x, gate_up_c, down_c, y and ws; B >= 0; nnz >= 0; L >= 1.
+ * SI_FLAG_CHECK validates offsets (non-decreasing, within [0, nnz]), slot range and duplicates
+ * on the device, synchronises and returns SI_ERR_RANGE / SI_ERR_DUPLICATE before computing.
+ */
+int si_selective_ffn(const void* x, si_dtype xdt, int64_t B, int64_t d,
+                     const int32_t* offsets, const int32_t* idx, int64_t nnz,
+                     const void* gate_up_c, const void* down_c, int64_t L, si_dtype wdt,
+                     float* y, void* ws, size_t ws_bytes, int flags, void* hip_stream);
+
+/*
+ * Layer step of a stacked FFN: x_out[b] = RMSNorm(x[b] + y[b]) with unit gain,
+ * r / sqrt(mean(r^2) + eps), computed in float32 and stored in xdt (bf16: round to nearest
+ * even). x [B][d] (xdt), y [B][d] float32, x_out [B][d] (xdt); x_out may alias x.
+ */
+int si_residual_rmsnorm(const void* x, si_dtype xdt, const float* y, int64_t B, int64_t d,
+                        float eps, void* x_out, void* hip_stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SELECTINFER_H */

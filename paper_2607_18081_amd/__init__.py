@@ -1,0 +1,23 @@
+"""MI355X-native selective-computation gated FFN (SelectInfer's hot path).
+
+The C ABI (include/selectinfer.h) is implemented in HIP for gfx950 in ``csrc/`` and built into
+``libselectinfer.so``; this package is its thin Python binding.
+"""
+from .api import (  # noqa: F401
+    BF16,
+    F32,
+    FLAG_CHECK,
+    FLAG_FAST_H,
+    FLAG_PER_TOKEN,
+    TOPK_ABS,
+    TOPK_RAW,
+    CompactLayer,
+    SelectInferError,
+    compact_ffn,
+    remap_ids,
+    residual_rmsnorm,
+    select_topk,
+    selective_ffn,
+    selective_ffn_workspace,
+    version,
+)

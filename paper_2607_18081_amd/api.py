@@ -1,0 +1,188 @@
+"""Python binding of the selective-FFN C ABI (argument marshalling only).
+
+Tensors are PyTorch tensors on a ROCm device; they supply device memory and the current HIP
+stream. Every computation happens in the HIP kernels of libselectinfer.so. Function names
+follow the C entry points without their ``si_`` prefix.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import torch
+
+from ._lib import load
+
+F32, BF16 = 0, 1
+TOPK_ABS, TOPK_RAW = 0, 1
+FLAG_CHECK, FLAG_PER_TOKEN, FLAG_FAST_H = 1, 2, 4
+
+_DT = {torch.float32: F32, torch.bfloat16: BF16}
+
+
+class SelectInferError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        msg = load().si_status_string(status).decode()
+        super().__init__(f"{where}: {msg} (status {status})")
+        self.status = status
+
+
+def _check(status: int, where: str) -> None:
+    if status != 0:
+        raise SelectInferError(status, where)
+
+
+def _dt(t: torch.Tensor) -> int:
+    try:
+        return _DT[t.dtype]
+    except KeyError:
+        raise TypeError(f"unsupported dtype {t.dtype}") from None
+
+
+def _dev(t: torch.Tensor) -> torch.device:
+    if t.device.type != "cuda":
+        raise ValueError("tensors must live on a ROCm GPU device")
+    return t.device
+
+
+def _ptr(t):
+    if t is None or t.numel() == 0:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("tensors must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(device: torch.device) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def version() -> int:
+    return load().si_version()
+
+
+@dataclass
+class CompactLayer:
+    """A compacted FFN layer: only the loaded neurons, neuron-major."""
+    gate_up_c: torch.Tensor      # [L][2][d]
+    down_c: torch.Tensor         # [L][d]
+    slot_to_orig: torch.Tensor   # [L] int32, ascending
+    orig_to_slot: torch.Tensor   # [N] int32, -1 = not loaded
+
+    @property
+    def L(self) -> int:
+        return self.gate_up_c.shape[0]
+
+    @property
+    def d(self) -> int:
+        return self.gate_up_c.shape[2]
+
+
+def compact_ffn(w_gate: torch.Tensor, w_up: torch.Tensor, w_down: torch.Tensor,
+                loaded: torch.Tensor) -> CompactLayer:
+    """si_compact_ffn: W_gate/W_up [N][d], W_down [d][N], loaded ids [L] -> CompactLayer."""
+    dev = _dev(w_gate)
+    N, d = w_gate.shape
+    if w_up.shape != (N, d) or w_down.shape != (d, N):
+        raise ValueError("weight shapes must be [N][d], [N][d], [d][N]")
+    if not (w_gate.dtype == w_up.dtype == w_down.dtype):
+        raise ValueError("weights must share one dtype")
+    loaded = loaded.to(device=dev, dtype=torch.int32).contiguous()
+    L = loaded.numel()
+    gu = torch.empty((L, 2, d), dtype=w_gate.dtype, device=dev)
+    dc = torch.empty((L, d), dtype=w_gate.dtype, device=dev)
+    s2o = torch.empty(L, dtype=torch.int32, device=dev)
+    o2s = torch.empty(N, dtype=torch.int32, device=dev)
+    st = load().si_compact_ffn(_ptr(w_gate), _ptr(w_up), _ptr(w_down), N, d, _dt(w_gate),
+                               _ptr(loaded), L, _ptr(gu), _ptr(dc), _ptr(s2o), _ptr(o2s),
+                               _stream(dev))
+    _check(st, "si_compact_ffn")
+    return CompactLayer(gu, dc, s2o, o2s)
+
+
+def remap_ids(orig_to_slot: torch.Tensor, ids: torch.Tensor, check: bool = False,
+              out: torch.Tensor | None = None) -> torch.Tensor:
+    """si_remap_ids: original ids -> slots (-1 where not loaded)."""
+    dev = _dev(orig_to_slot)
+    ids = ids.to(device=dev, dtype=torch.int32).contiguous()
+    if out is None:
+        out = torch.empty_like(ids)
+    st = load().si_remap_ids(_ptr(orig_to_slot), orig_to_slot.numel(), _ptr(ids), ids.numel(),
+                             _ptr(out), FLAG_CHECK if check else 0, _stream(dev))
+    _check(st, "si_remap_ids")
+    return out
+
+
+def select_topk(scores: torch.Tensor, k: int, mode: str = "abs",
+                out: torch.Tensor | None = None) -> torch.Tensor:
+    """si_select_topk: scores [B][L] float32 -> [B][k] int32, rows ascending."""
+    dev = _dev(scores)
+    if scores.dtype != torch.float32 or scores.dim() != 2:
+        raise ValueError("scores must be a 2-D float32 tensor")
+    B, L = scores.shape
+    if out is None:
+        out = torch.empty((B, k), dtype=torch.int32, device=dev)
+    m = {"abs": TOPK_ABS, "raw": TOPK_RAW}[mode]
+    st = load().si_select_topk(_ptr(scores), B, L, k, m, _ptr(out), _stream(dev))
+    _check(st, "si_select_topk")
+    return out
+
+
+def selective_ffn_workspace(B: int, nnz: int, L: int, d: int, xdt=BF16, wdt=BF16,
+                            flags: int = 0) -> int:
+    return int(load().si_selective_ffn_workspace(B, nnz, L, d, xdt, wdt, flags))
+
+
+_WS: dict = {}
+
+
+def _workspace(dev: torch.device, nbytes: int) -> torch.Tensor:
+    """A per-device workspace that only grows. Calls sharing it must not overlap in time
+    (pass ``workspace=`` explicitly when using several streams)."""
+    key = (dev.type, dev.index)
+    ws = _WS.get(key)
+    if ws is None or ws.numel() < nbytes:
+        ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev)
+        _WS[key] = ws
+    return ws
+
+
+def selective_ffn(x: torch.Tensor, offsets: torch.Tensor, idx: torch.Tensor,
+                  gate_up_c: torch.Tensor, down_c: torch.Tensor, flags: int = 0,
+                  y: torch.Tensor | None = None,
+                  workspace: torch.Tensor | None = None) -> torch.Tensor:
+    """si_selective_ffn: x [B][d], CSR active slots (offsets [B+1], idx [nnz]) -> y [B][d] f32."""
+    dev = _dev(x)
+    if x.dim() != 2:
+        raise ValueError("x must be [B][d]")
+    B, d = x.shape
+    L = gate_up_c.shape[0]
+    if gate_up_c.shape != (L, 2, d) or down_c.shape != (L, d):
+        raise ValueError("compacted weights must be [L][2][d] and [L][d]")
+    if offsets.dtype != torch.int32 or idx.dtype != torch.int32:
+        raise ValueError("offsets and idx must be int32")
+    if offsets.numel() < B + 1:
+        raise ValueError("offsets needs B + 1 entries")
+    nnz = idx.numel()
+    if y is None:
+        y = torch.empty((B, d), dtype=torch.float32, device=dev)
+    need = selective_ffn_workspace(B, nnz, L, d, _dt(x), _dt(gate_up_c), flags)
+    if workspace is None:
+        workspace = _workspace(dev, need)
+    st = load().si_selective_ffn(_ptr(x), _dt(x), B, d, _ptr(offsets), _ptr(idx), nnz,
+                                 _ptr(gate_up_c), _ptr(down_c), L, _dt(gate_up_c), _ptr(y),
+                                 _ptr(workspace), workspace.numel(), flags, _stream(dev))
+    _check(st, "si_selective_ffn")
+    return y
+
+
+def residual_rmsnorm(x: torch.Tensor, y: torch.Tensor, eps: float = 1e-5,
+                     out: torch.Tensor | None = None) -> torch.Tensor:
+    """si_residual_rmsnorm: RMSNorm(x + y), unit gain, stored in x's dtype."""
+    dev = _dev(x)
+    B, d = x.shape
+    if out is None:
+        out = torch.empty_like(x)
+    st = load().si_residual_rmsnorm(_ptr(x), _dt(x), _ptr(y), B, d, float(eps), _ptr(out),
+                                    _stream(dev))
+    _check(st, "si_residual_rmsnorm")
+    return out

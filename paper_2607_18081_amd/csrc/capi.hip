@@ -1,0 +1,203 @@
+// C ABI of the selective-FFN library: argument checks, dispatch to the kernels, status codes.
+#include <mutex>
+
+#include "common.h"
+#include "launch.h"
+#include "selectinfer.h"
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+
+// Per-device status word written by device-side checks. Only synchronous calls use it, under
+// g_check_mu, so overlapping checked calls on one device cannot mix their results.
+__device__ int si_status_word[2];
+
+std::mutex g_check_mu;
+int* g_status_ptr[kMaxDevices] = {};
+int g_num_cu[kMaxDevices] = {};
+
+int current_device() {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return -1;
+    return dev;
+}
+
+// caller holds g_check_mu
+int* status_word(int dev) {
+    if (!g_status_ptr[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(si_status_word)) != hipSuccess) return nullptr;
+        g_status_ptr[dev] = static_cast<int*>(p);
+    }
+    return g_status_ptr[dev];
+}
+
+int num_cu(int dev) {
+    static std::mutex mu;
+    std::lock_guard<std::mutex> lk(mu);
+    if (!g_num_cu[dev]) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            n <= 0)
+            n = 256;
+        g_num_cu[dev] = n;
+    }
+    return g_num_cu[dev];
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int from_hip(hipError_t e) { return e == hipSuccess ? SI_OK : SI_ERR_HIP; }
+
+// Clears the status word, runs `enqueue`, waits, and returns the device's verdict.
+template <typename F>
+int checked(hipStream_t s, int dev, F enqueue) {
+    std::lock_guard<std::mutex> lk(g_check_mu);
+    int* w = status_word(dev);
+    if (!w) return SI_ERR_HIP;
+    if (hipMemsetAsync(w, 0, 2 * sizeof(int), s) != hipSuccess) return SI_ERR_HIP;
+    if (enqueue(w) != hipSuccess) return SI_ERR_HIP;
+    int host[2] = {0, 0};
+    if (hipMemcpyAsync(host, w, sizeof(host), hipMemcpyDeviceToHost, s) != hipSuccess)
+        return SI_ERR_HIP;
+    if (hipStreamSynchronize(s) != hipSuccess) return SI_ERR_HIP;
+    return host[0];
+}
+
+bool valid_dtype(int t) { return t == SI_F32 || t == SI_BF16; }
+
+bool use_union(int64_t B, int64_t L, si_dtype xdt, si_dtype wdt, int flags) {
+    // Reading the union once costs |U| rows instead of nnz >= |U|, and the dense-over-union
+    // MFMA work stays far below the HBM time of those rows for any overlap (see the design
+    // notes), so B >= 2 always takes it when the dtypes allow bf16 MFMA.
+    return B >= 2 && xdt == SI_BF16 && wdt == SI_BF16 && !(flags & SI_FLAG_PER_TOKEN) &&
+           L <= 524288;
+}
+
+}  // namespace
+
+extern "C" {
+
+int si_version(void) { return 100; }
+
+const char* si_status_string(int status) {
+    switch (status) {
+        case SI_OK: return "ok";
+        case SI_ERR_INVALID: return "invalid argument";
+        case SI_ERR_RANGE: return "id, slot or offset out of range";
+        case SI_ERR_DUPLICATE: return "duplicate id";
+        case SI_ERR_NOT_LOADED: return "neuron not loaded";
+        case SI_ERR_UNSUPPORTED: return "unsupported dtype or size";
+        case SI_ERR_HIP: return "HIP runtime error";
+        case SI_ERR_WORKSPACE: return "workspace missing or too small";
+        default: return "unknown status";
+    }
+}
+
+int si_compact_ffn(const void* w_gate, const void* w_up, const void* w_down, int64_t N,
+                   int64_t d, si_dtype wdt, const int32_t* loaded, int64_t L, void* gate_up_c,
+                   void* down_c, int32_t* slot_to_orig, int32_t* orig_to_slot,
+                   void* hip_stream) {
+    if (!w_gate || !w_up || !w_down || !loaded || !gate_up_c || !down_c || !slot_to_orig ||
+        !orig_to_slot)
+        return SI_ERR_INVALID;
+    if (!valid_dtype(wdt)) return SI_ERR_UNSUPPORTED;
+    if (N < 1 || d < 1 || L < 1 || L > N || N > INT32_MAX) return SI_ERR_INVALID;
+    const int es = wdt == SI_BF16 ? 2 : 4;
+    if ((d * es) % 16 != 0) return SI_ERR_UNSUPPORTED;
+    if (!aligned16(w_gate) || !aligned16(w_up) || !aligned16(gate_up_c)) return SI_ERR_INVALID;
+    const int dev = current_device();
+    if (dev < 0) return SI_ERR_HIP;
+    hipStream_t s = static_cast<hipStream_t>(hip_stream);
+    int st = checked(s, dev, [&](int* err) {
+        return si::launch_compact_maps(loaded, L, N, slot_to_orig, orig_to_slot, err, s);
+    });
+    if (st != SI_OK) return st;
+    hipError_t e = si::launch_compact_gather(w_gate, w_up, w_down, N, d, es, slot_to_orig, L,
+                                             gate_up_c, down_c, s);
+    if (e != hipSuccess) return SI_ERR_HIP;
+    return from_hip(hipStreamSynchronize(s));
+}
+
+int si_remap_ids(const int32_t* orig_to_slot, int64_t N, const int32_t* ids, int64_t n,
+                 int32_t* slots, int flags, void* hip_stream) {
+    if (n < 0 || N < 1) return SI_ERR_INVALID;
+    if (n == 0) return SI_OK;
+    if (!orig_to_slot || !ids || !slots) return SI_ERR_INVALID;
+    hipStream_t s = static_cast<hipStream_t>(hip_stream);
+    if (flags & SI_FLAG_CHECK) {
+        const int dev = current_device();
+        if (dev < 0) return SI_ERR_HIP;
+        return checked(s, dev, [&](int* err) {
+            return si::launch_remap(orig_to_slot, N, ids, n, slots, err, s);
+        });
+    }
+    return from_hip(si::launch_remap(orig_to_slot, N, ids, n, slots, nullptr, s));
+}
+
+int si_select_topk(const float* scores, int64_t B, int64_t L, int64_t k, int mode,
+                   int32_t* out_idx, void* hip_stream) {
+    if (B < 0 || L < 1 || k < 0 || k > L || L > (1 << 24)) return SI_ERR_INVALID;
+    if (mode != SI_TOPK_ABS && mode != SI_TOPK_RAW) return SI_ERR_INVALID;
+    if (B == 0 || k == 0) return SI_OK;
+    if (!scores || !out_idx) return SI_ERR_INVALID;
+    return from_hip(si::launch_topk(scores, B, L, k, mode, out_idx,
+                                    static_cast<hipStream_t>(hip_stream)));
+}
+
+size_t si_selective_ffn_workspace(int64_t B, int64_t nnz, int64_t L, int64_t d, si_dtype xdt,
+                                  si_dtype wdt, int flags) {
+    if (B <= 0 || d <= 0 || L <= 0 || nnz < 0) return 0;
+    const int dev = current_device();
+    const int ncu = dev < 0 ? 256 : num_cu(dev);
+    if (use_union(B, L, xdt, wdt, flags)) return si::union_workspace(B, L, d, ncu);
+    const int P = si::decode_chunks(B, nnz, ncu);
+    return (size_t)B * P * d * sizeof(float);
+}
+
+int si_selective_ffn(const void* x, si_dtype xdt, int64_t B, int64_t d, const int32_t* offsets,
+                     const int32_t* idx, int64_t nnz, const void* gate_up_c, const void* down_c,
+                     int64_t L, si_dtype wdt, float* y, void* ws, size_t ws_bytes, int flags,
+                     void* hip_stream) {
+    if (B < 0 || d < 1 || L < 1 || nnz < 0) return SI_ERR_INVALID;
+    if (!valid_dtype(xdt) || !valid_dtype(wdt)) return SI_ERR_UNSUPPORTED;
+    if (B > 65535 || nnz > INT32_MAX || L > INT32_MAX) return SI_ERR_UNSUPPORTED;
+    if (si::decode_supported(xdt, wdt, d)) return SI_ERR_UNSUPPORTED;
+    if (B == 0) return SI_OK;
+    if (!x || !offsets || !gate_up_c || !down_c || !y) return SI_ERR_INVALID;
+    if (nnz > 0 && !idx) return SI_ERR_INVALID;
+    if (!aligned16(x) || !aligned16(gate_up_c) || !aligned16(down_c) || !aligned16(y))
+        return SI_ERR_INVALID;
+    const size_t need = si_selective_ffn_workspace(B, nnz, L, d, xdt, wdt, flags);
+    if (need > 0 && (!ws || ws_bytes < need || !aligned16(ws))) return SI_ERR_WORKSPACE;
+    const int dev = current_device();
+    if (dev < 0) return SI_ERR_HIP;
+    hipStream_t s = static_cast<hipStream_t>(hip_stream);
+    if (flags & SI_FLAG_CHECK) {
+        if (L > 524288) return SI_ERR_UNSUPPORTED;
+        const int st = checked(s, dev, [&](int* err) {
+            return si::launch_check_csr(offsets, idx, B, nnz, L, err, s);
+        });
+        if (st != SI_OK) return st;
+    }
+    const int ncu = num_cu(dev);
+    if (use_union(B, L, xdt, wdt, flags))
+        return from_hip(si::launch_union(x, B, d, offsets, idx, nnz, gate_up_c, down_c, L, y, ws,
+                                         flags, ncu, s));
+    const int P = si::decode_chunks(B, nnz, ncu);
+    return from_hip(si::launch_decode(x, xdt, B, d, offsets, idx, nnz, gate_up_c, down_c, L, wdt,
+                                      static_cast<float*>(ws), P, y, s));
+}
+
+int si_residual_rmsnorm(const void* x, si_dtype xdt, const float* y, int64_t B, int64_t d,
+                        float eps, void* x_out, void* hip_stream) {
+    if (B < 0 || d < 1 || !(eps >= 0.0f)) return SI_ERR_INVALID;
+    if (!valid_dtype(xdt)) return SI_ERR_UNSUPPORTED;
+    if (B == 0) return SI_OK;
+    if (!x || !y || !x_out) return SI_ERR_INVALID;
+    return from_hip(si::launch_residual_rmsnorm(x, xdt, y, B, d, eps, x_out,
+                                                static_cast<hipStream_t>(hip_stream)));
+}
+
+}  // extern "C"

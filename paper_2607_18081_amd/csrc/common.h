@@ -1,0 +1,114 @@
+// Device helpers shared by the selective-FFN kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace si {
+
+constexpr int kWave = 64;
+
+typedef uint16_t bf16_t;  // bfloat16 bit pattern
+
+// Error word layout written by device-side checks (first nonzero code wins).
+struct ErrWord {
+    int code;
+    int detail;
+};
+
+__device__ __forceinline__ void set_err(int* err, int code, int detail) {
+    // integer compare-and-swap on a status word; never on the decode hot path
+    if (atomicCAS(err, 0, code) == 0) err[1] = detail;
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
+    return __uint_as_float(bits16 << 16);
+}
+
+// low / high halves of a 32-bit word holding two bf16 values
+__device__ __forceinline__ float bf16lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// float -> bf16 bits, round to nearest even (inputs here are finite)
+__device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
+    uint32_t u = __float_as_uint(f);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+
+// 16-byte vector types
+struct alignas(16) V16 {
+    uint32_t w[4];
+};
+
+__device__ __forceinline__ V16 ld16(const void* p) {
+    return *reinterpret_cast<const V16*>(p);
+}
+__device__ __forceinline__ void st16(void* p, const V16& v) {
+    *reinterpret_cast<V16*>(p) = v;
+}
+
+// Unpack a 16-byte vector into V floats (V = 8 for bf16, 4 for f32).
+template <typename T>
+struct Elem;
+template <>
+struct Elem<float> {
+    static constexpr int V = 4;
+    __device__ __forceinline__ static void unpack(const V16& v, float* f) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) f[e] = __uint_as_float(v.w[e]);
+    }
+};
+template <>
+struct Elem<bf16_t> {
+    static constexpr int V = 8;
+    __device__ __forceinline__ static void unpack(const V16& v, float* f) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            f[2 * e] = bf16lo(v.w[e]);
+            f[2 * e + 1] = bf16hi(v.w[e]);
+        }
+    }
+};
+
+// SiLU(g) = g * sigmoid(g), float32
+__device__ __forceinline__ float silu_f32(float g) { return g / (1.0f + __expf(-g)); }
+
+// Sum over the 64 lanes of a wave; every lane receives the total.
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, kWave);
+    return v;
+}
+
+// Reduce NVAL per-lane values across the wave at once. On return, lane l holds the wave total
+// of value index l / (64 / NVAL). NVAL is a power of two, 1 <= NVAL <= 64. Costs
+// NVAL - 1 + log2(64 / NVAL) shuffles instead of 6 * NVAL.
+template <int NVAL>
+__device__ __forceinline__ float wave_transpose_sum(float (&v)[NVAL], int lane) {
+    static_assert((NVAL & (NVAL - 1)) == 0 && NVAL >= 1 && NVAL <= 64, "NVAL");
+    int cnt = NVAL;
+    int mask = 32;
+#pragma unroll
+    for (int step = 0; step < 6; ++step) {
+        if (cnt > 1) {
+            const int half = cnt >> 1;
+            const bool upper = (lane & mask) != 0;
+#pragma unroll
+            for (int m = 0; m < NVAL / 2; ++m) {
+                if (m < half) {
+                    float send = upper ? v[m] : v[m + half];
+                    float keep = upper ? v[m + half] : v[m];
+                    v[m] = keep + __shfl_xor(send, mask, kWave);
+                }
+            }
+            cnt = half;
+        } else {
+            v[0] += __shfl_xor(v[0], mask, kWave);
+        }
+        mask >>= 1;
+    }
+    return v[0];
+}
+
+}  // namespace si

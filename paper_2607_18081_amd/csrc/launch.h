@@ -1,0 +1,49 @@
+// Host-side launchers of the selective-FFN kernels (one per kernel file).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace si {
+
+// ---- k_decode.hip: per-token path ------------------------------------------------------
+// Number of row chunks (work-groups) per token for the per-token path.
+int decode_chunks(int64_t B, int64_t nnz, int num_cu);
+// 0 if the shape is supported, else nonzero.
+int decode_supported(int xdt, int wdt, int64_t d);
+// y[b][c] = sum over p of partials[b][p][c], p in fixed order.
+hipError_t launch_reduce_partials(const float* partials, int P, int64_t B, int64_t d, float* y,
+                                  hipStream_t s);
+hipError_t launch_decode(const void* x, int xdt, int64_t B, int64_t d, const int32_t* offsets,
+                         const int32_t* idx, int64_t nnz, const void* gate_up_c,
+                         const void* down_c, int64_t L, int wdt, float* partials, int P,
+                         float* y, hipStream_t s);
+
+// ---- k_union.hip: union (MFMA) path -----------------------------------------------------
+size_t union_workspace(int64_t B, int64_t L, int64_t d, int num_cu);
+hipError_t launch_union(const void* x, int64_t B, int64_t d, const int32_t* offsets,
+                        const int32_t* idx, int64_t nnz, const void* gate_up_c,
+                        const void* down_c, int64_t L, float* y, void* ws, int flags,
+                        int num_cu, hipStream_t s);
+
+// ---- k_topk.hip ---------------------------------------------------------------------------
+hipError_t launch_topk(const float* scores, int64_t B, int64_t L, int64_t k, int mode,
+                       int32_t* out, hipStream_t s);
+
+// ---- k_compact.hip ------------------------------------------------------------------------
+hipError_t launch_compact_maps(const int32_t* loaded, int64_t L, int64_t N,
+                               int32_t* slot_to_orig, int32_t* orig_to_slot, int* err,
+                               hipStream_t s);
+hipError_t launch_compact_gather(const void* w_gate, const void* w_up, const void* w_down,
+                                 int64_t N, int64_t d, int esize, const int32_t* slot_to_orig,
+                                 int64_t L, void* gate_up_c, void* down_c, hipStream_t s);
+
+// ---- k_misc.hip ---------------------------------------------------------------------------
+hipError_t launch_remap(const int32_t* orig_to_slot, int64_t N, const int32_t* ids, int64_t n,
+                        int32_t* slots, int* err, hipStream_t s);
+hipError_t launch_check_csr(const int32_t* offsets, const int32_t* idx, int64_t B,
+                            int64_t nnz, int64_t L, int* err, hipStream_t s);
+hipError_t launch_residual_rmsnorm(const void* x, int xdt, const float* y, int64_t B, int64_t d,
+                                   float eps, void* x_out, hipStream_t s);
+
+}  // namespace si

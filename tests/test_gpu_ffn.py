@@ -1,0 +1,229 @@
+"""GPU parity of si_selective_ffn against the fp64 oracle, per token.
+
+Tolerance (per token, relative L2, max over tokens): 1e-5 for f32 weights, 5e-3 for bf16
+weights. The per-token path only reassociates float32 sums, so it is also held to an internal
+1e-4 alarm; the union path rounds h to a bf16 hi+lo pair for its MFMA GEMM.
+"""
+import functools
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_18081_amd as si
+from tests.gpu_util import dev_tensor, host_array, max_rel_l2, rel_l2, say
+from workloads import CONFIGS, active_sets, csr_from_sets, layer_weights, loaded_ids, tokens_x
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-5, "bf16": 5e-3}
+ALARM_PER_TOKEN = 1e-4
+
+
+@functools.lru_cache(maxsize=2)
+def _layer(name, layer=0):
+    cfg = CONFIGS[name]
+    wg, wu, wd = layer_weights(cfg, layer)
+    loaded = loaded_ids(cfg, layer)
+    ref = oracle.compact(wg, wu, wd, loaded)
+    gpu = si.compact_ffn(dev_tensor(wg), dev_tensor(wu), dev_tensor(wd),
+                         torch.from_numpy(loaded))
+    return cfg, ref, gpu
+
+
+def _slots(ref, sets):
+    return [oracle.remap(ref["orig_to_slot"], s) for s in sets]
+
+
+def _run(x, slot_sets, gpu, flags=0):
+    off, idx = csr_from_sets(slot_sets)
+    y = si.selective_ffn(dev_tensor(x), dev_tensor(off), dev_tensor(idx), gpu.gate_up_c,
+                         gpu.down_c, flags=flags)
+    return host_array(y)
+
+
+def _oracle(x, slot_sets, ref):
+    return np.stack([oracle.selective_ffn(x[t], slot_sets[t], ref["gate_up_c"], ref["down_c"])
+                     for t in range(len(slot_sets))])
+
+
+def test_tiny_f32_all_tokens():
+    cfg, ref, gpu = _layer("tiny_f32")
+    say("tiny f32: 64 tokens, one call per token and one batched call")
+    toks = range(cfg.steps)
+    x = tokens_x(cfg, toks)
+    slots = _slots(ref, active_sets(cfg, toks))
+    want = _oracle(x, slots, ref)
+    per_call = np.stack([_run(x[t:t + 1], [slots[t]], gpu)[0] for t in toks])
+    assert max_rel_l2(per_call, want) <= TOL["f32"]
+    batched = _run(x, slots, gpu)
+    assert max_rel_l2(batched, want) <= TOL["f32"]
+
+
+def test_llama2_7b_decode_sampled_tokens():
+    cfg, ref, gpu = _layer("llama2_7b_decode")
+    toks = [0, 1, 2, 3, 511, 1023]
+    say(f"7B decode: tokens {toks}, B=1 calls as in the benchmark")
+    x = tokens_x(cfg, toks)
+    slots = _slots(ref, active_sets(cfg, toks))
+    want = _oracle(x, slots, ref)
+    got = np.stack([_run(x[i:i + 1], [slots[i]], gpu)[0] for i in range(len(toks))])
+    err = max_rel_l2(got, want)
+    say(f"7B decode max rel L2 {err:.3e}")
+    assert err <= TOL["bf16"] and err <= ALARM_PER_TOKEN
+    # bitwise reproducible
+    again = np.stack([_run(x[i:i + 1], [slots[i]], gpu)[0] for i in range(len(toks))])
+    assert np.array_equal(got, again)
+    # order of the index list does not matter beyond float32 reassociation
+    rev = np.stack([_run(x[i:i + 1], [slots[i][::-1].copy()], gpu)[0] for i in range(len(toks))])
+    assert max_rel_l2(rev, got) <= 1e-6
+
+
+def _rand_problem(seed, N, d, L, wdtype):
+    rng = np.random.default_rng(seed)
+    def draw(*shape, scale=0.02):
+        a = (rng.standard_normal(shape) * scale).astype(np.float32)
+        return (a.view(np.uint32) >> 16).astype(np.uint16) if wdtype == "bf16" else a
+    wg, wu, wd = draw(N, d), draw(N, d), draw(d, N)
+    loaded = rng.permutation(N)[:L].astype(np.int32)
+    ref = oracle.compact(wg, wu, wd, loaded)
+    gpu = si.compact_ffn(dev_tensor(wg), dev_tensor(wu), dev_tensor(wd),
+                         torch.from_numpy(loaded))
+    return rng, draw, ref, gpu
+
+
+@pytest.mark.parametrize("d,wdtype", [(8, "bf16"), (264, "bf16"), (1000, "bf16"),
+                                      (4104, "bf16"), (5120, "bf16"), (12, "f32"),
+                                      (1000, "f32"), (2052, "f32")])
+def test_per_token_ragged_shapes(d, wdtype):
+    N, L = 700, 530
+    say(f"per-token ragged d={d} {wdtype}")
+    rng, draw, ref, gpu = _rand_problem(d, N, d, L, wdtype)
+    ks = [0, 1, 2, 7, 8, 9, 17, 130, 529, 530]
+    sets = [rng.permutation(L)[:k].astype(np.int32) for k in ks]
+    x = draw(len(ks), d, scale=1.0)
+    want = _oracle(x, sets, ref)
+    got = np.stack([_run(x[i:i + 1], [sets[i]], gpu)[0] for i in range(len(ks))])
+    assert not np.any(got[0])                       # empty set -> exact zeros
+    err = max_rel_l2(got, want)
+    assert err <= TOL[wdtype] and (wdtype == "f32" or err <= ALARM_PER_TOKEN)
+    got_b = _run(x, sets, gpu, flags=si.FLAG_PER_TOKEN)
+    assert max_rel_l2(got_b, want) <= TOL[wdtype]
+
+
+@pytest.mark.parametrize("B,d", [(2, 264), (5, 1000), (17, 264), (33, 512), (70, 1000)])
+def test_union_path_ragged(B, d):
+    N, L = 900, 613
+    say(f"union ragged B={B} d={d}")
+    rng, draw, ref, gpu = _rand_problem(B * 1000 + d, N, d, L, "bf16")
+    sets = []
+    for b in range(B):
+        k = int(rng.integers(0, L + 1)) if b % 4 else (0 if b == 4 else int(rng.integers(1, 60)))
+        sets.append(rng.permutation(L)[:k].astype(np.int32))
+    x = draw(B, d, scale=1.0)
+    want = _oracle(x, sets, ref)
+    got = _run(x, sets, gpu)
+    for b in range(B):
+        if len(sets[b]) == 0:
+            assert not np.any(got[b])
+    assert max_rel_l2(got, want) <= TOL["bf16"]
+    fast = _run(x, sets, gpu, flags=si.FLAG_FAST_H)
+    assert max_rel_l2(fast, want) <= TOL["bf16"]
+
+
+def test_llama2_7b_batch16_union():
+    cfg, ref, gpu = _layer("llama2_7b_b16")
+    say("7B batch-16 union path: 2 steps of 16 tokens")
+    for step in range(2):
+        toks = range(step * 16, step * 16 + 16)
+        x = tokens_x(cfg, toks)
+        slots = _slots(ref, active_sets(cfg, toks))
+        want = _oracle(x, slots, ref)
+        got = _run(x, slots, gpu)
+        err = max_rel_l2(got, want)
+        say(f"union step {step} max rel L2 {err:.3e}")
+        assert err <= TOL["bf16"]
+        per_tok = _run(x, slots, gpu, flags=si.FLAG_PER_TOKEN)
+        assert max_rel_l2(per_tok, want) <= ALARM_PER_TOKEN
+        assert max_rel_l2(got, per_tok) <= TOL["bf16"]
+
+
+def test_llama2_13b_prefill_union_sampled():
+    cfg, ref, gpu = _layer("llama2_13b_prefill")
+    say("13B prefill: 512 tokens in one union call, 12 tokens checked")
+    toks = range(cfg.B)
+    x = tokens_x(cfg, toks)
+    slots = _slots(ref, active_sets(cfg, toks))
+    got = _run(x, slots, gpu)
+    sample = [0, 1, 77, 128, 255, 256, 300, 383, 384, 500, 510, 511]
+    want = _oracle(x[sample], [slots[t] for t in sample], ref)
+    err = max_rel_l2(got[sample], want)
+    say(f"13B prefill max rel L2 {err:.3e}")
+    assert err <= TOL["bf16"]
+    # every token's output is finite and nonzero
+    assert np.all(np.isfinite(got)) and np.all(np.abs(got).sum(axis=1) > 0)
+
+
+def test_llama3_8b_stack_teacher_forced():
+    name = "llama3_8b_stack"
+    cfg = CONFIGS[name]
+    toks = [0, 1]
+    say(f"8B stack: 2 layers teacher-forced, tokens {toks}")
+    x = tokens_x(cfg, toks)
+    for layer in range(2):
+        c, ref, gpu = _layer(name, layer)
+        slots = _slots(ref, active_sets(cfg, toks, layer))
+        y = _run(x, slots, gpu, flags=si.FLAG_PER_TOKEN)
+        want = _oracle(x, slots, ref)
+        assert max_rel_l2(y, want) <= ALARM_PER_TOKEN
+        xn = host_array(si.residual_rmsnorm(dev_tensor(x), dev_tensor(y.astype(np.float32))))
+        for t in range(len(toks)):
+            ref_next = oracle.residual_rmsnorm_bf16(x[t], want[t])
+            assert rel_l2(oracle.decode(xn[t]), oracle.decode(ref_next)) <= TOL["bf16"]
+        x = xn                                      # the oracle's next layer takes the GPU's x
+
+
+def test_check_flag_and_errors():
+    say("check flag and error paths")
+    rng, draw, ref, gpu = _rand_problem(5, 300, 64, 200, "bf16")
+    x = dev_tensor(draw(2, 64, scale=1.0))
+    good = [np.array([1, 5, 9], np.int32), np.array([0, 199], np.int32)]
+    off, idx = csr_from_sets(good)
+    y = si.selective_ffn(x, dev_tensor(off), dev_tensor(idx), gpu.gate_up_c, gpu.down_c,
+                         flags=si.FLAG_CHECK)
+    assert max_rel_l2(host_array(y), _oracle(host_array(x), good, ref)) <= TOL["bf16"]
+    cases = {
+        3: [np.array([1, 5, 1], np.int32), np.array([2], np.int32)],      # duplicate
+        2: [np.array([1, 200], np.int32), np.array([2], np.int32)],       # slot out of range
+    }
+    for code, sets in cases.items():
+        off, idx = csr_from_sets(sets)
+        with pytest.raises(si.SelectInferError) as e:
+            si.selective_ffn(x, dev_tensor(off), dev_tensor(idx), gpu.gate_up_c, gpu.down_c,
+                             flags=si.FLAG_CHECK)
+        assert e.value.status == code
+    bad_off = dev_tensor(np.array([0, 3, 2], np.int32))
+    with pytest.raises(si.SelectInferError) as e:
+        si.selective_ffn(x, bad_off, dev_tensor(np.array([1, 2, 3], np.int32)), gpu.gate_up_c,
+                         gpu.down_c, flags=si.FLAG_CHECK)
+    assert e.value.status == 2
+    # without the check, out-of-range slots are skipped (never read)
+    off, idx = csr_from_sets([np.array([1, 100000, 5, -3], np.int32), np.array([7], np.int32)])
+    y = host_array(si.selective_ffn(x, dev_tensor(off), dev_tensor(idx), gpu.gate_up_c,
+                                    gpu.down_c, flags=si.FLAG_PER_TOKEN))
+    want = _oracle(host_array(x), [np.array([1, 5]), np.array([7])], ref)
+    assert max_rel_l2(y, want) <= ALARM_PER_TOKEN
+    # too small a workspace is refused
+    off, idx = csr_from_sets(good)
+    with pytest.raises(si.SelectInferError) as e:
+        si.selective_ffn(x, dev_tensor(off), dev_tensor(idx), gpu.gate_up_c, gpu.down_c,
+                         workspace=torch.empty(16, dtype=torch.uint8, device="cuda:0"))
+    assert e.value.status == 7
+    # B = 0 and nnz = 0
+    e0 = si.selective_ffn(x[:0], dev_tensor(np.zeros(1, np.int32)), dev_tensor(np.zeros(0, np.int32)),
+                          gpu.gate_up_c, gpu.down_c)
+    assert e0.shape == (0, 64)
+    z = si.selective_ffn(x, dev_tensor(np.zeros(3, np.int32)), dev_tensor(np.zeros(0, np.int32)),
+                         gpu.gate_up_c, gpu.down_c)
+    assert not torch.any(z)
