@@ -1,0 +1,401 @@
+#!/usr/bin/env python3
+"""Benchmark of the selective-computation gated FFN on one MI355X.
+
+Default workload (the metric's configuration): a Llama-2-7B-shape FFN layer, bf16, d=4096,
+N=11008, 70% of neurons loaded (L=7706), 20% active per token (k=2202), batch-1 decode over a
+1024-token sequence. One step = one token through one compacted layer, i.e. one
+si_selective_ffn call. Inputs are seeded synthetic data resident in HBM before timing starts.
+
+Reported: tokens/s per layer (whole job, one GPU), and for the main weight-streaming kernel the
+achieved HBM bandwidth on the bytes the method touches (active rows x 3 matrices x d x 2 B),
+measured with HIP events around that kernel in every timed step, against the 8 TB/s peak.
+The oracle (fp64 NumPy, host) is timed on a bounded sample of the same workload.
+
+Other workloads (``--workload``) are available for measurement: tiny_f32, llama2_7b_b16
+(batch 16, union MFMA path), llama3_8b_stack (32 layers, residual RMSNorm between layers),
+llama2_13b_prefill (512 tokens, MFMA-bound union path).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "selective-FFN decode tokens/s per layer + achieved HBM GB/s vs MI355X peak"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+DEFAULT_WORKLOAD = "llama2_7b_decode"
+
+
+def parse_args():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None, help="timed steps (default: workload)")
+    ap.add_argument("--warmup", type=int, default=64)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--copies", type=int, default=32,
+                    help="resident copies of the compacted layer, rotated per step so that a "
+                         "repeated step cannot be served from the 256 MB Infinity Cache")
+    ap.add_argument("--no-graph", action="store_true", help="launch steps eagerly")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--timed-launches", type=int, default=256,
+                    help="steps whose main kernel is timed with HIP events")
+    return ap.parse_args()
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+# --------------------------------------------------------------------------------------------
+class Workload:
+    """Device state and step launchers of one workload."""
+
+    def __init__(self, cfg, copies, dev):
+        import numpy as np
+        import torch
+
+        import paper_2607_18081_amd as si
+        from workloads import active_sets, csr_from_sets, layer_weights, loaded_ids, tokens_x
+
+        self.cfg = cfg
+        self.dev = dev
+        self.si = si
+        self.np = np
+        self.torch = torch
+        self.layers = []          # per layer: list of resident copies (CompactLayer)
+        self.host = []            # per layer: (w_gate, w_up, w_down, loaded) on the host
+        nlay = cfg.layers
+        ncopy = copies if nlay == 1 else 1
+        T = cfg.steps * cfg.B
+        self.T = T
+        t0 = time.time()
+        for lay in range(nlay):
+            wg, wu, wd = layer_weights(cfg, lay)
+            loaded = loaded_ids(cfg, lay)
+            c0 = si.compact_ffn(self._dev(wg), self._dev(wu), self._dev(wd),
+                                torch.from_numpy(loaded))
+            cps = [c0]
+            for _ in range(ncopy - 1):
+                cps.append(si.CompactLayer(c0.gate_up_c.clone(), c0.down_c.clone(),
+                                           c0.slot_to_orig, c0.orig_to_slot))
+            self.layers.append(cps)
+            self.host.append((wg, wu, wd, loaded) if lay < 2 else None)
+            torch.cuda.synchronize()
+        log(f"{nlay} layer(s) x {ncopy} copies compacted in {time.time() - t0:.1f}s")
+        xt = tokens_x(cfg, range(T))
+        self.x_host = xt
+        self.x = self._dev(xt)
+        self.sets_host = []
+        self.off, self.slots = [], []
+        for lay in range(nlay):
+            sets = active_sets(cfg, range(T), lay)
+            off, ids = csr_from_sets(sets)
+            self.sets_host.append(sets if lay < 2 else None)
+            self.off.append(self._dev(off))
+            self.slots.append(si.remap_ids(self.layers[lay][0].orig_to_slot, self._dev(ids),
+                                           check=True))
+        self.y = torch.empty((T, cfg.d), dtype=torch.float32, device=dev)
+        if nlay > 1:
+            self.xbuf = [torch.empty((1, cfg.d), dtype=self.x.dtype, device=dev) for _ in range(2)]
+        B = cfg.B
+        need = max(si.selective_ffn_workspace(B, self.slots[l].numel(), cfg.L, cfg.d,
+                                              si.BF16 if cfg.wdtype == "bf16" else si.F32,
+                                              si.BF16 if cfg.wdtype == "bf16" else si.F32)
+                   for l in range(nlay))
+        self.ws = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+        self.union_rows = None
+        if B > 1:
+            # rows each step reads once: the union of its tokens' active sets
+            self.union_rows = []
+            for s in range(cfg.steps):
+                u = np.unique(np.concatenate(
+                    [self.sets_host[0][t] for t in range(s * B, (s + 1) * B)]))
+                self.union_rows.append(len(u))
+
+    def _dev(self, a):
+        a = self.np.ascontiguousarray(a)
+        if a.dtype == self.np.uint16:
+            return self.torch.from_numpy(a.view(self.np.int16)).to(self.dev).view(
+                self.torch.bfloat16)
+        return self.torch.from_numpy(a).to(self.dev)
+
+    @property
+    def steps_in_sequence(self):
+        return self.cfg.steps
+
+    def launch(self, step, timing=None):
+        """Enqueue step `step` (mod the workload length); `timing` = list of event pairs, one
+        per layer, to bracket the main kernel."""
+        si, cfg = self.si, self.cfg
+        s = step % self.cfg.steps
+        B = cfg.B
+        t0 = s * B
+        if cfg.layers == 1:
+            cp = self.layers[0][step % len(self.layers[0])]
+            if timing:
+                si.set_timing_events(*timing[0])
+            si.selective_ffn(self.x[t0:t0 + B], self.off[0][t0:t0 + B + 1], self.slots[0],
+                             cp.gate_up_c, cp.down_c, y=self.y[t0:t0 + B], workspace=self.ws)
+        else:
+            xin = self.x[t0:t0 + 1]
+            for lay in range(cfg.layers):
+                cp = self.layers[lay][0]
+                if timing:
+                    si.set_timing_events(*timing[lay])
+                y = self.y[t0:t0 + 1]
+                si.selective_ffn(xin, self.off[lay][t0:t0 + 2], self.slots[lay], cp.gate_up_c,
+                                 cp.down_c, y=y, workspace=self.ws)
+                if timing:
+                    si.set_timing_events(None, None)
+                xout = self.xbuf[lay % 2]
+                si.residual_rmsnorm(xin, y, out=xout)
+                xin = xout
+        if timing:
+            si.set_timing_events(None, None)
+
+    # work of one main-kernel launch ------------------------------------------------------
+    def row_bytes(self):
+        return 3 * self.cfg.d * (2 if self.cfg.wdtype == "bf16" else 4)
+
+    def launch_bytes(self, step):
+        """Algorithmic HBM bytes of the main kernel(s) of one launch: rows read x 3 x d x s."""
+        cfg = self.cfg
+        rows = cfg.k if cfg.B == 1 else self.union_rows[step % cfg.steps]
+        return rows * self.row_bytes()
+
+    def launch_flops(self, step):
+        """Dense-over-union MFMA flops of one union launch (GEMM1 2x and GEMM2 1x)."""
+        cfg = self.cfg
+        rows = self.union_rows[step % cfg.steps]
+        return 2.0 * 3 * cfg.B * rows * cfg.d
+
+
+# --------------------------------------------------------------------------------------------
+def run_gpu(work, steps, warmup, use_graph, timed_launches):
+    """Warm up, time `steps` steps (one HIP graph replay, or eager launches), then time the
+    main kernel of up to `timed_launches` steps with HIP events.
+
+    Event records inside a replayed graph do not bracket kernels on ROCm, so the kernel
+    durations come from an eager pass over the same steps. That pass is queued behind a short
+    device-side sleep, so every launch is already queued when the GPU reaches it and the events
+    measure device time only.
+    """
+    import torch
+
+    cfg = work.cfg
+    nlay = cfg.layers
+    for i in range(warmup):
+        work.launch(i)
+    torch.cuda.synchronize()
+
+    def enqueue_all():
+        for i in range(steps):
+            work.launch(warmup + i)
+
+    graph = None
+    if use_graph:
+        try:
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph):
+                enqueue_all()
+            graph.replay()          # upload and first run, untimed
+            torch.cuda.synchronize()
+        except Exception as e:      # capture unsupported here: fall back to eager launches
+            log(f"graph capture failed ({e!r}); timing eager launches")
+            graph = None
+            torch.cuda.synchronize()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    if graph is not None:
+        graph.replay()
+    else:
+        enqueue_all()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    # main-kernel durations, measured with HIP events on the launch stream
+    n = min(steps, timed_launches)
+    evs = []
+    for _ in range(n * nlay):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        b.record()
+        evs.append((a, b))
+    torch.cuda.synchronize()
+    try:
+        torch.cuda._sleep(int(50e6))  # ~20 ms: lets the host queue the whole pass first
+    except (AttributeError, RuntimeError):
+        log("no device sleep available: kernel timings may include launch latency")
+    for i in range(n):
+        work.launch(warmup + i, timing=evs[i * nlay:(i + 1) * nlay])
+    torch.cuda.synchronize()
+    kern_ms = [a.elapsed_time(b) for a, b in evs]
+    return wall, kern_ms, graph is not None, list(range(warmup, warmup + n))
+
+
+def check_outputs(work, tokens):
+    """Recompute a few timed tokens with the oracle and return the worst relative L2."""
+    import numpy as np
+
+    import oracle
+
+    cfg = work.cfg
+    if cfg.layers > 1:
+        return None
+    wg, wu, wd, loaded = work.host[0]
+    ref = oracle.compact(wg, wu, wd, loaded)
+    y = work.y.cpu().numpy()
+    worst = 0.0
+    for t in tokens:
+        slots = oracle.remap(ref["orig_to_slot"], work.sets_host[0][t])
+        want = oracle.selective_ffn(work.x_host[t], slots, ref["gate_up_c"], ref["down_c"])
+        err = float(np.linalg.norm(y[t] - want) / max(np.linalg.norm(want), 1e-300))
+        worst = max(worst, err)
+    return worst, ref
+
+
+def cpu_baseline(work, ref, seconds):
+    """Time the oracle (as is) on the host, one token at a time, for about `seconds`."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    import oracle
+
+    cfg = work.cfg
+    n = 0
+    with threadpool_limits(limits=1):
+        t0 = time.perf_counter()
+        while n < work.T and time.perf_counter() - t0 < seconds:
+            slots = oracle.remap(ref["orig_to_slot"], work.sets_host[0][n])
+            oracle.selective_ffn(work.x_host[n], slots, ref["gate_up_c"], ref["down_c"])
+            n += 1
+        el = time.perf_counter() - t0
+    return {
+        "value": n / el,
+        "unit": "tokens/s/layer",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": f"first {n} of the workload's {work.T} tokens, one si_selective_ffn-equivalent "
+                  f"oracle call each (id remap + fp64 NumPy selective FFN), single thread, "
+                  f"{el:.1f} s on {os.cpu_count()} visible host CPUs",
+    }
+
+
+def traffic_record(workload):
+    """HBM traffic per launch from committed rocprofv3 counter runs, if taken on this source."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path))
+        src = os.path.join(ROOT, "paper_2607_18081_amd", "csrc", rec["kernel_source"])
+        h = hashlib.sha256(open(src, "rb").read()).hexdigest()
+        return rec["bytes_per_launch"] if h == rec["source_sha256"] else None
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+KERNEL_SOURCE = {"llama2_7b_decode": "k_decode.hip", "tiny_f32": "k_decode.hip",
+                 "llama3_8b_stack": "k_decode.hip", "llama2_7b_b16": "k_union.hip",
+                 "llama2_13b_prefill": "k_union.hip"}
+
+
+def main():
+    args = parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; the multi-GPU sharding "
+                                   "of the path is a design (see DESIGN.md), not an executable "
+                                   "path", "n_gpus": args.gpus}))
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from workloads import CONFIGS
+
+    cfg = CONFIGS[args.workload]
+    steps = args.steps if args.steps is not None else (
+        cfg.steps if cfg.B == 1 and cfg.layers == 1 else (64 if cfg.layers > 1 else
+                                                          max(cfg.steps, 16)))
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    log(f"workload {cfg.name}: d={cfg.d} N={cfg.N} L={cfg.L} k={cfg.k} B={cfg.B} "
+        f"layers={cfg.layers} {cfg.wdtype}; steps={steps} warmup={args.warmup}")
+    work = Workload(cfg, args.copies, dev)
+    wall, kern_ms, graphed, launches = run_gpu(work, steps, args.warmup, not args.no_graph,
+                                               args.timed_launches)
+    nlay = cfg.layers
+    tokens = steps * cfg.B
+    value = tokens * nlay / wall                     # tokens/s per layer
+    ms_per_step = wall * 1e3 / steps
+    kern_ms = np.array(kern_ms)
+    # a union launch does 2*3*B flops per weight byte; above the MFMA/HBM ridge
+    # (2500 TFLOP/s / 8 TB/s = 312) it is bound by the matrix cores
+    if cfg.layers == 1 and cfg.B > MFMA_BF16_PEAK_TFLOPS / HBM_PEAK_GBS * 1e3:
+        flops = np.mean([work.launch_flops(i) for i in launches])
+        achieved = flops / (kern_ms.mean() * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": MFMA_BF16_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": None}
+    else:
+        byts = np.mean([work.launch_bytes(i) for i in launches])
+        achieved = byts / (kern_ms.mean() * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": achieved / HBM_PEAK_GBS, "traffic": traffic_record(cfg.name)}
+    roof["kernel_ms_mean"] = float(kern_ms.mean())
+    roof["kernel_ms_p50"] = float(np.median(kern_ms))
+    roof["kernel_launches_timed"] = int(len(kern_ms))
+    roof["bytes_per_launch" if roof["bound"] == "hbm" else "flops_per_launch"] = float(
+        np.mean([work.launch_bytes(i) if roof["bound"] == "hbm" else work.launch_flops(i)
+                 for i in launches]))
+
+    parity = None
+    cpu = None
+    if cfg.layers == 1:
+        last = (args.warmup + steps - 1) % cfg.steps
+        check_toks = sorted({last * cfg.B, last * cfg.B + cfg.B - 1})
+        worst, ref = check_outputs(work, check_toks)
+        tol = 5e-3 if cfg.wdtype == "bf16" else 1e-5
+        parity = {"tokens_checked": check_toks, "max_rel_l2": worst, "tol": tol}
+        if worst > tol:
+            log(f"PARITY FAILURE: rel L2 {worst:.3e} > {tol}")
+            sys.exit(1)
+        if not args.no_cpu_baseline:
+            cpu = cpu_baseline(work, ref, args.cpu_seconds)
+
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "tokens/s/layer",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.wdtype,
+        "data": "synthetic (seeded; weights N(0,0.02), x N(0,1), Zipf(1.1) popularity)",
+        "config": {"workload": cfg.name, "d": cfg.d, "N": cfg.N, "loaded": cfg.L,
+                   "active": cfg.k, "batch": cfg.B, "layers": cfg.layers,
+                   "tokens_per_step": cfg.B, "sequence_tokens": cfg.steps * cfg.B,
+                   "weight_copies": len(work.layers[0]), "hip_graph": graphed,
+                   "parallelism": "single GPU"},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "parity": parity,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

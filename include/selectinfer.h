@@ -158,6 +158,21 @@ int si_selective_ffn(const void* x, si_dtype xdt, int64_t B, int64_t d,
                      float* y, void* ws, size_t ws_bytes, int flags, void* hip_stream);
 
 /*
+ * Instrumentation: time the main kernel of si_selective_ffn with caller-owned HIP events.
+ *
+ *   start, stop: hipEvent_t handles (created with timing enabled), or both NULL to stop.
+ *
+ * The setting belongs to the calling host thread. While set, every si_selective_ffn call from
+ * that thread launches its weight-streaming kernels with these events attached to their
+ * dispatch (hipExtLaunchKernelGGL): `start` takes the start time of the first of them and
+ * `stop` the end time of the last (per-token path: the gather-GEMV kernel; union path: GEMM1
+ * through GEMM2), so hipEventElapsedTime(start, stop) is their device time, without queueing
+ * or marker overheads. Meant for eager timing runs, not for graph capture. Returns
+ * SI_ERR_INVALID if exactly one of the two is NULL.
+ */
+int si_set_timing_events(void* start, void* stop);
+
+/*
  * Layer step of a stacked FFN: x_out[b] = RMSNorm(x[b] + y[b]) with unit gain,
  * r / sqrt(mean(r^2) + eps), computed in float32 and stored in xdt (bf16: round to nearest
  * even). x [B][d] (xdt), y [B][d] float32, x_out [B][d] (xdt); x_out may alias x.

@@ -19,5 +19,6 @@ from .api import (  # noqa: F401
     select_topk,
     selective_ffn,
     selective_ffn_workspace,
+    set_timing_events,
     version,
 )

@@ -175,6 +175,17 @@ def selective_ffn(x: torch.Tensor, offsets: torch.Tensor, idx: torch.Tensor,
     return y
 
 
+def set_timing_events(start: "torch.cuda.Event | None", stop: "torch.cuda.Event | None") -> None:
+    """si_set_timing_events: bracket the main kernel of later selective_ffn calls on this thread.
+
+    Events must have timing enabled and must already exist on the device (torch creates them
+    lazily: record each once before passing it). Pass None, None to stop.
+    """
+    h0 = None if start is None else start.cuda_event
+    h1 = None if stop is None else stop.cuda_event
+    _check(load().si_set_timing_events(h0, h1), "si_set_timing_events")
+
+
 def residual_rmsnorm(x: torch.Tensor, y: torch.Tensor, eps: float = 1e-5,
                      out: torch.Tensor | None = None) -> torch.Tensor:
     """si_residual_rmsnorm: RMSNorm(x + y), unit gain, stored in x's dtype."""

@@ -65,14 +65,18 @@ int checked(hipStream_t s, int dev, F enqueue) {
     return host[0];
 }
 
+// per host thread: events bracketing the main kernel of si_selective_ffn
+thread_local hipEvent_t t_ev_start = nullptr;
+thread_local hipEvent_t t_ev_stop = nullptr;
+
 bool valid_dtype(int t) { return t == SI_F32 || t == SI_BF16; }
 
-bool use_union(int64_t B, int64_t L, si_dtype xdt, si_dtype wdt, int flags) {
+bool use_union(int64_t B, int64_t L, int64_t d, si_dtype xdt, si_dtype wdt, int flags) {
     // Reading the union once costs |U| rows instead of nnz >= |U|, and the dense-over-union
     // MFMA work stays far below the HBM time of those rows for any overlap (see the design
     // notes), so B >= 2 always takes it when the dtypes allow bf16 MFMA.
     return B >= 2 && xdt == SI_BF16 && wdt == SI_BF16 && !(flags & SI_FLAG_PER_TOKEN) &&
-           L <= 524288;
+           si::union_supported(B, L, d);
 }
 
 }  // namespace
@@ -151,7 +155,7 @@ size_t si_selective_ffn_workspace(int64_t B, int64_t nnz, int64_t L, int64_t d, 
     if (B <= 0 || d <= 0 || L <= 0 || nnz < 0) return 0;
     const int dev = current_device();
     const int ncu = dev < 0 ? 256 : num_cu(dev);
-    if (use_union(B, L, xdt, wdt, flags)) return si::union_workspace(B, L, d, ncu);
+    if (use_union(B, L, d, xdt, wdt, flags)) return si::union_workspace(B, L, d, ncu);
     const int P = si::decode_chunks(B, nnz, ncu);
     return (size_t)B * P * d * sizeof(float);
 }
@@ -182,12 +186,19 @@ int si_selective_ffn(const void* x, si_dtype xdt, int64_t B, int64_t d, const in
         if (st != SI_OK) return st;
     }
     const int ncu = num_cu(dev);
-    if (use_union(B, L, xdt, wdt, flags))
+    if (use_union(B, L, d, xdt, wdt, flags))
         return from_hip(si::launch_union(x, B, d, offsets, idx, nnz, gate_up_c, down_c, L, y, ws,
-                                         flags, ncu, s));
+                                         flags, ncu, s, t_ev_start, t_ev_stop));
     const int P = si::decode_chunks(B, nnz, ncu);
     return from_hip(si::launch_decode(x, xdt, B, d, offsets, idx, nnz, gate_up_c, down_c, L, wdt,
-                                      static_cast<float*>(ws), P, y, s));
+                                      static_cast<float*>(ws), P, y, s, t_ev_start, t_ev_stop));
+}
+
+int si_set_timing_events(void* start, void* stop) {
+    if ((start == nullptr) != (stop == nullptr)) return SI_ERR_INVALID;
+    t_ev_start = static_cast<hipEvent_t>(start);
+    t_ev_stop = static_cast<hipEvent_t>(stop);
+    return SI_OK;
 }
 
 int si_residual_rmsnorm(const void* x, si_dtype xdt, const float* y, int64_t B, int64_t d,

@@ -48,6 +48,28 @@ __device__ __forceinline__ void st16(void* p, const V16& v) {
     *reinterpret_cast<V16*>(p) = v;
 }
 
+// Raw buffer loads (gfx9 buffer descriptors). The descriptor's range check returns zeros, and
+// reads no memory, for a byte offset outside the buffer: kernels pass kOOB for rows or columns
+// that must contribute nothing, so loads need no branches. Offsets are 32-bit, so a buffer
+// read this way must be smaller than 2 GiB.
+typedef __attribute__((ext_vector_type(4))) int i32x4_t;
+constexpr int kOOB = (int)0x80000000;
+constexpr int kBufWord3 = 0x00020000;  // dword 3 of a raw gfx9 descriptor: 32-bit data format
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, kBufWord3);
+}
+
+__device__ __forceinline__ V16 bload16(__amdgpu_buffer_rsrc_t r, int off) {
+    const i32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+    V16 o;
+    o.w[0] = (uint32_t)v[0];
+    o.w[1] = (uint32_t)v[1];
+    o.w[2] = (uint32_t)v[2];
+    o.w[3] = (uint32_t)v[3];
+    return o;
+}
+
 // Unpack a 16-byte vector into V floats (V = 8 for bf16, 4 for f32).
 template <typename T>
 struct Elem;
@@ -72,7 +94,7 @@ struct Elem<bf16_t> {
 };
 
 // SiLU(g) = g * sigmoid(g), float32
-__device__ __forceinline__ float silu_f32(float g) { return g / (1.0f + __expf(-g)); }
+__device__ __forceinline__ float silu_f32(float g) { return __fdividef(g, 1.0f + __expf(-g)); }
 
 // Sum over the 64 lanes of a wave; every lane receives the total.
 __device__ __forceinline__ float wave_sum(float v) {
@@ -82,32 +104,40 @@ __device__ __forceinline__ float wave_sum(float v) {
 }
 
 // Reduce NVAL per-lane values across the wave at once. On return, lane l holds the wave total
-// of value index l / (64 / NVAL). NVAL is a power of two, 1 <= NVAL <= 64. Costs
-// NVAL - 1 + log2(64 / NVAL) shuffles instead of 6 * NVAL.
+// of value index l / (64 / NVAL). NVAL is a power of two, 1 <= NVAL <= 64. Each step pairs the
+// lanes that differ in one lane-id bit: the lower lane keeps the lower half of its values, the
+// upper lane the upper half, and each adds its partner's copy of the half it keeps. Costs
+// NVAL - 1 + log2(64 / NVAL) shuffles instead of 6 * NVAL. All indices are compile-time.
+template <int CNT, int MASK>
+struct TransposeSum {
+    __device__ __forceinline__ static void run(float* v, int lane) {
+        constexpr int half = CNT / 2;
+        const bool upper = (lane & MASK) != 0;
+#pragma unroll
+        for (int m = 0; m < half; ++m) {
+            const float send = upper ? v[m] : v[m + half];
+            const float keep = upper ? v[m + half] : v[m];
+            v[m] = keep + __shfl_xor(send, MASK, kWave);
+        }
+        TransposeSum<half, MASK / 2>::run(v, lane);
+    }
+};
+template <int MASK>
+struct TransposeSum<1, MASK> {
+    __device__ __forceinline__ static void run(float* v, int lane) {
+        v[0] += __shfl_xor(v[0], MASK, kWave);
+        TransposeSum<1, MASK / 2>::run(v, lane);
+    }
+};
+template <>
+struct TransposeSum<1, 0> {
+    __device__ __forceinline__ static void run(float*, int) {}
+};
+
 template <int NVAL>
 __device__ __forceinline__ float wave_transpose_sum(float (&v)[NVAL], int lane) {
     static_assert((NVAL & (NVAL - 1)) == 0 && NVAL >= 1 && NVAL <= 64, "NVAL");
-    int cnt = NVAL;
-    int mask = 32;
-#pragma unroll
-    for (int step = 0; step < 6; ++step) {
-        if (cnt > 1) {
-            const int half = cnt >> 1;
-            const bool upper = (lane & mask) != 0;
-#pragma unroll
-            for (int m = 0; m < NVAL / 2; ++m) {
-                if (m < half) {
-                    float send = upper ? v[m] : v[m + half];
-                    float keep = upper ? v[m + half] : v[m];
-                    v[m] = keep + __shfl_xor(send, mask, kWave);
-                }
-            }
-            cnt = half;
-        } else {
-            v[0] += __shfl_xor(v[0], mask, kWave);
-        }
-        mask >>= 1;
-    }
+    TransposeSum<NVAL, 32>::run(v, lane);
     return v[0];
 }
 

@@ -14,6 +14,8 @@
 //
 // Kernel 2 (reduce_partials) adds the P partial rows of each token in a fixed order, so the
 // result is deterministic and no global atomics are used.
+#include <hip/hip_ext.h>
+
 #include "common.h"
 #include "launch.h"
 
@@ -26,7 +28,7 @@ constexpr int kThreads = kWaves * kWave;
 
 template <int NI>
 struct RowsPerBatch {
-    static constexpr int value = NI == 1 ? 8 : NI == 2 ? 4 : 2;
+    static constexpr int value = NI == 1 ? 16 : NI == 2 ? 8 : NI == 3 ? 4 : 2;
 };
 
 typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
@@ -69,7 +71,54 @@ struct XSlice<bf16_t, bf16_t> {
     }
 };
 
-template <typename WT, typename XT, int NI>
+// Row loads of the gather-GEMV. BUF: buffer loads with range-checked 32-bit offsets (no
+// branches; the compacted tensors must be smaller than 2 GiB); else guarded global loads.
+template <typename WT, bool BUF>
+struct RowLoader;
+
+template <typename WT>
+struct RowLoader<WT, true> {
+    __amdgpu_buffer_rsrc_t rg, rd;
+    int64_t d;
+    __device__ __forceinline__ RowLoader(const WT* gu, const WT* dc, int64_t L, int64_t d_)
+        : d(d_) {
+        rg = make_rsrc(gu, L * 2 * d_ * (int64_t)sizeof(WT));
+        rd = make_rsrc(dc, L * d_ * (int64_t)sizeof(WT));
+    }
+    __device__ __forceinline__ void load(bool ok, int32_t j, int64_t col, V16& g, V16& u,
+                                         V16& dn) const {
+        const int og = ok ? (int)(((int64_t)j * 2 * d + col) * sizeof(WT)) : kOOB;
+        const int od = ok ? (int)(((int64_t)j * d + col) * sizeof(WT)) : kOOB;
+        g = bload16(rg, og);
+        u = bload16(rg, ok ? og + (int)(d * sizeof(WT)) : kOOB);
+        dn = bload16(rd, od);
+    }
+};
+
+template <typename WT>
+struct RowLoader<WT, false> {
+    const WT* gu;
+    const WT* dc;
+    int64_t d;
+    __device__ __forceinline__ RowLoader(const WT* gu_, const WT* dc_, int64_t, int64_t d_)
+        : gu(gu_), dc(dc_), d(d_) {}
+    __device__ __forceinline__ void load(bool ok, int32_t j, int64_t col, V16& g, V16& u,
+                                         V16& dn) const {
+        const V16 z = V16{{0u, 0u, 0u, 0u}};
+        if (ok) {
+            const WT* gp = gu + (int64_t)j * 2 * d + col;
+            g = ld16(gp);
+            u = ld16(gp + d);
+            dn = ld16(dc + (int64_t)j * d + col);
+        } else {
+            g = z;
+            u = z;
+            dn = z;
+        }
+    }
+};
+
+template <typename WT, typename XT, int NI, bool BUF>
 __global__ __launch_bounds__(kThreads) void sffn_rows(
     const XT* __restrict__ x, int64_t d, const int32_t* __restrict__ offsets,
     const int32_t* __restrict__ idx, int64_t nnz, const WT* __restrict__ gate_up_c,
@@ -104,37 +153,20 @@ __global__ __launch_bounds__(kThreads) void sffn_rows(
 #pragma unroll
         for (int e = 0; e < V; ++e) acc[i][e] = 0.0f;
     }
+    const RowLoader<WT, BUF> ldr(gate_up_c, down_c, L, d);
 
     __shared__ float red[2][NVAL][kWaves];
     int buf = 0;
-    const int64_t two_d = 2 * d;
-
     for (int64_t rb = r0; rb < r1; rb += R) {
         const int nr = (int)((r1 - rb) < R ? (r1 - rb) : R);
-        int32_t j[R];
-        bool ok[R];
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-            const int32_t s = r < nr ? idx[rb + r] : -1;
-            ok[r] = (s >= 0) && (s < L);
-            j[r] = ok[r] ? s : 0;
-        }
         V16 gv[R][NI], uv[R][NI], dv[R][NI];
 #pragma unroll
         for (int r = 0; r < R; ++r) {
+            // wave-uniform slot id: the row base stays in scalar registers
+            const int32_t s = __builtin_amdgcn_readfirstlane(r < nr ? idx[rb + r] : -1);
+            const bool ok = (s >= 0) && (s < L);
 #pragma unroll
-            for (int i = 0; i < NI; ++i) {
-                if (ok[r] && cok[i]) {
-                    const WT* gp = gate_up_c + (int64_t)j[r] * two_d + col[i];
-                    gv[r][i] = ld16(gp);
-                    uv[r][i] = ld16(gp + d);
-                    dv[r][i] = ld16(down_c + (int64_t)j[r] * d + col[i]);
-                } else {
-                    gv[r][i] = V16{{0u, 0u, 0u, 0u}};
-                    uv[r][i] = V16{{0u, 0u, 0u, 0u}};
-                    dv[r][i] = V16{{0u, 0u, 0u, 0u}};
-                }
-            }
+            for (int i = 0; i < NI; ++i) ldr.load(ok && cok[i], s, col[i], gv[r][i], uv[r][i], dv[r][i]);
         }
         float vals[NVAL];
 #pragma unroll
@@ -148,19 +180,23 @@ __global__ __launch_bounds__(kThreads) void sffn_rows(
             vals[r] = g;
             vals[R + r] = u;
         }
+        // lane l: this wave's total of value l / PER; then the 8 waves meet in LDS
         const float tot = wave_transpose_sum<NVAL>(vals, lane);
         if ((lane % PER) == 0) red[buf][lane / PER][w] = tot;
         __syncthreads();
+        // lane r < R holds g_r, lane R + r holds u_r (summed over waves in a fixed order)
+        float t = 0.0f;
+        if (lane < NVAL) {
+#pragma unroll
+            for (int q = 0; q < kWaves; ++q) t += red[buf][lane][q];
+        }
+        const float uu = __shfl_down(t, R, kWave);
+        const float hv = silu_f32(t) * uu;  // valid in lanes 0 .. R-1
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             if (r < nr) {
-                float g = 0.0f, u = 0.0f;
-#pragma unroll
-                for (int q = 0; q < kWaves; ++q) {
-                    g += red[buf][r][q];
-                    u += red[buf][R + r][q];
-                }
-                const float h = silu_f32(g) * u;
+                const float h = __builtin_bit_cast(
+                    float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, hv), r));
 #pragma unroll
                 for (int i = 0; i < NI; ++i) {
                     float df[V];
@@ -190,48 +226,49 @@ __global__ __launch_bounds__(kThreads) void sffn_rows(
     }
 }
 
-// y[b][c] = sum_{p = 0..P-1} partials[b][p][c], fixed order. Work-group: 32 columns (8 float4
-// groups) x 32 lanes over p; lane (pg, cg) sums p = pg, pg + 32, ...; then a fixed LDS tree.
+// y[b][c] = sum_{p = 0..P-1} partials[b][p][c] in a fixed order. One wave per 4 columns (a
+// float4 group): lane l adds p = l, l + 64, ... in order, then a fixed transposing shuffle tree
+// leaves column c + l/16 in lanes 16*(l/16). No LDS, no barrier.
 __global__ __launch_bounds__(256) void reduce_partials(const float* __restrict__ partials, int P,
                                                        int64_t d, float* __restrict__ y) {
-    const int cg = threadIdx.x & 7;
-    const int pg = threadIdx.x >> 3;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t c = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * 4;
     const int b = blockIdx.y;
-    const int64_t c = (int64_t)blockIdx.x * 32 + cg * 4;
-    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (c < d) {
-        const float* base = partials + (int64_t)b * P * d + c;
-        for (int p = pg; p < P; p += 32) {
-            const float4 v = *reinterpret_cast<const float4*>(base + (int64_t)p * d);
-            s.x += v.x;
-            s.y += v.y;
-            s.z += v.z;
-            s.w += v.w;
-        }
-    }
-    __shared__ float4 sh[32][8];
-    sh[pg][cg] = s;
-    __syncthreads();
+    if (c >= d) return;
+    const float* base = partials + (int64_t)b * P * d + c;
+    float4 v[4];
 #pragma unroll
-    for (int st = 16; st >= 1; st >>= 1) {
-        if (pg < st) {
-            float4 a = sh[pg][cg];
-            const float4 o = sh[pg + st][cg];
-            a.x += o.x;
-            a.y += o.y;
-            a.z += o.z;
-            a.w += o.w;
-            sh[pg][cg] = a;
-        }
-        __syncthreads();
+    for (int q = 0; q < 4; ++q) {
+        const int pp = lane + kWave * q;
+        v[q] = pp < P ? *reinterpret_cast<const float4*>(base + (int64_t)pp * d)
+                      : make_float4(0.f, 0.f, 0.f, 0.f);
     }
-    if (pg == 0 && c < d) *reinterpret_cast<float4*>(y + (int64_t)b * d + c) = sh[0][cg];
+    float s[4] = {v[0].x, v[0].y, v[0].z, v[0].w};
+#pragma unroll
+    for (int q = 1; q < 4; ++q) {
+        s[0] += v[q].x;
+        s[1] += v[q].y;
+        s[2] += v[q].z;
+        s[3] += v[q].w;
+    }
+    for (int pp = lane + 4 * kWave; pp < P; pp += kWave) {
+        const float4 t = *reinterpret_cast<const float4*>(base + (int64_t)pp * d);
+        s[0] += t.x;
+        s[1] += t.y;
+        s[2] += t.z;
+        s[3] += t.w;
+    }
+    const float tot = wave_transpose_sum<4>(s, lane);
+    if ((lane & 15) == 0) y[(int64_t)b * d + c + (lane >> 4)] = tot;
 }
 
-template <typename WT, typename XT>
+// ev0/ev1 (optional): stamped from the kernel's own dispatch (hipExtLaunchKernelGGL), so
+// their elapsed time is the kernel's device time without queueing or marker overheads.
+template <typename WT, typename XT, bool BUF>
 hipError_t launch_rows_t(const void* x, int64_t B, int64_t d, const int32_t* offsets,
                          const int32_t* idx, int64_t nnz, const void* gu, const void* dc,
-                         int64_t L, float* partials, int P, hipStream_t s) {
+                         int64_t L, float* partials, int P, hipStream_t s, hipEvent_t ev0,
+                         hipEvent_t ev1) {
     constexpr int V = Elem<WT>::V;
     const int64_t span = (int64_t)kThreads * V;
     const int ni = (int)((d + span - 1) / span);
@@ -242,8 +279,8 @@ hipError_t launch_rows_t(const void* x, int64_t B, int64_t d, const int32_t* off
     const WT* dn = static_cast<const WT*>(dc);
 #define SI_ROWS_CASE(N)                                                                        \
     case N:                                                                                    \
-        hipLaunchKernelGGL((sffn_rows<WT, XT, N>), grid, block, 0, s, xx, d, offsets, idx, nnz, \
-                           g, dn, L, partials, P);                                             \
+        hipExtLaunchKernelGGL((sffn_rows<WT, XT, N, BUF>), grid, block, 0, s, ev0, ev1, 0, xx, d, \
+                              offsets, idx, nnz, g, dn, L, partials, P);                       \
         break;
     switch (ni) {
         SI_ROWS_CASE(1)
@@ -280,21 +317,26 @@ int decode_chunks(int64_t B, int64_t nnz, int num_cu) {
 hipError_t launch_decode(const void* x, int xdt, int64_t B, int64_t d, const int32_t* offsets,
                          const int32_t* idx, int64_t nnz, const void* gate_up_c,
                          const void* down_c, int64_t L, int wdt, float* partials, int P,
-                         float* y, hipStream_t s) {
+                         float* y, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
     if (B == 0) return hipSuccess;
     hipError_t e;
+    // buffer loads take 32-bit byte offsets: both compacted tensors must stay below 2 GiB
+    const int64_t es = wdt == 1 ? 2 : 4;
+    const bool buf = L * 2 * d * es < ((int64_t)1 << 31);
+#define SI_DEC(WT, XT)                                                                        \
+    (buf ? launch_rows_t<WT, XT, true>(x, B, d, offsets, idx, nnz, gate_up_c, down_c, L,      \
+                                       partials, P, s, ev0, ev1)                              \
+         : launch_rows_t<WT, XT, false>(x, B, d, offsets, idx, nnz, gate_up_c, down_c, L,     \
+                                        partials, P, s, ev0, ev1))
     if (wdt == 1 && xdt == 1)
-        e = launch_rows_t<bf16_t, bf16_t>(x, B, d, offsets, idx, nnz, gate_up_c, down_c, L,
-                                          partials, P, s);
+        e = SI_DEC(bf16_t, bf16_t);
     else if (wdt == 1 && xdt == 0)
-        e = launch_rows_t<bf16_t, float>(x, B, d, offsets, idx, nnz, gate_up_c, down_c, L,
-                                         partials, P, s);
+        e = SI_DEC(bf16_t, float);
     else if (wdt == 0 && xdt == 1)
-        e = launch_rows_t<float, bf16_t>(x, B, d, offsets, idx, nnz, gate_up_c, down_c, L,
-                                         partials, P, s);
+        e = SI_DEC(float, bf16_t);
     else
-        e = launch_rows_t<float, float>(x, B, d, offsets, idx, nnz, gate_up_c, down_c, L,
-                                        partials, P, s);
+        e = SI_DEC(float, float);
+#undef SI_DEC
     if (e != hipSuccess) return e;
     return launch_reduce_partials(partials, P, B, d, y, s);
 }
@@ -302,7 +344,8 @@ hipError_t launch_decode(const void* x, int xdt, int64_t B, int64_t d, const int
 hipError_t launch_reduce_partials(const float* partials, int P, int64_t B, int64_t d, float* y,
                                   hipStream_t s) {
     if (B == 0) return hipSuccess;
-    dim3 grid((unsigned)((d + 31) / 32), (unsigned)B);
+    // one wave per float4 group, four waves per work-group
+    dim3 grid((unsigned)((d + 15) / 16), (unsigned)B);
     hipLaunchKernelGGL(reduce_partials, grid, dim3(256), 0, s, partials, P, d, y);
     return hipGetLastError();
 }

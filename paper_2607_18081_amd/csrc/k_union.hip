@@ -12,11 +12,24 @@
 // H enters GEMM2's bf16 MFMA as a pair hi = bf16(H), lo = bf16(H - hi), so the product keeps
 // about 16 significant bits of H (SI_FLAG_FAST_H uses hi only).
 //
-// Kernels: per-token bitmaps of the active slots; one work-group ORs them into the union and
-// lists its slots in ascending order; GEMM1 (v_mfma_f32_16x16x32_bf16, 16 tokens x 16 union
-// rows per work-group, K split over 4 waves and summed in LDS in a fixed order); GEMM2 (16*MT
-// tokens x 256 columns per work-group, down rows staged through LDS, K = union rows split in
-// KS chunks whose float32 partials are added in a fixed order by the decode path's reducer).
+// Kernels:
+//  - token bitmaps: one work-group per token marks its active slots in an L-bit bitmap;
+//  - GEMM1 (v_mfma_f32_16x16x32_bf16): one work-group per 32-slot bitmap word and 16 x MT1
+//    tokens. It ORs the word over the batch (the union's slots in this word), takes those rows
+//    as two 16-row MFMA tiles (slots outside the union load nothing: their loads are out of
+//    range), splits K over 8 waves that meet in LDS in a fixed order, and writes H by slot,
+//    zero for slots outside the union. Within a K block of 128, the lanes of group g feed
+//    elements 32 e + 8 g .. +7 to MFMA e, so one load instruction covers 64 contiguous bytes
+//    of each row; the token operand uses the same K permutation, so the sum is unchanged.
+//    The y = 0 work-groups also publish the union word for GEMM2;
+//  - GEMM2: a work-group takes 16 x MT tokens, 256 columns and one of KS chunks of bitmap
+//    words, with K = slot: each non-empty word is one K step of 32 slots whose down rows (zero
+//    rows outside the union, again without memory traffic) are staged in LDS, double buffered
+//    with three tiles in flight, and read back transposed into the MFMA B-operand layout with
+//    ds_read_b64_tr_b16. The KS float32 partials are added in a fixed order by the shared
+//    partial reducer.
+#include <hip/hip_ext.h>
+
 #include "common.h"
 #include "launch.h"
 
@@ -25,6 +38,7 @@ namespace si {
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
 typedef __attribute__((ext_vector_type(4))) float f32x4_t;
 typedef __attribute__((ext_vector_type(4))) unsigned int u32x4_t;
+typedef __attribute__((ext_vector_type(4))) short s16x4_t;
 
 namespace {
 
@@ -38,12 +52,17 @@ __device__ __forceinline__ f32x4_t mfma16x16x32(const bf16x8_t& a, const bf16x8_
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
+constexpr int kG2Cols = 256;               // GEMM2 columns per work-group
+constexpr int kG2Pitch = kG2Cols + 16;     // LDS row pitch (bf16): rows 32 bytes apart in bank
+constexpr int kGemm1Waves = 8;
+
 struct Plan {
-    int64_t W;      // 32-bit words per token bitmap
-    int64_t Lp;     // row stride of H (union index), multiple of 64
-    int KS;         // GEMM2 split-K chunks
+    int64_t W;      // 32-bit words per token bitmap (slot s is bit s % 32 of word s / 32)
+    int64_t Lp;     // row stride of H, indexed by slot: 32 W rounded up to 64
+    int KS;         // GEMM2 split-K chunks (of bitmap words)
     int MT;         // GEMM2 m-subtiles (16 tokens each) per work-group
-    size_t off_bits, off_list, off_count, off_h, off_part, total;
+    int MT1;        // GEMM1 m-subtiles per work-group
+    size_t off_bits, off_words, off_h, off_part, total;
 };
 
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
@@ -51,23 +70,21 @@ size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 Plan make_plan(int64_t B, int64_t L, int64_t d, int num_cu) {
     Plan p;
     p.W = (L + 31) / 32;
-    p.Lp = (L + 63) / 64 * 64;
+    p.Lp = (p.W * 32 + 63) / 64 * 64;
     p.MT = B >= 128 ? 8 : (B >= 64 ? 4 : (B >= 32 ? 2 : 1));
-    const int64_t ntn = (d + 255) / 256;
+    p.MT1 = B >= 64 ? 4 : (B >= 32 ? 2 : 1);
+    const int64_t ntn = (d + kG2Cols - 1) / kG2Cols;
     const int64_t ntm = (B + 16 * p.MT - 1) / (16 * p.MT);
-    int64_t ks = (2 * (int64_t)num_cu + ntn * ntm - 1) / (ntn * ntm);
-    const int64_t kmax = (L + 31) / 32;
-    if (ks > kmax) ks = kmax;
+    int64_t ks = ((int64_t)num_cu + ntn * ntm - 1) / (ntn * ntm);
+    if (ks > p.W) ks = p.W;
     if (ks > 64) ks = 64;
     if (ks < 1) ks = 1;
     p.KS = (int)ks;
     size_t o = 0;
     p.off_bits = o;
     o = align256(o + (size_t)B * p.W * 4);
-    p.off_list = o;
-    o = align256(o + (size_t)L * 4);
-    p.off_count = o;
-    o = align256(o + 16);
+    p.off_words = o;
+    o = align256(o + (size_t)p.W * 4);
     p.off_h = o;
     o = align256(o + (size_t)B * p.Lp * 4);
     p.off_part = o;
@@ -76,16 +93,41 @@ Plan make_plan(int64_t B, int64_t L, int64_t d, int num_cu) {
     return p;
 }
 
-// Token b's active slots as a bitmap of L bits (LDS), written to bits[b][0..W).
+__device__ __forceinline__ void clamp_range(const int32_t* offsets, int64_t b, int64_t nnz,
+                                            int64_t& lo, int64_t& hi) {
+    lo = offsets[b];
+    hi = offsets[b + 1];
+    lo = lo < 0 ? 0 : (lo > nnz ? nnz : lo);
+    hi = hi < lo ? lo : (hi > nnz ? nnz : hi);
+}
+
+// Position of the r-th (0-based) set bit of u; requires r < popcount(u).
+__device__ __forceinline__ int nth_set_bit(uint32_t u, int r) {
+    int pos = 0;
+#pragma unroll
+    for (int half = 16; half >= 1; half >>= 1) {
+        const uint32_t low = (1u << half) - 1u;
+        const int c = __popc(u & low);
+        if (r >= c) {
+            r -= c;
+            u >>= half;
+            pos += half;
+        } else {
+            u &= low;
+        }
+    }
+    return pos;
+}
+
+// Token b's active slots as a bitmap (LDS), written to bits[b][0..W).
 __global__ __launch_bounds__(256) void token_bitmaps(const int32_t* __restrict__ offsets,
                                                      const int32_t* __restrict__ idx,
                                                      int64_t nnz, int64_t L, int64_t W,
                                                      uint32_t* __restrict__ bits) {
     extern __shared__ uint32_t bm[];
     const int64_t b = blockIdx.x;
-    int64_t lo = offsets[b], hi = offsets[b + 1];
-    lo = lo < 0 ? 0 : (lo > nnz ? nnz : lo);
-    hi = hi < lo ? lo : (hi > nnz ? nnz : hi);
+    int64_t lo, hi;
+    clamp_range(offsets, b, nnz, lo, hi);
     for (int64_t q = threadIdx.x; q < W; q += 256) bm[q] = 0u;
     __syncthreads();
     for (int64_t r = lo + threadIdx.x; r < hi; r += 256) {
@@ -96,189 +138,224 @@ __global__ __launch_bounds__(256) void token_bitmaps(const int32_t* __restrict__
     for (int64_t q = threadIdx.x; q < W; q += 256) bits[b * W + q] = bm[q];
 }
 
-// Union of the B bitmaps, listed as ascending slot ids; count[0] = |U|.
-constexpr int kUThreads = 1024;
-__global__ __launch_bounds__(kUThreads) void build_union(const uint32_t* __restrict__ bits,
-                                                         int64_t B, int64_t W,
-                                                         int32_t* __restrict__ ulist,
-                                                         int32_t* __restrict__ count) {
-    __shared__ int wave_cnt[kUThreads / kWave];
-    const int lane = threadIdx.x & 63;
-    const int w = threadIdx.x >> 6;
-    int64_t run = 0;
-    for (int64_t base = 0; base < W; base += kUThreads) {
-        const int64_t q = base + threadIdx.x;
-        uint32_t u = 0u;
-        if (q < W)
-            for (int64_t b = 0; b < B; ++b) u |= bits[b * W + q];
-        const int c = __popc(u);
-        // exclusive prefix of c over the block: wave inclusive scan + wave totals
-        int incl = c;
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-            const int t = __shfl_up(incl, o, kWave);
-            if (lane >= o) incl += t;
-        }
-        if (lane == 63) wave_cnt[w] = incl;
-        __syncthreads();
-        int before = 0, all = 0;
-        for (int qq = 0; qq < kUThreads / kWave; ++qq) {
-            before += qq < w ? wave_cnt[qq] : 0;
-            all += wave_cnt[qq];
-        }
-        __syncthreads();
-        int64_t pos = run + before + incl - c;
-        while (u) {
-            const int bit = __ffs(u) - 1;
-            ulist[pos++] = (int32_t)(q * 32 + bit);
-            u &= u - 1u;
-        }
-        run += all;
-    }
-    if (threadIdx.x == 0) count[0] = (int32_t)run;
-}
-
-// GEMM1 + SiLU*up*mask epilogue. Work-group: 16 tokens (blockIdx.y) x 16 union rows
-// (blockIdx.x); 4 waves take K blocks of 128 round-robin. Within a K block, lane (n, g)
-// (n = lane % 16, g = lane / 16) reads 64 contiguous bytes of row n at offset g*32 and feeds
-// them to 4 MFMAs; the token operand uses the same K permutation, so the sum is unchanged.
-__global__ __launch_bounds__(256) void union_gemm1(const bf16_t* __restrict__ x, int64_t B,
-                                                   int64_t d, const bf16_t* __restrict__ gu,
-                                                   const int32_t* __restrict__ ulist,
-                                                   const int32_t* __restrict__ count,
-                                                   const uint32_t* __restrict__ bits, int64_t W,
-                                                   float* __restrict__ H, int64_t Lp) {
-    const int64_t nU = count[0];
-    const int64_t n0 = (int64_t)blockIdx.x * 16;
-    if (n0 >= nU) return;
-    const int64_t m0 = (int64_t)blockIdx.y * 16;
+// GEMM1 + SiLU*up*mask epilogue (see the file comment). Grid: (W, ceil(B/(16*MT1))).
+template <int MT1>
+__global__ __launch_bounds__(64 * kGemm1Waves) void union_gemm1(
+    const bf16_t* __restrict__ x, int64_t B, int64_t d, const bf16_t* __restrict__ gu,
+    int64_t L, const uint32_t* __restrict__ bits, int64_t W, uint32_t* __restrict__ words,
+    float* __restrict__ H, int64_t Lp) {
+    constexpr int MTOK = 16 * MT1;
+    const int64_t wd = blockIdx.x;                 // slots 32 wd .. 32 wd + 31
+    const int64_t m0 = (int64_t)blockIdx.y * MTOK;
     const int lane = threadIdx.x & 63;
     const int w = threadIdx.x >> 6;
     const int nn = lane & 15;
     const int g = lane >> 4;
-    const bool nok = n0 + nn < nU;
-    const int64_t slot = nok ? ulist[n0 + nn] : 0;
-    const bool mok = m0 + nn < B;
-    const bf16_t* grow = gu + slot * 2 * d;
-    const bf16_t* urow = grow + d;
-    const bf16_t* xrow = x + (mok ? (m0 + nn) : 0) * d;
 
-    f32x4_t accg = {0.f, 0.f, 0.f, 0.f};
-    f32x4_t accu = {0.f, 0.f, 0.f, 0.f};
-    const int64_t nkb = (d + 127) / 128;
-    const V16 z = V16{{0u, 0u, 0u, 0u}};
-    for (int64_t kb = w; kb < nkb; kb += 4) {
-        const int64_t base = kb * 128 + g * 32;
-        V16 gv[4], uv[4], xv[4];
+    // this word of the union (OR over the batch) and of each token of the tile
+    __shared__ uint32_t wor[kGemm1Waves];
+    __shared__ uint32_t tokw[MTOK];
+    uint32_t uw = 0u;
+    for (int64_t b = threadIdx.x; b < B; b += 64 * kGemm1Waves) uw |= bits[b * W + wd];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const int64_t pos = base + e * 8;
-            const bool in = pos < d;
-            gv[e] = (in && nok) ? ld16(grow + pos) : z;
-            uv[e] = (in && nok) ? ld16(urow + pos) : z;
-            xv[e] = (in && mok) ? ld16(xrow + pos) : z;
-        }
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const bf16x8_t a = as_bf16x8(xv[e]);
-            accg = mfma16x16x32(a, as_bf16x8(gv[e]), accg);
-            accu = mfma16x16x32(a, as_bf16x8(uv[e]), accu);
-        }
-    }
-    __shared__ float red[4][2][4][64];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        red[w][0][i][lane] = accg[i];
-        red[w][1][i][lane] = accu[i];
+    for (int m = 32; m >= 1; m >>= 1) uw |= (uint32_t)__shfl_xor((int)uw, m, kWave);
+    if (lane == 0) wor[w] = uw;
+    if (threadIdx.x < MTOK) {
+        const int64_t tok = m0 + threadIdx.x;
+        tokw[threadIdx.x] = tok < B ? bits[tok * W + wd] : 0u;
     }
     __syncthreads();
-    if (w != 0) return;
-    // accumulator layout: register i of lane l is (token 4*(l/16) + i, row l % 16)
+    uint32_t u = 0u;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        float gs = 0.f, us = 0.f;
+    for (int q = 0; q < kGemm1Waves; ++q) u |= wor[q];
+    if (blockIdx.y == 0 && threadIdx.x == 0) words[wd] = u;
+    const int n = __popc(u);
+
+    // H of the slots outside the union is zero
+    for (int q = threadIdx.x; q < MTOK * 32; q += 64 * kGemm1Waves) {
+        const int64_t tok = m0 + q / 32;
+        const int j = q % 32;
+        if (tok < B && !((u >> j) & 1u)) H[tok * Lp + wd * 32 + j] = 0.0f;
+    }
+    if (n == 0) return;
+
+    // row nn of MFMA tile st is the (16 st + nn)-th union slot of this word
+    const __amdgpu_buffer_rsrc_t rg = make_rsrc(gu, L * 2 * d * 2);
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, B * d * 2);
+    int64_t slot[2];
+    int goff[2];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            gs += red[q][0][i][lane];
-            us += red[q][1][i][lane];
+    for (int st = 0; st < 2; ++st) {
+        const int r = 16 * st + nn;
+        slot[st] = r < n ? wd * 32 + nth_set_bit(u, r) : -1;
+        goff[st] = slot[st] >= 0 ? (int)(slot[st] * 4 * d) : kOOB;   // gate row, bytes
+    }
+    int xoff[MT1];
+#pragma unroll
+    for (int mt = 0; mt < MT1; ++mt) {
+        const int64_t tok = m0 + mt * 16 + nn;
+        xoff[mt] = tok < B ? (int)(tok * 2 * d) : kOOB;
+    }
+    f32x4_t accg[MT1][2], accu[MT1][2];
+#pragma unroll
+    for (int mt = 0; mt < MT1; ++mt)
+#pragma unroll
+        for (int st = 0; st < 2; ++st) {
+            accg[mt][st] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            accu[mt][st] = f32x4_t{0.f, 0.f, 0.f, 0.f};
         }
-        const int64_t tok = m0 + 4 * g + i;
-        const int64_t n = n0 + nn;
-        if (tok < B && n < nU) {
-            const uint32_t s = (uint32_t)ulist[n];
-            const bool act = (bits[tok * W + (s >> 5)] >> (s & 31)) & 1u;
-            H[tok * Lp + n] = act ? silu_f32(gs) * us : 0.0f;
+    const int ntile = n > 16 ? 2 : 1;
+    const int64_t nkb = (d + 127) / 128;
+    for (int64_t kb = w; kb < nkb; kb += kGemm1Waves) {
+        V16 gv[2][4], uv[2][4];
+#pragma unroll
+        for (int st = 0; st < 2; ++st)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int64_t pos = kb * 128 + e * 32 + g * 8;    // element index in the row
+                const bool in = pos < d && goff[st] != kOOB;
+                gv[st][e] = bload16(rg, in ? goff[st] + (int)(pos * 2) : kOOB);
+                uv[st][e] = bload16(rg, in ? goff[st] + (int)((d + pos) * 2) : kOOB);
+            }
+#pragma unroll
+        for (int mt = 0; mt < MT1; ++mt) {
+            V16 xv[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int64_t pos = kb * 128 + e * 32 + g * 8;
+                xv[e] = bload16(rx, (pos < d && xoff[mt] != kOOB) ? xoff[mt] + (int)(pos * 2)
+                                                                 : kOOB);
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const bf16x8_t a = as_bf16x8(xv[e]);
+#pragma unroll
+                for (int st = 0; st < 2; ++st) {
+                    if (st < ntile) {
+                        accg[mt][st] = mfma16x16x32(a, as_bf16x8(gv[st][e]), accg[mt][st]);
+                        accu[mt][st] = mfma16x16x32(a, as_bf16x8(uv[st][e]), accu[mt][st]);
+                    }
+                }
+            }
         }
     }
+    // the 8 waves' partial tiles meet in LDS; wave 0 adds them in a fixed order
+    __shared__ float red[kGemm1Waves][2][4][64];
+#pragma unroll
+    for (int mt = 0; mt < MT1; ++mt)
+#pragma unroll
+        for (int st = 0; st < 2; ++st) {
+            if (st >= ntile) continue;                    // uniform
+            __syncthreads();
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                red[w][0][i][lane] = accg[mt][st][i];
+                red[w][1][i][lane] = accu[mt][st][i];
+            }
+            __syncthreads();
+            if (w == 0) {
+                // accumulator layout: register i of lane l is (token 4*(l/16) + i, row l % 16)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    float gs = 0.f, us = 0.f;
+#pragma unroll
+                    for (int q = 0; q < kGemm1Waves; ++q) {
+                        gs += red[q][0][i][lane];
+                        us += red[q][1][i][lane];
+                    }
+                    const int tl = mt * 16 + 4 * g + i;       // token within the tile
+                    const int64_t tok = m0 + tl;
+                    if (tok < B && slot[st] >= 0) {
+                        const bool act = (tokw[tl] >> (slot[st] - wd * 32)) & 1u;
+                        H[tok * Lp + slot[st]] = act ? silu_f32(gs) * us : 0.0f;
+                    }
+                }
+            }
+        }
 }
 
-// GEMM2: partial[b][ks][c] = sum over union rows n in chunk ks of H[b][n] * down_c[U[n]][c].
-// Work-group: 16*MT tokens x 256 columns; wave w owns columns w*64 .. w*64+63 (4 MFMA
-// n-subtiles). Per K step of 32 union rows the 256 threads stage a [32][256] tile of down
-// rows in LDS (16-byte loads); lane (n, g) then reads its B operand (8 rows of one column).
+// GEMM2 (see the file comment). Grid: (ceil(d/256), ceil(B/(16*MT)), KS); 4 waves.
 template <int MT>
 __global__ __launch_bounds__(256) void union_gemm2(const float* __restrict__ H, int64_t Lp,
                                                    int64_t B, const bf16_t* __restrict__ dc,
-                                                   int64_t d, const int32_t* __restrict__ ulist,
-                                                   const int32_t* __restrict__ count,
+                                                   int64_t d, int64_t L,
+                                                   const uint32_t* __restrict__ words, int64_t W,
                                                    float* __restrict__ part, int KS, int fast) {
-    const int64_t nU = count[0];
     const int ks = blockIdx.z;
-    int64_t chunk = (nU + KS - 1) / KS;
-    chunk = (chunk + 31) / 32 * 32;
-    const int64_t kbeg = (int64_t)ks * chunk;
-    const int64_t kend = (kbeg + chunk < nU) ? kbeg + chunk : nU;
-    const int64_t c0 = (int64_t)blockIdx.x * 256;
+    const int64_t cw = (W + KS - 1) / KS;          // bitmap words per chunk
+    const int64_t w0 = (int64_t)ks * cw;
+    const int64_t w1 = (w0 + cw < W) ? w0 + cw : W;
+    const int64_t c0 = (int64_t)blockIdx.x * kG2Cols;
     const int64_t m0 = (int64_t)blockIdx.y * 16 * MT;
     const int lane = threadIdx.x & 63;
     const int w = threadIdx.x >> 6;
     const int nn = lane & 15;
     const int g = lane >> 4;
 
-    __shared__ __align__(16) uint16_t tile[32][256];
+    __shared__ __align__(16) uint16_t tile[2][32][kG2Pitch];
     f32x4_t acc[MT][4];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[mt][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-    const int sr = threadIdx.x >> 3;        // staging: row 0..31
-    const int sc = (threadIdx.x & 7) * 32;  // staging: first of 32 columns
-    const V16 z = V16{{0u, 0u, 0u, 0u}};
-    for (int64_t k0 = kbeg; k0 < kend; k0 += 32) {
-        {
-            const int64_t k = k0 + sr;
-            const bool rok = k < kend;
-            const int64_t slot = rok ? ulist[k] : 0;
-            const bf16_t* src = dc + slot * d + c0 + sc;
-            V16 v[4];
+    const __amdgpu_buffer_rsrc_t rd = make_rsrc(dc, L * d * 2);
+    const int sr = threadIdx.x >> 3;         // staging: tile row (slot 32 wd + sr)
+    const int sc = (threadIdx.x & 7) * 32;   // staging: first of 32 columns
+    // three words' down rows in flight in registers ahead of the LDS tile being consumed
+    constexpr int kDepth = 3;
+    V16 nxt[kDepth][4];
+    auto fetch = [&](int64_t wd, V16 (&v)[4]) {
+        const uint32_t u = wd < w1 ? words[wd] : 0u;
+        const bool rok = (u >> sr) & 1u;
+        const int64_t slot = wd * 32 + sr;
 #pragma unroll
-            for (int e = 0; e < 4; ++e)
-                v[e] = (rok && c0 + sc + e * 8 < d) ? ld16(src + e * 8) : z;
-            __syncthreads();
-#pragma unroll
-            for (int e = 0; e < 4; ++e) st16(&tile[sr][sc + e * 8], v[e]);
-            __syncthreads();
+        for (int e = 0; e < 4; ++e) {
+            const int64_t col = c0 + sc + e * 8;
+            v[e] = bload16(rd, (rok && col < d) ? (int)((slot * d + col) * 2) : kOOB);
         }
+    };
+    // consume the LDS tile `bsel` holding slots 32 wd .. 32 wd + 31
+    auto consume = [&](int64_t wd, int bsel) {
+        // B operand: lane (nn, g) needs rows 8g..8g+7 of column nn of each 16-column subtile;
+        // ds_read_b64_tr_b16 hands lane i of a 16-lane group element i%4 of the 8-byte pieces
+        // addressed by lanes i/4 + 4j, so lane nn addresses row 8g + nn/4 (+4), columns
+        // 4*(nn%4) .. +3 of the subtile.
         bf16x8_t bop[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const int col = w * 64 + j * 16 + nn;
-            uint32_t pk[4];
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-                pk[q] = (uint32_t)tile[g * 8 + 2 * q][col] |
-                        ((uint32_t)tile[g * 8 + 2 * q + 1][col] << 16);
-            bop[j] = as_bf16x8(V16{{pk[0], pk[1], pk[2], pk[3]}});
+            const int col = w * 64 + j * 16 + 4 * (nn & 3);
+            const int row = 8 * g + (nn >> 2);
+            const s16x4_t lo4 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) s16x4_t*)&tile[bsel][row][col]);
+            const s16x4_t hi4 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) s16x4_t*)&tile[bsel][row + 4][col]);
+            const uint32_t p0 = (uint16_t)lo4[0] | ((uint32_t)(uint16_t)lo4[1] << 16);
+            const uint32_t p1 = (uint16_t)lo4[2] | ((uint32_t)(uint16_t)lo4[3] << 16);
+            const uint32_t p2 = (uint16_t)hi4[0] | ((uint32_t)(uint16_t)hi4[1] << 16);
+            const uint32_t p3 = (uint16_t)hi4[2] | ((uint32_t)(uint16_t)hi4[3] << 16);
+            bop[j] = as_bf16x8(V16{{p0, p1, p2, p3}});
         }
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
             const int64_t tok = m0 + mt * 16 + nn;
+            // A operand: H of token tok at slots 32 wd + 8 g .. +7 (contiguous, 32-byte aligned)
             float hv[8];
+            if (tok < B) {
+                const float* hrow = H + tok * Lp + wd * 32 + g * 8;
+                const float4 a = *reinterpret_cast<const float4*>(hrow);
+                const float4 b = *reinterpret_cast<const float4*>(hrow + 4);
+                hv[0] = a.x;
+                hv[1] = a.y;
+                hv[2] = a.z;
+                hv[3] = a.w;
+                hv[4] = b.x;
+                hv[5] = b.y;
+                hv[6] = b.z;
+                hv[7] = b.w;
+            } else {
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int64_t k = k0 + g * 8 + e;
-                hv[e] = (tok < B && k < kend) ? H[tok * Lp + k] : 0.0f;
+                for (int e = 0; e < 8; ++e) hv[e] = 0.0f;
             }
             uint32_t hi[4], lo[4];
 #pragma unroll
@@ -298,6 +375,22 @@ __global__ __launch_bounds__(256) void union_gemm2(const float* __restrict__ H, 
                 if (!fast) acc[mt][j] = mfma16x16x32(alo, bop[j], acc[mt][j]);
             }
         }
+    };
+#pragma unroll
+    for (int q = 0; q < kDepth; ++q) fetch(w0 + q, nxt[q]);
+    int buf = 0;
+    for (int64_t wg = w0; wg < w1; wg += kDepth) {
+#pragma unroll
+        for (int q = 0; q < kDepth; ++q) {
+            const int64_t wd = wg + q;
+            if (wd >= w1) break;                      // uniform over the work-group
+#pragma unroll
+            for (int e = 0; e < 4; ++e) st16(&tile[buf][sr][sc + e * 8], nxt[q][e]);
+            __syncthreads();
+            fetch(wd + kDepth, nxt[q]);               // refill: kDepth words ahead
+            if (words[wd] != 0u) consume(wd, buf);    // uniform: empty words add nothing
+            buf ^= 1;
+        }
     }
     // accumulator: register i of lane l is (token 4*(l/16) + i, column l % 16) of a subtile
 #pragma unroll
@@ -314,6 +407,12 @@ __global__ __launch_bounds__(256) void union_gemm2(const float* __restrict__ H, 
 
 }  // namespace
 
+bool union_supported(int64_t B, int64_t L, int64_t d) {
+    // buffer loads take 32-bit byte offsets
+    return L * 2 * d * 2 < ((int64_t)1 << 31) && B * d * 2 < ((int64_t)1 << 31) &&
+           L <= 524288;
+}
+
 size_t union_workspace(int64_t B, int64_t L, int64_t d, int num_cu) {
     return make_plan(B, L, d, num_cu).total;
 }
@@ -321,12 +420,11 @@ size_t union_workspace(int64_t B, int64_t L, int64_t d, int num_cu) {
 hipError_t launch_union(const void* x, int64_t B, int64_t d, const int32_t* offsets,
                         const int32_t* idx, int64_t nnz, const void* gate_up_c,
                         const void* down_c, int64_t L, float* y, void* ws, int flags,
-                        int num_cu, hipStream_t s) {
+                        int num_cu, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
     const Plan p = make_plan(B, L, d, num_cu);
     uint8_t* base = static_cast<uint8_t*>(ws);
     uint32_t* bits = reinterpret_cast<uint32_t*>(base + p.off_bits);
-    int32_t* ulist = reinterpret_cast<int32_t*>(base + p.off_list);
-    int32_t* count = reinterpret_cast<int32_t*>(base + p.off_count);
+    uint32_t* words = reinterpret_cast<uint32_t*>(base + p.off_words);
     float* H = reinterpret_cast<float*>(base + p.off_h);
     float* part = reinterpret_cast<float*>(base + p.off_part);
     const bf16_t* xx = static_cast<const bf16_t*>(x);
@@ -335,15 +433,24 @@ hipError_t launch_union(const void* x, int64_t B, int64_t d, const int32_t* offs
 
     hipLaunchKernelGGL(token_bitmaps, dim3((unsigned)B), dim3(256), (size_t)p.W * 4, s, offsets,
                        idx, nnz, L, p.W, bits);
-    hipLaunchKernelGGL(build_union, dim3(1), dim3(kUThreads), 0, s, bits, B, p.W, ulist, count);
-    hipLaunchKernelGGL(union_gemm1, dim3((unsigned)((L + 15) / 16), (unsigned)((B + 15) / 16)),
-                       dim3(256), 0, s, xx, B, d, gu, ulist, count, bits, p.W, H, p.Lp);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const dim3 g1((unsigned)p.W, (unsigned)((B + 16 * p.MT1 - 1) / (16 * p.MT1)));
+#define SI_G1(M)                                                                                \
+    hipExtLaunchKernelGGL(union_gemm1<M>, g1, dim3(64 * kGemm1Waves), 0, s, ev0, nullptr, 0, xx, \
+                          B, d, gu, L, bits, p.W, words, H, p.Lp)
+    switch (p.MT1) {
+        case 4: SI_G1(4); break;
+        case 2: SI_G1(2); break;
+        default: SI_G1(1); break;
+    }
+#undef SI_G1
     const int fast = (flags & 4) ? 1 : 0;
-    dim3 g2((unsigned)((d + 255) / 256), (unsigned)((B + 16 * p.MT - 1) / (16 * p.MT)),
-            (unsigned)p.KS);
+    dim3 g2((unsigned)((d + kG2Cols - 1) / kG2Cols),
+            (unsigned)((B + 16 * p.MT - 1) / (16 * p.MT)), (unsigned)p.KS);
 #define SI_G2(MTV)                                                                             \
-    hipLaunchKernelGGL(union_gemm2<MTV>, g2, dim3(256), 0, s, H, p.Lp, B, dc, d, ulist, count, \
-                       part, p.KS, fast)
+    hipExtLaunchKernelGGL(union_gemm2<MTV>, g2, dim3(256), 0, s, nullptr, ev1, 0, H, p.Lp, B, dc, \
+                          d, L, words, p.W, part, p.KS, fast)
     switch (p.MT) {
         case 8: SI_G2(8); break;
         case 4: SI_G2(4); break;
@@ -351,7 +458,7 @@ hipError_t launch_union(const void* x, int64_t B, int64_t d, const int32_t* offs
         default: SI_G2(1); break;
     }
 #undef SI_G2
-    hipError_t e = hipGetLastError();
+    e = hipGetLastError();
     if (e != hipSuccess) return e;
     return launch_reduce_partials(part, p.KS, B, d, y, s);
 }

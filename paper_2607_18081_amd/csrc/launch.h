@@ -17,14 +17,16 @@ hipError_t launch_reduce_partials(const float* partials, int P, int64_t B, int64
 hipError_t launch_decode(const void* x, int xdt, int64_t B, int64_t d, const int32_t* offsets,
                          const int32_t* idx, int64_t nnz, const void* gate_up_c,
                          const void* down_c, int64_t L, int wdt, float* partials, int P,
-                         float* y, hipStream_t s);
+                         float* y, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 
 // ---- k_union.hip: union (MFMA) path -----------------------------------------------------
+// sizes the union kernels handle (their buffer loads take 32-bit byte offsets)
+bool union_supported(int64_t B, int64_t L, int64_t d);
 size_t union_workspace(int64_t B, int64_t L, int64_t d, int num_cu);
 hipError_t launch_union(const void* x, int64_t B, int64_t d, const int32_t* offsets,
                         const int32_t* idx, int64_t nnz, const void* gate_up_c,
                         const void* down_c, int64_t L, float* y, void* ws, int flags,
-                        int num_cu, hipStream_t s);
+                        int num_cu, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 
 // ---- k_topk.hip ---------------------------------------------------------------------------
 hipError_t launch_topk(const float* scores, int64_t B, int64_t L, int64_t k, int mode,

@@ -106,7 +106,7 @@ def test_remap_matches_oracle():
         si.remap_ids(o2s, torch.from_numpy(np.concatenate([ids[:5], not_loaded])), check=True)
     assert e.value.status == 4
     with pytest.raises(si.SelectInferError) as e:
-        si.remap_ids(o2s, torch.tensor([1, N + 3], dtype=torch.int32), check=True)
+        si.remap_ids(o2s, torch.tensor([int(ids[0]), N + 3], dtype=torch.int32), check=True)
     assert e.value.status == 2
     assert si.remap_ids(o2s, torch.zeros(0, dtype=torch.int32)).numel() == 0
 
