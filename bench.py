@@ -292,22 +292,20 @@ def cpu_baseline(work, ref, seconds):
 
 
 def traffic_record(workload):
-    """HBM traffic per launch from committed rocprofv3 counter runs, if taken on this source."""
+    """HBM bytes per launch of the main kernel, from the committed rocprofv3 counter runs
+    (profiles/traffic_<workload>.json), or None when the kernel sources changed since."""
     path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
     if not os.path.exists(path):
         return None
     try:
         rec = json.load(open(path))
-        src = os.path.join(ROOT, "paper_2607_18081_amd", "csrc", rec["kernel_source"])
-        h = hashlib.sha256(open(src, "rb").read()).hexdigest()
-        return rec["bytes_per_launch"] if h == rec["source_sha256"] else None
+        h = hashlib.sha256()
+        for f in rec["kernel_sources"]:
+            h.update(open(os.path.join(ROOT, "paper_2607_18081_amd", "csrc", f), "rb").read())
+        return rec["bytes_per_launch"] if h.hexdigest() == rec["sources_sha256"] else None
     except (OSError, KeyError, ValueError):
         return None
 
-
-KERNEL_SOURCE = {"llama2_7b_decode": "k_decode.hip", "tiny_f32": "k_decode.hip",
-                 "llama3_8b_stack": "k_decode.hip", "llama2_7b_b16": "k_union.hip",
-                 "llama2_13b_prefill": "k_union.hip"}
 
 
 def main():
