@@ -95,12 +95,18 @@ class Workload:
         self.x_host = xt
         self.x = self._dev(xt)
         self.sets_host = []
-        self.off, self.slots = [], []
+        self.off, self.slots, self.ibase = [], [], []
         for lay in range(nlay):
             sets = active_sets(cfg, range(T), lay)
             off, ids = csr_from_sets(sets)
             self.sets_host.append(sets if lay < 2 else None)
-            self.off.append(self._dev(off))
+            # per step, the CSR of its B tokens as a top-k pass would hand it over: the step's
+            # own slot slice, offsets from 0 (row s of `rel`)
+            base = off[0:T:cfg.B].astype(np.int64)
+            rel = np.stack([off[s * cfg.B:(s + 1) * cfg.B + 1] - off[s * cfg.B]
+                            for s in range(cfg.steps)]).astype(np.int32)
+            self.ibase.append([int(v) for v in base])
+            self.off.append(self._dev(rel))
             self.slots.append(si.remap_ids(self.layers[lay][0].orig_to_slot, self._dev(ids),
                                            check=True))
         self.y = torch.empty((T, cfg.d), dtype=torch.float32, device=dev)
@@ -128,6 +134,12 @@ class Workload:
                 self.torch.bfloat16)
         return self.torch.from_numpy(a).to(self.dev)
 
+    def _slots(self, lay, s):
+        """Slot ids of step s (a view, no copy)."""
+        lo = self.ibase[lay][s]
+        hi = self.ibase[lay][s + 1] if s + 1 < len(self.ibase[lay]) else self.slots[lay].numel()
+        return self.slots[lay][lo:hi]
+
     @property
     def steps_in_sequence(self):
         return self.cfg.steps
@@ -143,7 +155,7 @@ class Workload:
             cp = self.layers[0][step % len(self.layers[0])]
             if timing:
                 si.set_timing_events(*timing[0])
-            si.selective_ffn(self.x[t0:t0 + B], self.off[0][t0:t0 + B + 1], self.slots[0],
+            si.selective_ffn(self.x[t0:t0 + B], self.off[0][s], self._slots(0, s),
                              cp.gate_up_c, cp.down_c, y=self.y[t0:t0 + B], workspace=self.ws)
         else:
             xin = self.x[t0:t0 + 1]
@@ -152,7 +164,7 @@ class Workload:
                 if timing:
                     si.set_timing_events(*timing[lay])
                 y = self.y[t0:t0 + 1]
-                si.selective_ffn(xin, self.off[lay][t0:t0 + 2], self.slots[lay], cp.gate_up_c,
+                si.selective_ffn(xin, self.off[lay][s], self._slots(lay, s), cp.gate_up_c,
                                  cp.down_c, y=y, workspace=self.ws)
                 if timing:
                     si.set_timing_events(None, None)

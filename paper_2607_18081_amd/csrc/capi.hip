@@ -156,8 +156,7 @@ size_t si_selective_ffn_workspace(int64_t B, int64_t nnz, int64_t L, int64_t d, 
     const int dev = current_device();
     const int ncu = dev < 0 ? 256 : num_cu(dev);
     if (use_union(B, L, d, xdt, wdt, flags)) return si::union_workspace(B, L, d, ncu);
-    const int P = si::decode_chunks(B, nnz, ncu);
-    return (size_t)B * P * d * sizeof(float);
+    return si::decode_workspace(B, nnz, d, ncu);
 }
 
 int si_selective_ffn(const void* x, si_dtype xdt, int64_t B, int64_t d, const int32_t* offsets,

@@ -70,6 +70,18 @@ __device__ __forceinline__ V16 bload16(__amdgpu_buffer_rsrc_t r, int off) {
     return o;
 }
 
+// Buffer load at a per-lane offset plus a wave-uniform (scalar-register) offset. The row base
+// of a gather goes in the scalar offset, so addressing a row costs no vector instructions.
+__device__ __forceinline__ V16 bload16s(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+    const i32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+    V16 o;
+    o.w[0] = (uint32_t)v[0];
+    o.w[1] = (uint32_t)v[1];
+    o.w[2] = (uint32_t)v[2];
+    o.w[3] = (uint32_t)v[3];
+    return o;
+}
+
 // Unpack a 16-byte vector into V floats (V = 8 for bf16, 4 for f32).
 template <typename T>
 struct Elem;
@@ -92,6 +104,18 @@ struct Elem<bf16_t> {
         }
     }
 };
+
+// Float32 partial sums of the two-level reductions are stored column-chunked: for token b,
+// partial p and column c, element ((b * nch + c / 16) * P + p) * 16 + c % 16, with
+// nch = ceil(d / 16). The P partials of 16 columns are then one contiguous block of P * 64
+// bytes, which the reducer reads in full 128-byte lines, and a writer's 16 columns are 64
+// contiguous bytes.
+constexpr int kChunk = 16;
+__host__ __device__ __forceinline__ int64_t part_chunks(int64_t d) { return (d + kChunk - 1) / kChunk; }
+__host__ __device__ __forceinline__ int64_t part_off(int64_t b, int64_t p, int64_t col, int64_t P,
+                                                     int64_t nch) {
+    return ((b * nch + col / kChunk) * P + p) * kChunk + col % kChunk;
+}
 
 // SiLU(g) = g * sigmoid(g), float32
 __device__ __forceinline__ float silu_f32(float g) { return __fdividef(g, 1.0f + __expf(-g)); }

@@ -6,14 +6,15 @@
 // Kernel 1 (sffn_rows): work-group (p, b) takes chunk p of token b's active list. Its 8 waves
 // split the d columns: wave w, lane l own the 16-byte column groups ((i*8 + w)*64 + l), so a
 // row is read as one fully coalesced sweep of the work-group. For a batch of up to R rows the
-// work-group issues every gate, up and down load of the batch at once (the down rows do not
-// depend on h, so they stream in while the dot products complete), reduces each row's two dot
+// work-group issues every gate and up load of the batch, then every down load (the down rows
+// do not depend on h, so they stream in while the dot products complete), reduces each row's two dot
 // products across the wave with a transposing shuffle reduction and across the 8 waves through
 // LDS, applies SiLU*up, and accumulates h_j * down_j into per-lane float32 registers. The
-// work-group's partial sum over its rows is written as one float32 row of the workspace.
+// work-group's partial sum over its rows is written to the workspace in the column-chunked
+// partial layout (common.h).
 //
-// Kernel 2 (reduce_partials) adds the P partial rows of each token in a fixed order, so the
-// result is deterministic and no global atomics are used.
+// Kernel 2 (reduce_chunks) adds the P partials of each token in a fixed order, so the result
+// is deterministic and no global atomics are used.
 #include <hip/hip_ext.h>
 
 #include "common.h"
@@ -35,16 +36,41 @@ typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
 
 // The token's x restricted to one lane's 16-byte column group, in the form its dot products
 // use: packed bf16 pairs when both x and the weights are bf16 (v_dot2_f32_bf16), else float.
+// Loaded through a buffer descriptor over the token's row, so a lane outside the row passes
+// kOOB and gets zeros without a branch: a conditional load would make the compiler wait for it
+// at the branch join, ahead of the row loads, and add a memory round trip to the kernel start.
+typedef __attribute__((ext_vector_type(2))) int i32x2_t;
+
 template <typename WT, typename XT>
 struct XSlice {
     static constexpr int V = Elem<WT>::V;
+    static constexpr int WORDS = V * (int)sizeof(XT) / 4;  // 2, 4 or 8
     float v[V];
-    __device__ __forceinline__ void load(const XT* p, bool ok) {
+    __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t r, int off) {
+        uint32_t wd[WORDS];
+        if (WORDS == 2) {
+            const i32x2_t t = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+            wd[0] = (uint32_t)t[0];
+            wd[1] = (uint32_t)t[1];
+        } else {
 #pragma unroll
-        for (int e = 0; e < V; ++e) v[e] = ok ? xval(p + e) : 0.0f;
+            for (int q = 0; q < WORDS / 4; ++q) {
+                const V16 t = bload16(r, off == kOOB ? kOOB : off + 16 * q);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) wd[4 * q + e] = t.w[e];
+            }
+        }
+#pragma unroll
+        for (int e = 0; e < V; ++e) v[e] = xval(wd, e, (const XT*)nullptr);
     }
-    __device__ __forceinline__ static float xval(const float* p) { return *p; }
-    __device__ __forceinline__ static float xval(const bf16_t* p) { return bf16_to_f32(*p); }
+    template <int N>
+    __device__ __forceinline__ static float xval(const uint32_t (&wd)[N], int e, const float*) {
+        return __uint_as_float(wd[e]);
+    }
+    template <int N>
+    __device__ __forceinline__ static float xval(const uint32_t (&wd)[N], int e, const bf16_t*) {
+        return (e & 1) ? bf16hi(wd[e >> 1]) : bf16lo(wd[e >> 1]);
+    }
     __device__ __forceinline__ float dot(const V16& w, float acc) const {
         float f[V];
         Elem<WT>::unpack(w, f);
@@ -57,8 +83,8 @@ struct XSlice {
 template <>
 struct XSlice<bf16_t, bf16_t> {
     uint32_t v[4];
-    __device__ __forceinline__ void load(const bf16_t* p, bool ok) {
-        const V16 t = ok ? ld16(p) : V16{{0u, 0u, 0u, 0u}};
+    __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t r, int off) {
+        const V16 t = bload16(r, off);
 #pragma unroll
         for (int q = 0; q < 4; ++q) v[q] = t.w[q];
     }
@@ -71,52 +97,76 @@ struct XSlice<bf16_t, bf16_t> {
     }
 };
 
-// Row loads of the gather-GEMV. BUF: buffer loads with range-checked 32-bit offsets (no
-// branches; the compacted tensors must be smaller than 2 GiB); else guarded global loads.
-template <typename WT, bool BUF>
+// Row loads of the gather-GEMV; lane column group i of row j, for a wave-uniform slot id j and
+// validity flag ok. BUF: buffer loads with 32-bit offsets (the compacted tensors must be
+// smaller than 2 GiB); a row or column that must read nothing gets an offset past the end of
+// the buffer, so the access reads no memory and returns zeros, without a branch. Otherwise
+// guarded global loads.
+template <typename WT, bool BUF, int NI>
 struct RowLoader;
 
-template <typename WT>
-struct RowLoader<WT, true> {
+template <typename WT, int NI>
+struct RowLoader<WT, true, NI> {
     __amdgpu_buffer_rsrc_t rg, rd;
-    int64_t d;
-    __device__ __forceinline__ RowLoader(const WT* gu, const WT* dc, int64_t L, int64_t d_)
-        : d(d_) {
-        rg = make_rsrc(gu, L * 2 * d_ * (int64_t)sizeof(WT));
-        rd = make_rsrc(dc, L * d_ * (int64_t)sizeof(WT));
+    int rowg, rowd;    // bytes per row of gate_up_c and down_c
+    int vcol[NI];      // lane column byte offset, or kOOB outside the row
+    __device__ __forceinline__ RowLoader(const WT* gu, const WT* dc, int64_t L, int64_t d,
+                                         const int64_t (&col)[NI], const bool (&cok)[NI]) {
+        rg = make_rsrc(gu, L * 2 * d * (int64_t)sizeof(WT));
+        rd = make_rsrc(dc, L * d * (int64_t)sizeof(WT));
+        rowg = (int)(2 * d * (int64_t)sizeof(WT));
+        rowd = (int)(d * (int64_t)sizeof(WT));
+#pragma unroll
+        for (int i = 0; i < NI; ++i) vcol[i] = cok[i] ? (int)(col[i] * (int64_t)sizeof(WT)) : kOOB;
     }
-    __device__ __forceinline__ void load(bool ok, int32_t j, int64_t col, V16& g, V16& u,
-                                         V16& dn) const {
-        const int og = ok ? (int)(((int64_t)j * 2 * d + col) * sizeof(WT)) : kOOB;
-        const int od = ok ? (int)(((int64_t)j * d + col) * sizeof(WT)) : kOOB;
+    // kOOB + a row offset (< 2^31) stays out of range without wrapping
+    __device__ __forceinline__ void load_gu(bool ok, int32_t j, int i, V16& g, V16& u) const {
+        const int og = ok ? vcol[i] + j * rowg : kOOB;
         g = bload16(rg, og);
-        u = bload16(rg, ok ? og + (int)(d * sizeof(WT)) : kOOB);
-        dn = bload16(rd, od);
+        u = bload16(rg, og + rowd);
+    }
+    __device__ __forceinline__ void load_dn(bool ok, int32_t j, int i, V16& dn) const {
+        dn = bload16(rd, ok ? vcol[i] + j * rowd : kOOB);
     }
 };
 
-template <typename WT>
-struct RowLoader<WT, false> {
+template <typename WT, int NI>
+struct RowLoader<WT, false, NI> {
     const WT* gu;
     const WT* dc;
     int64_t d;
-    __device__ __forceinline__ RowLoader(const WT* gu_, const WT* dc_, int64_t, int64_t d_)
-        : gu(gu_), dc(dc_), d(d_) {}
-    __device__ __forceinline__ void load(bool ok, int32_t j, int64_t col, V16& g, V16& u,
-                                         V16& dn) const {
-        const V16 z = V16{{0u, 0u, 0u, 0u}};
-        if (ok) {
-            const WT* gp = gu + (int64_t)j * 2 * d + col;
-            g = ld16(gp);
-            u = ld16(gp + d);
-            dn = ld16(dc + (int64_t)j * d + col);
-        } else {
-            g = z;
-            u = z;
-            dn = z;
+    int64_t col[NI];
+    bool cok[NI];
+    __device__ __forceinline__ RowLoader(const WT* gu_, const WT* dc_, int64_t, int64_t d_,
+                                         const int64_t (&col_)[NI], const bool (&cok_)[NI])
+        : gu(gu_), dc(dc_), d(d_) {
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+            col[i] = col_[i];
+            cok[i] = cok_[i];
         }
     }
+    __device__ __forceinline__ void load_gu(bool ok, int32_t j, int i, V16& g, V16& u) const {
+        if (ok && cok[i]) {
+            const WT* gp = gu + (int64_t)j * 2 * d + col[i];
+            g = ld16(gp);
+            u = ld16(gp + d);
+        } else {
+            g = V16{{0u, 0u, 0u, 0u}};
+            u = g;
+        }
+    }
+    __device__ __forceinline__ void load_dn(bool ok, int32_t j, int i, V16& dn) const {
+        dn = (ok && cok[i]) ? ld16(dc + (int64_t)j * d + col[i]) : V16{{0u, 0u, 0u, 0u}};
+    }
 };
+
+// floor(n * p / P) for 0 <= n, 0 <= p <= P: the first row of chunk p when n rows are dealt to
+// P chunks. The host keeps nnz * P below 2^32 (decode_chunks), so 32-bit arithmetic is exact;
+// the GPU has no integer divide instruction and a 64-bit emulation is several times longer.
+__device__ __forceinline__ int64_t split(int64_t n, int p, int P) {
+    return (int64_t)((uint32_t)n * (uint32_t)p / (uint32_t)P);
+}
 
 template <typename WT, typename XT, int NI, bool BUF>
 __global__ __launch_bounds__(kThreads) void sffn_rows(
@@ -133,41 +183,86 @@ __global__ __launch_bounds__(kThreads) void sffn_rows(
     const int lane = threadIdx.x & (kWave - 1);
     const int w = threadIdx.x >> 6;
 
-    int64_t lo = offsets[b], hi = offsets[b + 1];
-    lo = lo < 0 ? 0 : (lo > nnz ? nnz : lo);
-    hi = hi < lo ? lo : (hi > nnz ? nnz : hi);
-    const int64_t n = hi - lo;
-    const int64_t r0 = lo + (n * p) / P;
-    const int64_t r1 = lo + (n * (p + 1)) / P;
-
     int64_t col[NI];
     bool cok[NI];
-    XSlice<WT, XT> xs[NI];
     float acc[NI][V];
-    const XT* xb = x + (int64_t)b * d;
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
         col[i] = ((int64_t)(i * kWaves + w) * kWave + lane) * V;
         cok[i] = col[i] < d;
-        xs[i].load(xb + (cok[i] ? col[i] : 0), cok[i]);
 #pragma unroll
         for (int e = 0; e < V; ++e) acc[i][e] = 0.0f;
     }
-    const RowLoader<WT, BUF> ldr(gate_up_c, down_c, L, d);
+    const RowLoader<WT, BUF, NI> ldr(gate_up_c, down_c, L, d, col, cok);
+
+    // Slot ids of batch [rb, rb + nr): a batch that lies inside idx is read with unconditional
+    // scalar loads, which the compiler merges into one wide load (separate conditional loads
+    // would each wait for the previous one). Rows past nr get -1.
+    auto fetch_ids = [&](int64_t rb, int nr, int32_t (&sl)[R]) {
+        if (rb + R <= nnz) {
+#pragma unroll
+            for (int r = 0; r < R; ++r) sl[r] = idx[rb + r];
+        } else {
+#pragma unroll
+            for (int r = 0; r < R; ++r) sl[r] = rb + r < nnz ? idx[rb + r] : -1;
+        }
+#pragma unroll
+        for (int r = 0; r < R; ++r) sl[r] = r < nr ? sl[r] : -1;
+    };
+    // Issues the row loads of a batch: every gate/up load, then the down loads. The memory
+    // system returns the gate/up rows first, so the dot products and the cross-wave exchange
+    // finish while the down rows are still streaming in. Ids are wave-uniform, so the row
+    // bases stay in scalar registers.
+    V16 gv[R][NI], uv[R][NI], dv[R][NI];
+    auto issue = [&](const int32_t (&sl)[R]) {
+        bool okr[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) okr[r] = (sl[r] >= 0) && (sl[r] < L);
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+#pragma unroll
+            for (int i = 0; i < NI; ++i) ldr.load_gu(okr[r], sl[r], i, gv[r][i], uv[r][i]);
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+#pragma unroll
+            for (int i = 0; i < NI; ++i) ldr.load_dn(okr[r], sl[r], i, dv[r][i]);
+    };
+
+    // x first: vector loads complete in issue order, so the dot products of the first rows
+    // wait only for x and their own rows
+    XSlice<WT, XT> xs[NI];
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(x + (int64_t)b * d, d * (int64_t)sizeof(XT));
+#pragma unroll
+    for (int i = 0; i < NI; ++i) xs[i].load(rx, cok[i] ? (int)(col[i] * (int64_t)sizeof(XT)) : kOOB);
+
+    // The first batch's slot ids are fetched together with the token's offsets, from the
+    // range this work-group gets when the B tokens hold nnz / B rows each from index 0 (a
+    // top-k output, or one token with offsets {0, nnz}): the row loads then wait for one
+    // memory round trip instead of two (offsets, then ids). The guess is checked before the
+    // ids are used; a wrong guess fetches them again and costs only that round trip.
+    const int64_t per = split(nnz, 1, (int)gridDim.y);
+    const int64_t g0 = (int64_t)b * per + split(per, p, P);
+    int32_t sl[R];
+    fetch_ids(g0, R, sl);
+
+    int64_t lo = offsets[b], hi = offsets[b + 1];
+    lo = lo < 0 ? 0 : (lo > nnz ? nnz : lo);
+    hi = hi < lo ? lo : (hi > nnz ? nnz : hi);
+    const int64_t n = hi - lo;
+    int64_t rb = lo + split(n, p, P);
+    const int64_t r1 = lo + split(n, p + 1, P);
+    int nr = (int)((r1 - rb) < R ? (r1 - rb) : R);
+    if (rb == g0) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) sl[r] = r < nr ? sl[r] : -1;
+    } else {
+        fetch_ids(rb, nr, sl);
+    }
+    issue(sl);
 
     __shared__ float red[2][NVAL][kWaves];
     int buf = 0;
-    for (int64_t rb = r0; rb < r1; rb += R) {
-        const int nr = (int)((r1 - rb) < R ? (r1 - rb) : R);
-        V16 gv[R][NI], uv[R][NI], dv[R][NI];
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-            // wave-uniform slot id: the row base stays in scalar registers
-            const int32_t s = __builtin_amdgcn_readfirstlane(r < nr ? idx[rb + r] : -1);
-            const bool ok = (s >= 0) && (s < L);
-#pragma unroll
-            for (int i = 0; i < NI; ++i) ldr.load(ok && cok[i], s, col[i], gv[r][i], uv[r][i], dv[r][i]);
-        }
+    while (nr > 0) {
         float vals[NVAL];
 #pragma unroll
         for (int r = 0; r < R; ++r) {
@@ -207,12 +302,19 @@ __global__ __launch_bounds__(kThreads) void sffn_rows(
             }
         }
         buf ^= 1;
+        rb += R;
+        if (rb >= r1) break;
+        nr = (int)((r1 - rb) < R ? (r1 - rb) : R);
+        fetch_ids(rb, nr, sl);
+        issue(sl);
     }
 
-    float* out = partials + ((int64_t)b * P + p) * d;
+    const int64_t nch = part_chunks(d);
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
         if (cok[i]) {
+            // V <= 16 consecutive columns starting at a multiple of V stay inside one chunk
+            float* out = partials + part_off(b, p, col[i], P, nch);
 #pragma unroll
             for (int e = 0; e < V; e += 4) {
                 V16 o;
@@ -220,46 +322,73 @@ __global__ __launch_bounds__(kThreads) void sffn_rows(
                 o.w[1] = __float_as_uint(acc[i][e + 1]);
                 o.w[2] = __float_as_uint(acc[i][e + 2]);
                 o.w[3] = __float_as_uint(acc[i][e + 3]);
-                st16(out + col[i] + e, o);
+                st16(out + e, o);
             }
         }
     }
 }
 
-// y[b][c] = sum_{p = 0..P-1} partials[b][p][c] in a fixed order. One wave per 4 columns (a
-// float4 group): lane l adds p = l, l + 64, ... in order, then a fixed transposing shuffle tree
-// leaves column c + l/16 in lanes 16*(l/16). No LDS, no barrier.
-__global__ __launch_bounds__(256) void reduce_partials(const float* __restrict__ partials, int P,
-                                                       int64_t d, float* __restrict__ y) {
+// y[b][c] = sum_{p = 0..P-1} of the partials of column c, in a fixed order. One (token, chunk)
+// pair per WPP waves: its P x 16 floats are contiguous; thread t adds the float4 groups
+// t, t + 64 WPP, ... (all of column quarter t % 4) in ascending order, then a fixed shuffle tree
+// over the lanes of one quarter and, for WPP = 4, a fixed-order sum of the waves through LDS.
+template <int WPP>
+__global__ __launch_bounds__(256) void reduce_chunks(const float* __restrict__ partials, int P,
+                                                     int64_t pairs, int64_t nch, int64_t d,
+                                                     float* __restrict__ y) {
+    constexpr int NT = WPP * kWave;
     const int lane = threadIdx.x & (kWave - 1);
-    const int64_t c = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * 4;
-    const int b = blockIdx.y;
-    if (c >= d) return;
-    const float* base = partials + (int64_t)b * P * d + c;
-    float4 v[4];
+    const int w = threadIdx.x >> 6;
+    const int64_t pair = (int64_t)blockIdx.x * (4 / WPP) + w / WPP;
+    if (pair >= pairs) return;  // uniform per work-group when WPP = 4
+    const int t = (w % WPP) * kWave + lane;
+    const float4* base = reinterpret_cast<const float4*>(partials + pair * (int64_t)P * kChunk);
+    const int n4 = P * (kChunk / 4);
+    float s[4] = {0.f, 0.f, 0.f, 0.f};
+    int i = t;
+    for (; i + 3 * NT < n4; i += 4 * NT) {
+        float4 v[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        const int pp = lane + kWave * q;
-        v[q] = pp < P ? *reinterpret_cast<const float4*>(base + (int64_t)pp * d)
-                      : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
-    float s[4] = {v[0].x, v[0].y, v[0].z, v[0].w};
+        for (int q = 0; q < 4; ++q) v[q] = base[i + q * NT];
 #pragma unroll
-    for (int q = 1; q < 4; ++q) {
-        s[0] += v[q].x;
-        s[1] += v[q].y;
-        s[2] += v[q].z;
-        s[3] += v[q].w;
+        for (int q = 0; q < 4; ++q) {
+            s[0] += v[q].x;
+            s[1] += v[q].y;
+            s[2] += v[q].z;
+            s[3] += v[q].w;
+        }
     }
-    for (int pp = lane + 4 * kWave; pp < P; pp += kWave) {
-        const float4 t = *reinterpret_cast<const float4*>(base + (int64_t)pp * d);
-        s[0] += t.x;
-        s[1] += t.y;
-        s[2] += t.z;
-        s[3] += t.w;
+    for (; i < n4; i += NT) {
+        const float4 v = base[i];
+        s[0] += v.x;
+        s[1] += v.y;
+        s[2] += v.z;
+        s[3] += v.w;
     }
-    const float tot = wave_transpose_sum<4>(s, lane);
-    if ((lane & 15) == 0) y[(int64_t)b * d + c + (lane >> 4)] = tot;
+#pragma unroll
+    for (int m = 4; m < kWave; m <<= 1)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) s[e] += __shfl_xor(s[e], m, kWave);
+    const int64_t b = pair / nch;
+    const int64_t c0 = (pair % nch) * kChunk;
+    if (WPP == 1) {
+        const int64_t c = c0 + 4 * lane;
+        if (lane < 4 && c < d)  // d is a multiple of 4: the float4 is all in range
+            *reinterpret_cast<float4*>(y + b * d + c) = make_float4(s[0], s[1], s[2], s[3]);
+    } else {
+        __shared__ float red[WPP][kChunk];
+        if (lane < 4) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) red[w][lane * 4 + e] = s[e];
+        }
+        __syncthreads();
+        if (t < kChunk && c0 + t < d) {
+            float a = 0.f;
+#pragma unroll
+            for (int q = 0; q < WPP; ++q) a += red[q][t];
+            y[b * d + c0 + t] = a;
+        }
+    }
 }
 
 // ev0/ev1 (optional): stamped from the kernel's own dispatch (hipExtLaunchKernelGGL), so
@@ -310,6 +439,9 @@ int decode_chunks(int64_t B, int64_t nnz, int num_cu) {
     int64_t target = num_cu / B;
     if (target < 1) target = 1;
     int64_t P = per_tok < target ? per_tok : target;
+    // the kernel's row split uses 32-bit products: nnz * P < 2^32 (nnz itself is below 2^31)
+    const int64_t cap = nnz > 0 ? (int64_t)0xffffffff / nnz : P;
+    if (P > cap) P = cap;
     if (P < 1) P = 1;
     return (int)P;
 }
@@ -344,10 +476,20 @@ hipError_t launch_decode(const void* x, int xdt, int64_t B, int64_t d, const int
 hipError_t launch_reduce_partials(const float* partials, int P, int64_t B, int64_t d, float* y,
                                   hipStream_t s) {
     if (B == 0) return hipSuccess;
-    // one wave per float4 group, four waves per work-group
-    dim3 grid((unsigned)((d + 15) / 16), (unsigned)B);
-    hipLaunchKernelGGL(reduce_partials, grid, dim3(256), 0, s, partials, P, d, y);
+    const int64_t nch = part_chunks(d);
+    const int64_t pairs = B * nch;
+    if (P >= 64) {  // four waves per (token, chunk) pair
+        hipLaunchKernelGGL(reduce_chunks<4>, dim3((unsigned)pairs), dim3(256), 0, s, partials, P,
+                           pairs, nch, d, y);
+    } else {        // one wave per pair, four pairs per work-group
+        hipLaunchKernelGGL(reduce_chunks<1>, dim3((unsigned)((pairs + 3) / 4)), dim3(256), 0, s,
+                           partials, P, pairs, nch, d, y);
+    }
     return hipGetLastError();
+}
+
+size_t decode_workspace(int64_t B, int64_t nnz, int64_t d, int num_cu) {
+    return (size_t)B * decode_chunks(B, nnz, num_cu) * part_chunks(d) * kChunk * sizeof(float);
 }
 
 }  // namespace si

@@ -88,7 +88,7 @@ Plan make_plan(int64_t B, int64_t L, int64_t d, int num_cu) {
     p.off_h = o;
     o = align256(o + (size_t)B * p.Lp * 4);
     p.off_part = o;
-    o = align256(o + (size_t)p.KS * B * d * 4);
+    o = align256(o + (size_t)p.KS * B * part_chunks(d) * kChunk * 4);
     p.total = o;
     return p;
 }
@@ -392,7 +392,9 @@ __global__ __launch_bounds__(256) void union_gemm2(const float* __restrict__ H, 
             buf ^= 1;
         }
     }
-    // accumulator: register i of lane l is (token 4*(l/16) + i, column l % 16) of a subtile
+    // accumulator: register i of lane l is (token 4*(l/16) + i, column l % 16) of a subtile;
+    // the 16 lanes of a row write 64 contiguous bytes of the chunked partial layout
+    const int64_t nch = part_chunks(d);
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -401,7 +403,7 @@ __global__ __launch_bounds__(256) void union_gemm2(const float* __restrict__ H, 
             for (int i = 0; i < 4; ++i) {
                 const int64_t tok = m0 + mt * 16 + 4 * g + i;
                 const int64_t col = c0 + w * 64 + j * 16 + nn;
-                if (tok < B && col < d) part[(tok * KS + ks) * d + col] = acc[mt][j][i];
+                if (tok < B && col < d) part[part_off(tok, ks, col, KS, nch)] = acc[mt][j][i];
             }
 }
 

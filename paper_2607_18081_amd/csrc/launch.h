@@ -11,7 +11,10 @@ namespace si {
 int decode_chunks(int64_t B, int64_t nnz, int num_cu);
 // 0 if the shape is supported, else nonzero.
 int decode_supported(int xdt, int wdt, int64_t d);
-// y[b][c] = sum over p of partials[b][p][c], p in fixed order.
+// Workspace bytes of the per-token path: B * P float32 partials of d columns (chunked layout).
+size_t decode_workspace(int64_t B, int64_t nnz, int64_t d, int num_cu);
+// y[b][c] = sum over p of the partials of token b, column c (column-chunked layout of
+// common.h), p in fixed order.
 hipError_t launch_reduce_partials(const float* partials, int P, int64_t B, int64_t d, float* y,
                                   hipStream_t s);
 hipError_t launch_decode(const void* x, int xdt, int64_t B, int64_t d, const int32_t* offsets,
