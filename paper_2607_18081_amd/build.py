@@ -23,6 +23,10 @@ CFLAGS = [
     "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
     # no packed-FP32 VALU instructions in any kernel
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMAs accumulate in VGPRs: left to its heuristics the compiler keeps the accumulators in
+    # AGPRs but feeds the MFMAs from VGPRs, copying every accumulator in and out around each
+    # MFMA once the tiles use more than 256 registers in all
+    "-mllvm", "-amdgpu-mfma-vgpr-form=1",
     "-I", INCLUDE, "-I", CSRC,
 ]
 

@@ -391,6 +391,29 @@ __global__ __launch_bounds__(256) void reduce_chunks(const float* __restrict__ p
     }
 }
 
+// The same sum for few partials (P < 16): thread i owns float4 group i % 4 of chunk i / 4 (over
+// tokens and chunks) and adds its P float4 values in ascending p.
+__global__ __launch_bounds__(256) void reduce_few(const float* __restrict__ partials, int P,
+                                                  int64_t n4, int64_t nch, int64_t d,
+                                                  float* __restrict__ y) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= n4) return;
+    const int64_t pair = i >> 2;  // (token, chunk)
+    const int q = (int)(i & 3);
+    const float4* base = reinterpret_cast<const float4*>(partials + pair * (int64_t)P * kChunk) + q;
+    float4 s = base[0];
+    for (int p = 1; p < P; ++p) {
+        const float4 v = base[p * (kChunk / 4)];
+        s.x += v.x;
+        s.y += v.y;
+        s.z += v.z;
+        s.w += v.w;
+    }
+    const int64_t b = pair / nch;
+    const int64_t c = (pair % nch) * kChunk + 4 * q;
+    if (c < d) *reinterpret_cast<float4*>(y + b * d + c) = s;  // d % 4 == 0
+}
+
 // ev0/ev1 (optional): stamped from the kernel's own dispatch (hipExtLaunchKernelGGL), so
 // their elapsed time is the kernel's device time without queueing or marker overheads.
 template <typename WT, typename XT, bool BUF>
@@ -478,7 +501,11 @@ hipError_t launch_reduce_partials(const float* partials, int P, int64_t B, int64
     if (B == 0) return hipSuccess;
     const int64_t nch = part_chunks(d);
     const int64_t pairs = B * nch;
-    if (P >= 64) {  // four waves per (token, chunk) pair
+    if (P < 16) {  // one thread per float4 of y: a wave reads 16 chunks' partials contiguously
+        const int64_t n4 = B * nch * (kChunk / 4);
+        hipLaunchKernelGGL(reduce_few, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s,
+                           partials, P, n4, nch, d, y);
+    } else if (P >= 64) {  // four waves per (token, chunk) pair
         hipLaunchKernelGGL(reduce_chunks<4>, dim3((unsigned)pairs), dim3(256), 0, s, partials, P,
                            pairs, nch, d, y);
     } else {        // one wave per pair, four pairs per work-group

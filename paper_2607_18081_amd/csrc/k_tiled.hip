@@ -1,0 +1,492 @@
+// Union path for large batches (prefill-like): LDS-tiled bf16 MFMA gather-GEMMs over an
+// explicit list of the union's slots.
+//
+// The computation is the one of the union path (Selective Computation section; see
+// k_union.hip): with U = A_1 u ... u A_B,
+//   H[b][u] = SiLU(x_b . gate_c[U_u]) * (x_b . up_c[U_u]) * [U_u in A_b],   Y = H . down_c[U].
+// For many tokens the weights are reused across the batch, so both products are compute
+// bound and are tiled for MFMA throughput instead of streamed:
+//  - or_blocks / union_scan: the OR of the token bitmaps per block of 64 tokens, then one
+//    work-group ORs the blocks and turns the union into the ascending list of its slots;
+//  - gemm1_tiled: a work-group computes 256 tokens x 80 union slots, K = d in steps of 64.
+//    The 160 weight rows of its tile are ordered per group of 16 slots as 16 gate rows then
+//    16 up rows, so gate and up of one (token, slot) land in the same lane and register of two
+//    neighbouring MFMA tiles and the SiLU*up*mask epilogue needs no data exchange. Both
+//    operands are K-contiguous rows (token rows of x, neuron rows of gate_up_c) staged in LDS
+//    with a 144-byte pitch, which keeps the 16 rows read by one ds_read_b128 in distinct banks.
+//    H is written as two bf16 planes, hi = bf16(h) and lo = bf16(h - hi).
+//  - gemm2_tiled: Y partials for 256 tokens x 128 columns over one of KS chunks of the union,
+//    K = union position in steps of 64. H rows are K-contiguous; the down rows are staged as
+//    row segments and read back transposed into the MFMA B layout with ds_read_b64_tr_b16.
+//    hi and lo both enter the MFMA (about 16 significant bits of h) unless SI_FLAG_FAST_H.
+//    The KS partials are added in a fixed order by the shared partial reducer.
+// Tiles are loaded with range-checked buffer loads (zeros outside), staged through registers
+// while the previous tile is multiplied out of LDS.
+#include <hip/hip_ext.h>
+
+#include "common.h"
+#include "launch.h"
+
+namespace si {
+
+namespace {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
+typedef __attribute__((ext_vector_type(4))) float f32x4_t;
+typedef __attribute__((ext_vector_type(4))) unsigned int u32x4_t;
+typedef __attribute__((ext_vector_type(4))) short s16x4_t;
+
+__device__ __forceinline__ bf16x8_t as_bf16x8(const V16& v) {
+    const u32x4_t t = {v.w[0], v.w[1], v.w[2], v.w[3]};
+    return __builtin_bit_cast(bf16x8_t, t);
+}
+
+__device__ __forceinline__ f32x4_t mfma16x16x32(const bf16x8_t& a, const bf16x8_t& b,
+                                                const f32x4_t& c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+constexpr int kBK = 64;          // K step (elements)
+constexpr int kKP = kBK + 8;     // LDS pitch (bf16) of K-contiguous tiles: 144 bytes
+constexpr int kT1M = 256;        // GEMM1 tokens per work-group (4 waves x 64)
+constexpr int kT1S = 80;         // GEMM1 union slots per work-group (5 groups of 16)
+constexpr int kT1N = 2 * kT1S;   // GEMM1 weight rows per work-group
+constexpr int kT2M = 256;        // GEMM2 tokens per work-group (2 waves x 128)
+constexpr int kT2N = 128;        // GEMM2 columns per work-group (2 waves x 64)
+constexpr int kT2P = kT2N + 16;  // LDS pitch (bf16) of the down-row tile
+
+// part[c][w] = OR of bits[b][w] over the 64 tokens b of block c. Work-group (wx, c): 64 words
+// x 64 tokens; each wave ORs 16 tokens of the 64 words, then the 4 waves meet in LDS.
+__global__ __launch_bounds__(256) void or_blocks(const uint32_t* __restrict__ bits, int64_t B,
+                                                 int64_t W, uint32_t* __restrict__ part) {
+    const int lane = threadIdx.x & 63;
+    const int wv = threadIdx.x >> 6;
+    const int64_t w = (int64_t)blockIdx.x * 64 + lane;
+    const int64_t b0 = (int64_t)blockIdx.y * 64 + 16 * wv;
+    uint32_t u = 0u;
+    if (w < W) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+            if (b0 + i < B) u |= bits[(b0 + i) * W + w];
+    }
+    __shared__ uint32_t red[4][64];
+    red[wv][lane] = u;
+    __syncthreads();
+    if (wv == 0 && w < W) part[(int64_t)blockIdx.y * W + w] = red[0][lane] | red[1][lane] |
+                                                               red[2][lane] | red[3][lane];
+}
+
+// One work-group: the union of the nb block bitmaps part[0..nb)[W], its set bits in ascending
+// order -> ulist, their number -> *ucount. Thread t owns a contiguous run of words; an
+// exclusive scan of the runs' counts in LDS gives each run its first position.
+__global__ __launch_bounds__(1024) void union_scan(const uint32_t* __restrict__ part, int64_t nb,
+                                                   int64_t W, int32_t* __restrict__ ulist,
+                                                   int* __restrict__ ucount) {
+    __shared__ int cnt[1024];
+    const int t = threadIdx.x;
+    const int64_t per = (W + 1023) / 1024;
+    const int64_t w0 = (int64_t)t * per;
+    const int64_t w1 = (w0 + per < W) ? w0 + per : W;
+    auto word = [&](int64_t w) {
+        uint32_t u = 0u;
+        for (int64_t c = 0; c < nb; ++c) u |= part[c * W + w];
+        return u;
+    };
+    int c = 0;
+    for (int64_t w = w0; w < w1; ++w) c += __popc(word(w));
+    cnt[t] = c;
+    __syncthreads();
+    // Hillis-Steele inclusive scan over 1024 counts
+    for (int off = 1; off < 1024; off <<= 1) {
+        const int v = t >= off ? cnt[t - off] : 0;
+        __syncthreads();
+        cnt[t] += v;
+        __syncthreads();
+    }
+    int pos = cnt[t] - c;
+    for (int64_t w = w0; w < w1; ++w) {
+        uint32_t u = word(w);
+        while (u) {
+            const int j = __ffs(u) - 1;
+            ulist[pos++] = (int32_t)(w * 32 + j);
+            u &= u - 1u;
+        }
+    }
+    if (t == 1023) *ucount = cnt[1023];
+}
+
+// ---- GEMM1 ---------------------------------------------------------------------------------
+// Grid: 8 * ntm * ceil(nst / 8) work-groups of 256 threads. Work-groups 8 apart (same XCD)
+// share a slot tile, so its weight rows are fetched from HBM once per XCD.
+__global__ __launch_bounds__(256) void gemm1_tiled(
+    const bf16_t* __restrict__ x, int64_t B, int64_t d, const bf16_t* __restrict__ gu, int64_t L,
+    const int32_t* __restrict__ ulist, const int* __restrict__ ucount,
+    const uint32_t* __restrict__ bits, int64_t W, bf16_t* __restrict__ Hhi,
+    bf16_t* __restrict__ Hlo, int64_t Up, int ntm) {
+    const int id = blockIdx.x;
+    const int st = (id / (8 * ntm)) * 8 + (id % 8);
+    const int tm = (id / 8) % ntm;
+    const int nU = *ucount;
+    const int64_t u0 = (int64_t)st * kT1S;
+    if (u0 >= nU) return;  // uniform
+    const int64_t m0 = (int64_t)tm * kT1M;
+    const int t = threadIdx.x;
+    const int lane = t & 63;
+    const int w = t >> 6;
+    const int nn = lane & 15;
+    const int g = lane >> 4;
+
+    __shared__ __align__(16) bf16_t sA[kT1M][kKP];
+    __shared__ __align__(16) bf16_t sB[kT1N][kKP];
+
+    // staging: thread t moves 16-byte chunk t % 8 of rows t / 8 + 32 j
+    const int ch = t & 7;
+    const int r0 = t >> 3;
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, B * d * 2);
+    const __amdgpu_buffer_rsrc_t rg = make_rsrc(gu, L * 2 * d * 2);
+    int aoff[8], boff[5];  // byte offset of the row start, or kOOB
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const int64_t tok = m0 + r0 + 32 * j;
+        aoff[j] = tok < B ? (int)(tok * d * 2) : kOOB;
+    }
+#pragma unroll
+    for (int j = 0; j < 5; ++j) {
+        const int r = r0 + 32 * j;              // weight row of the tile
+        const int64_t u = u0 + 16 * (r / 32) + (r % 16);
+        const int plane = (r % 32) / 16;        // 0 gate, 1 up
+        const int32_t slot = u < nU ? ulist[u] : -1;
+        boff[j] = (slot >= 0 && slot < L) ? (int)(((int64_t)slot * 2 + plane) * d * 2) : kOOB;
+    }
+    V16 pa[8], pb[5];
+    auto fetch = [&](int64_t k0) {
+        const int64_t k = k0 + 8 * ch;
+        const bool kin = k < d;  // d % 8 == 0: a chunk is all in or all out
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            pa[j] = bload16(rx, (kin && aoff[j] != kOOB) ? aoff[j] + (int)(k * 2) : kOOB);
+#pragma unroll
+        for (int j = 0; j < 5; ++j)
+            pb[j] = bload16(rg, (kin && boff[j] != kOOB) ? boff[j] + (int)(k * 2) : kOOB);
+    };
+
+    f32x4_t acc[4][10];
+#pragma unroll
+    for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+        for (int nj = 0; nj < 10; ++nj) acc[mi][nj] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+    fetch(0);
+    for (int64_t k0 = 0; k0 < d; k0 += kBK) {
+        __syncthreads();  // the previous tile has been read
+#pragma unroll
+        for (int j = 0; j < 8; ++j) st16(&sA[r0 + 32 * j][8 * ch], pa[j]);
+#pragma unroll
+        for (int j = 0; j < 5; ++j) st16(&sB[r0 + 32 * j][8 * ch], pb[j]);
+        __syncthreads();
+        fetch(k0 + kBK);  // in flight while this tile is used (past the end: reads nothing)
+        // keep the prefetch ahead of the MFMAs (the scheduler would otherwise sink the loads
+        // to the end of the iteration and expose their whole latency at the next LDS store)
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            bf16x8_t a[4];
+#pragma unroll
+            for (int mi = 0; mi < 4; ++mi)
+                a[mi] = as_bf16x8(ld16(&sA[64 * w + 16 * mi + nn][32 * ks + 8 * g]));
+            // B fragments one ahead: the next one's LDS read is in flight during this one's
+            // four MFMAs
+            bf16x8_t bq[2];
+            bq[0] = as_bf16x8(ld16(&sB[nn][32 * ks + 8 * g]));
+#pragma unroll
+            for (int nj = 0; nj < 10; ++nj) {
+                if (nj + 1 < 10)
+                    bq[(nj + 1) & 1] = as_bf16x8(ld16(&sB[16 * (nj + 1) + nn][32 * ks + 8 * g]));
+                const bf16x8_t b = bq[nj & 1];
+#pragma unroll
+                for (int mi = 0; mi < 4; ++mi) acc[mi][nj] = mfma16x16x32(a[mi], b, acc[mi][nj]);
+            }
+        }
+    }
+
+    // epilogue: register i of lane l of tile (mi, nj) is token 64 w + 16 mi + 4 g + i and
+    // weight row 16 nj + nn; tiles 2q and 2q + 1 are gate and up of slots u0 + 16 q + nn
+#pragma unroll
+    for (int q = 0; q < 5; ++q) {
+        const int64_t u = u0 + 16 * q + nn;
+        const int32_t slot = u < nU ? ulist[u] : -1;
+#pragma unroll
+        for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int64_t tok = m0 + 64 * w + 16 * mi + 4 * g + i;
+                if (tok < B && slot >= 0) {
+                    const bool act = (bits[tok * W + slot / 32] >> (slot % 32)) & 1u;
+                    const float h = act ? silu_f32(acc[mi][2 * q][i]) * acc[mi][2 * q + 1][i]
+                                        : 0.0f;
+                    const uint32_t hb = f32_to_bf16_rne(h);
+                    Hhi[tok * Up + u] = (bf16_t)hb;
+                    Hlo[tok * Up + u] = (bf16_t)f32_to_bf16_rne(h - bf16_to_f32(hb));
+                }
+            }
+    }
+}
+
+// ---- GEMM2 ---------------------------------------------------------------------------------
+// Grid: (ceil(d / 128), ceil(B / 256), KS), 256 threads. Partials in the chunked layout.
+__global__ __launch_bounds__(256) void gemm2_tiled(
+    const bf16_t* __restrict__ Hhi, const bf16_t* __restrict__ Hlo, int64_t Up, int64_t B,
+    const bf16_t* __restrict__ dc, int64_t d, int64_t L, const int32_t* __restrict__ ulist,
+    const int* __restrict__ ucount, float* __restrict__ part, int KS, int fast) {
+    const int nU = *ucount;
+    const int ks = blockIdx.z;
+    const int64_t kper = (((int64_t)nU + KS - 1) / KS + kBK - 1) / kBK * kBK;
+    const int64_t kb = (int64_t)ks * kper;
+    const int64_t ke = (kb + kper < nU) ? kb + kper : nU;
+    const int64_t n0 = (int64_t)blockIdx.x * kT2N;
+    const int64_t m0 = (int64_t)blockIdx.y * kT2M;
+    const int t = threadIdx.x;
+    const int lane = t & 63;
+    const int w = t >> 6;
+    const int wm = w >> 1;
+    const int wn = w & 1;
+    const int nn = lane & 15;
+    const int g = lane >> 4;
+
+    __shared__ __align__(16) bf16_t sH[2][kT2M][kKP];
+    __shared__ __align__(16) bf16_t sD[kBK][kT2P];
+
+    // staging of H: chunk t % 8 of rows t / 8 + 32 j; of the down rows: 16-byte chunk t % 16
+    // of union positions t / 16 + 16 j
+    const int ch = t & 7;
+    const int r0 = t >> 3;
+    const int dch = t & 15;
+    const int dr0 = t >> 4;
+    const __amdgpu_buffer_rsrc_t rh = make_rsrc(Hhi, B * Up * 2);
+    const __amdgpu_buffer_rsrc_t rl = make_rsrc(Hlo, B * Up * 2);
+    const __amdgpu_buffer_rsrc_t rd = make_rsrc(dc, L * d * 2);
+    int hoff[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const int64_t tok = m0 + r0 + 32 * j;
+        hoff[j] = tok < B ? (int)(tok * Up * 2) : kOOB;
+    }
+    const int64_t dcol = n0 + 8 * dch;
+    const bool dcol_in = dcol < d;  // d % 8 == 0
+    V16 ph[8], pl[8], pd[4];
+    // slot ids of the down rows of the next fetch, loaded one K step ahead of their use so
+    // the row loads do not wait on them (union positions past the chunk read as -1)
+    const __amdgpu_buffer_rsrc_t ru = make_rsrc(ulist, ke * 4);
+    int32_t sl[4];
+    auto load_slots = [&](int64_t k0) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t u = k0 + dr0 + 16 * j;
+            sl[j] = u < ke ? (int32_t)__builtin_amdgcn_raw_buffer_load_b32(ru, (int)(u * 4), 0, 0)
+                           : -1;
+        }
+    };
+    auto fetch = [&](int64_t k0) {
+        const int64_t k = k0 + 8 * ch;  // 8 union positions of one chunk
+        const int64_t nv = ke - k;      // valid positions in the chunk, if below 8
+        // H past the chunk's K range is not part of this sum: zero it (branch-free)
+        uint32_t keep[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            keep[e] = (2 * e + 1 < nv) ? 0xffffffffu : (2 * e < nv ? 0x0000ffffu : 0u);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int off = (nv > 0 && hoff[j] != kOOB) ? hoff[j] + (int)(k * 2) : kOOB;
+            ph[j] = bload16(rh, off);
+            pl[j] = bload16(rl, fast ? kOOB : off);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                ph[j].w[e] &= keep[e];
+                pl[j].w[e] &= keep[e];
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            pd[j] = bload16(rd, (sl[j] >= 0 && sl[j] < L && dcol_in)
+                                    ? (int)(((int64_t)sl[j] * d + dcol) * 2)
+                                    : kOOB);
+        load_slots(k0 + kBK);
+    };
+
+    f32x4_t acc[8][4];
+#pragma unroll
+    for (int mi = 0; mi < 8; ++mi)
+#pragma unroll
+        for (int nj = 0; nj < 4; ++nj) acc[mi][nj] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+    if (kb < ke) {
+        load_slots(kb);
+        fetch(kb);
+    }
+    for (int64_t k0 = kb; k0 < ke; k0 += kBK) {
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            st16(&sH[0][r0 + 32 * j][8 * ch], ph[j]);
+            st16(&sH[1][r0 + 32 * j][8 * ch], pl[j]);
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) st16(&sD[dr0 + 16 * j][8 * dch], pd[j]);
+        __syncthreads();
+        fetch(k0 + kBK);  // past the end of the chunk: reads nothing
+        __builtin_amdgcn_sched_barrier(0);  // the prefetch stays ahead of the MFMAs
+#pragma unroll
+        for (int ks2 = 0; ks2 < 2; ++ks2) {
+            // B operand: lane (nn, g) needs union positions 8 g .. 8 g + 7 of column nn of a
+            // 16-column subtile; ds_read_b64_tr_b16 hands lane i of a 16-lane group element
+            // i % 4 of the 8-byte pieces addressed by lanes i / 4 + 4 j, so lane nn addresses
+            // position 8 g + nn / 4 (and + 4), columns 4 (nn % 4) .. + 3 of the subtile.
+            bf16x8_t bop[4];
+#pragma unroll
+            for (int nj = 0; nj < 4; ++nj) {
+                const int col = 64 * wn + 16 * nj + 4 * (nn & 3);
+                const int row = 32 * ks2 + 8 * g + (nn >> 2);
+                const s16x4_t lo4 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (__attribute__((address_space(3))) s16x4_t*)&sD[row][col]);
+                const s16x4_t hi4 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (__attribute__((address_space(3))) s16x4_t*)&sD[row + 4][col]);
+                const uint32_t p0 = (uint16_t)lo4[0] | ((uint32_t)(uint16_t)lo4[1] << 16);
+                const uint32_t p1 = (uint16_t)lo4[2] | ((uint32_t)(uint16_t)lo4[3] << 16);
+                const uint32_t p2 = (uint16_t)hi4[0] | ((uint32_t)(uint16_t)hi4[1] << 16);
+                const uint32_t p3 = (uint16_t)hi4[2] | ((uint32_t)(uint16_t)hi4[3] << 16);
+                bop[nj] = as_bf16x8(V16{{p0, p1, p2, p3}});
+            }
+            // A fragments (hi, lo) one row-tile ahead of their MFMAs
+            bf16x8_t ah[2], al[2];
+            ah[0] = as_bf16x8(ld16(&sH[0][128 * wm + nn][32 * ks2 + 8 * g]));
+            al[0] = as_bf16x8(ld16(&sH[1][128 * wm + nn][32 * ks2 + 8 * g]));
+#pragma unroll
+            for (int mi = 0; mi < 8; ++mi) {
+                if (mi + 1 < 8) {
+                    const int row = 128 * wm + 16 * (mi + 1) + nn;
+                    ah[(mi + 1) & 1] = as_bf16x8(ld16(&sH[0][row][32 * ks2 + 8 * g]));
+                    al[(mi + 1) & 1] = as_bf16x8(ld16(&sH[1][row][32 * ks2 + 8 * g]));
+                }
+#pragma unroll
+                for (int nj = 0; nj < 4; ++nj)
+                    acc[mi][nj] = mfma16x16x32(ah[mi & 1], bop[nj], acc[mi][nj]);
+                if (!fast) {
+#pragma unroll
+                    for (int nj = 0; nj < 4; ++nj)
+                        acc[mi][nj] = mfma16x16x32(al[mi & 1], bop[nj], acc[mi][nj]);
+                }
+            }
+        }
+    }
+
+    // register i of lane l of tile (mi, nj): token 128 wm + 16 mi + 4 g + i, column
+    // 64 wn + 16 nj + nn; the 16 lanes of a row write 64 contiguous bytes
+    const int64_t nch = part_chunks(d);
+#pragma unroll
+    for (int mi = 0; mi < 8; ++mi)
+#pragma unroll
+        for (int nj = 0; nj < 4; ++nj)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int64_t tok = m0 + 128 * wm + 16 * mi + 4 * g + i;
+                const int64_t col = n0 + 64 * wn + 16 * nj + nn;
+                if (tok < B && col < d) part[part_off(tok, ks, col, KS, nch)] = acc[mi][nj][i];
+            }
+}
+
+struct TPlan {
+    int64_t W, Lp, Up;
+    int ntm1, nst, ntm2, ntn2, KS;
+    int64_t nb;  // blocks of 64 tokens
+    size_t off_bits, off_words, off_ulist, off_count, off_hhi, off_hlo, off_part, total;
+};
+
+size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+TPlan make_tplan(int64_t B, int64_t L, int64_t d, int num_cu) {
+    TPlan p;
+    p.W = (L + 31) / 32;
+    p.Lp = p.W * 32;
+    p.Up = (L + kBK - 1) / kBK * kBK;
+    p.ntm1 = (int)((B + kT1M - 1) / kT1M);
+    p.nst = (int)((L + kT1S - 1) / kT1S);
+    p.ntm2 = (int)((B + kT2M - 1) / kT2M);
+    p.ntn2 = (int)((d + kT2N - 1) / kT2N);
+    const int64_t tiles = (int64_t)p.ntm2 * p.ntn2;
+    int64_t ks = num_cu / tiles;  // whole rounds only: one wave of work-groups per CU
+    if (ks < 1) ks = 1;
+    const int64_t kmax = (L + kBK - 1) / kBK;
+    if (ks > kmax) ks = kmax;
+    if (ks > 64) ks = 64;
+    p.KS = (int)ks;
+    size_t o = 0;
+    p.off_bits = o;
+    o = align256(o + (size_t)B * p.W * 4);
+    p.nb = (B + 63) / 64;
+    p.off_words = o;
+    o = align256(o + (size_t)p.nb * p.W * 4);
+    p.off_ulist = o;
+    o = align256(o + (size_t)p.Lp * 4);
+    p.off_count = o;
+    o = align256(o + 4);
+    p.off_hhi = o;
+    o = align256(o + (size_t)B * p.Up * 2);
+    p.off_hlo = o;
+    o = align256(o + (size_t)B * p.Up * 2);
+    p.off_part = o;
+    o = align256(o + (size_t)p.KS * B * part_chunks(d) * kChunk * 4);
+    p.total = o;
+    return p;
+}
+
+}  // namespace
+
+bool tiled_supported(int64_t B, int64_t L, int64_t d) {
+    const int64_t Up = (L + kBK - 1) / kBK * kBK;
+    const int64_t lim = (int64_t)1 << 31;
+    // 32-bit buffer offsets; the token bitmaps are built in LDS (at most 64 KB)
+    return L * 2 * d * 2 < lim && B * d * 2 < lim && B * Up * 2 < lim && L <= 524288;
+}
+
+size_t tiled_workspace(int64_t B, int64_t L, int64_t d, int num_cu) {
+    return make_tplan(B, L, d, num_cu).total;
+}
+
+hipError_t launch_union_tiled(const void* x, int64_t B, int64_t d, const int32_t* offsets,
+                              const int32_t* idx, int64_t nnz, const void* gate_up_c,
+                              const void* down_c, int64_t L, float* y, void* ws, int flags,
+                              int num_cu, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+    const TPlan p = make_tplan(B, L, d, num_cu);
+    uint8_t* base = static_cast<uint8_t*>(ws);
+    uint32_t* bits = reinterpret_cast<uint32_t*>(base + p.off_bits);
+    uint32_t* words = reinterpret_cast<uint32_t*>(base + p.off_words);
+    int32_t* ulist = reinterpret_cast<int32_t*>(base + p.off_ulist);
+    int* ucount = reinterpret_cast<int*>(base + p.off_count);
+    bf16_t* hhi = reinterpret_cast<bf16_t*>(base + p.off_hhi);
+    bf16_t* hlo = reinterpret_cast<bf16_t*>(base + p.off_hlo);
+    float* part = reinterpret_cast<float*>(base + p.off_part);
+    const bf16_t* xx = static_cast<const bf16_t*>(x);
+    const bf16_t* gu = static_cast<const bf16_t*>(gate_up_c);
+    const bf16_t* dc = static_cast<const bf16_t*>(down_c);
+
+    hipError_t e = launch_token_bitmaps(offsets, idx, nnz, B, L, p.W, bits, s);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(or_blocks, dim3((unsigned)((p.W + 63) / 64), (unsigned)p.nb), dim3(256), 0,
+                       s, bits, B, p.W, words);
+    hipLaunchKernelGGL(union_scan, dim3(1), dim3(1024), 0, s, words, p.nb, p.W, ulist, ucount);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int nst8 = (p.nst + 7) / 8 * 8;
+    hipExtLaunchKernelGGL(gemm1_tiled, dim3((unsigned)(nst8 * p.ntm1)), dim3(256), 0, s, ev0,
+                          nullptr, 0, xx, B, d, gu, L, ulist, ucount, bits, p.W, hhi, hlo, p.Up,
+                          p.ntm1);
+    const int fast = (flags & 4) ? 1 : 0;
+    hipExtLaunchKernelGGL(gemm2_tiled, dim3((unsigned)p.ntn2, (unsigned)p.ntm2, (unsigned)p.KS),
+                          dim3(256), 0, s, nullptr, ev1, 0, hhi, hlo, p.Up, B, dc, d, L, ulist,
+                          ucount, part, p.KS, fast);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_reduce_partials(part, p.KS, B, d, y, s);
+}
+
+}  // namespace si

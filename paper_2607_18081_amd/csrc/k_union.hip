@@ -409,6 +409,22 @@ __global__ __launch_bounds__(256) void union_gemm2(const float* __restrict__ H, 
 
 }  // namespace
 
+hipError_t launch_token_bitmaps(const int32_t* offsets, const int32_t* idx, int64_t nnz,
+                                int64_t B, int64_t L, int64_t W, uint32_t* bits, hipStream_t s) {
+    hipLaunchKernelGGL(token_bitmaps, dim3((unsigned)B), dim3(256), (size_t)W * 4, s, offsets,
+                       idx, nnz, L, W, bits);
+    return hipGetLastError();
+}
+
+// batches from which the LDS-tiled GEMMs (k_tiled.hip) take over: below, the weights are
+// streamed once and the row-word kernels here are bandwidth bound; above, reuse across the
+// batch makes the products compute bound
+constexpr int64_t kTiledMinB = 128;
+
+static bool use_tiled(int64_t B, int64_t L, int64_t d) {
+    return B >= kTiledMinB && tiled_supported(B, L, d);
+}
+
 bool union_supported(int64_t B, int64_t L, int64_t d) {
     // buffer loads take 32-bit byte offsets
     return L * 2 * d * 2 < ((int64_t)1 << 31) && B * d * 2 < ((int64_t)1 << 31) &&
@@ -416,6 +432,7 @@ bool union_supported(int64_t B, int64_t L, int64_t d) {
 }
 
 size_t union_workspace(int64_t B, int64_t L, int64_t d, int num_cu) {
+    if (use_tiled(B, L, d)) return tiled_workspace(B, L, d, num_cu);
     return make_plan(B, L, d, num_cu).total;
 }
 
@@ -423,6 +440,9 @@ hipError_t launch_union(const void* x, int64_t B, int64_t d, const int32_t* offs
                         const int32_t* idx, int64_t nnz, const void* gate_up_c,
                         const void* down_c, int64_t L, float* y, void* ws, int flags,
                         int num_cu, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+    if (use_tiled(B, L, d))
+        return launch_union_tiled(x, B, d, offsets, idx, nnz, gate_up_c, down_c, L, y, ws, flags,
+                                  num_cu, s, ev0, ev1);
     const Plan p = make_plan(B, L, d, num_cu);
     uint8_t* base = static_cast<uint8_t*>(ws);
     uint32_t* bits = reinterpret_cast<uint32_t*>(base + p.off_bits);
@@ -433,9 +453,7 @@ hipError_t launch_union(const void* x, int64_t B, int64_t d, const int32_t* offs
     const bf16_t* gu = static_cast<const bf16_t*>(gate_up_c);
     const bf16_t* dc = static_cast<const bf16_t*>(down_c);
 
-    hipLaunchKernelGGL(token_bitmaps, dim3((unsigned)B), dim3(256), (size_t)p.W * 4, s, offsets,
-                       idx, nnz, L, p.W, bits);
-    hipError_t e = hipGetLastError();
+    hipError_t e = launch_token_bitmaps(offsets, idx, nnz, B, L, p.W, bits, s);
     if (e != hipSuccess) return e;
     const dim3 g1((unsigned)p.W, (unsigned)((B + 16 * p.MT1 - 1) / (16 * p.MT1)));
 #define SI_G1(M)                                                                                \

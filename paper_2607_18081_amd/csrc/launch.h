@@ -31,6 +31,19 @@ hipError_t launch_union(const void* x, int64_t B, int64_t d, const int32_t* offs
                         const void* down_c, int64_t L, float* y, void* ws, int flags,
                         int num_cu, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 
+// one bitmap of L bits per token (W = ceil(L / 32) words): bit s of token b is set iff slot s
+// is in the token's active list
+hipError_t launch_token_bitmaps(const int32_t* offsets, const int32_t* idx, int64_t nnz,
+                                int64_t B, int64_t L, int64_t W, uint32_t* bits, hipStream_t s);
+
+// ---- k_tiled.hip: union path for large batches (LDS-tiled MFMA GEMMs) ----------------------
+bool tiled_supported(int64_t B, int64_t L, int64_t d);
+size_t tiled_workspace(int64_t B, int64_t L, int64_t d, int num_cu);
+hipError_t launch_union_tiled(const void* x, int64_t B, int64_t d, const int32_t* offsets,
+                              const int32_t* idx, int64_t nnz, const void* gate_up_c,
+                              const void* down_c, int64_t L, float* y, void* ws, int flags,
+                              int num_cu, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
+
 // ---- k_topk.hip ---------------------------------------------------------------------------
 hipError_t launch_topk(const float* scores, int64_t B, int64_t L, int64_t k, int mode,
                        int32_t* out, hipStream_t s);

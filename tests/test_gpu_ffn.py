@@ -132,6 +132,39 @@ def test_union_path_ragged(B, d):
     assert max_rel_l2(fast, want) <= TOL["bf16"]
 
 
+@pytest.mark.parametrize("B,d,L,sparse", [(128, 264, 613, False), (257, 1000, 300, False),
+                                           (300, 264, 613, True), (130, 64, 81, False)])
+def test_union_tiled_ragged(B, d, L, sparse):
+    """Batches of 128 tokens and more take the LDS-tiled GEMMs: ragged token, slot and K tiles,
+    a union much smaller than L (sparse), split-K tails, empty sets."""
+    N = L + 97
+    say(f"union tiled B={B} d={d} L={L} sparse={sparse}")
+    rng, draw, ref, gpu = _rand_problem(B * 7 + d + L, N, d, L, "bf16")
+    pool = rng.permutation(L)[:max(1, L // 5)] if sparse else np.arange(L)
+    sets = []
+    for b in range(B):
+        if b % 9 == 4:
+            k = 0
+        else:
+            k = int(rng.integers(1, len(pool) + 1))
+        sets.append(np.sort(rng.permutation(pool)[:k]).astype(np.int32))
+    x = draw(B, d, scale=1.0)
+    want = _oracle(x, sets, ref)
+    got = _run(x, sets, gpu)
+    for b in range(B):
+        if len(sets[b]) == 0:
+            assert not np.any(got[b])
+    err = max_rel_l2(got, want)
+    say(f"  hi+lo max rel L2 {err:.3e}")
+    assert err <= 1e-4          # h enters the MFMA as a bf16 hi + lo pair: ~16 bits
+    fast = _run(x, sets, gpu, flags=si.FLAG_FAST_H)
+    errf = max_rel_l2(fast, want)
+    say(f"  hi only max rel L2 {errf:.3e}")
+    assert errf <= TOL["bf16"]
+    again = _run(x, sets, gpu)
+    assert np.array_equal(got, again)   # fixed-order reductions: bitwise reproducible
+
+
 def test_llama2_7b_batch16_union():
     cfg, ref, gpu = _layer("llama2_7b_b16")
     say("7B batch-16 union path: 2 steps of 16 tokens")
