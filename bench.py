@@ -324,9 +324,9 @@ def main():
     args = parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; the multi-GPU sharding "
-                                   "of the path is a design (see DESIGN.md), not an executable "
-                                   "path", "n_gpus": args.gpus}))
+        print(json.dumps({"error": "this benchmark runs on one GPU only: sharding the path "
+                                   "across GPUs is designed but not implemented",
+                          "n_gpus": args.gpus}))
         sys.exit(2)
     import numpy as np
     import torch
