@@ -24,3 +24,11 @@ from .ffn import (  # noqa: F401
     silu,
     stack_step,
 )
+from .selection import (  # noqa: F401
+    activations,
+    dynamic_set,
+    merge_scores,
+    profile_scores,
+    rank_neurons,
+    select_dynamic,
+)

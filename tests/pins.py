@@ -292,5 +292,106 @@ def pin_memory(impl):
     assert impl.compacted_bytes(d, L, 2) == 189_382_656
 
 
+# --------------------------------------------------------------------------------------------
+# Neuron selection (Selective Computation section) and the profiler score (Eq. 1)
+# --------------------------------------------------------------------------------------------
+def _lib_activations(X, wg, wu):
+    """Library reference: SiLU(X W_gate^T) * (X W_up^T) with NumPy matmul and SciPy's logistic."""
+    from scipy.special import expit
+
+    Xf = _f64(X)
+    G = Xf @ _f64(wg).T
+    U = Xf @ _f64(wu).T
+    return G * expit(G) * U
+
+
+def _gu(wg, wu):
+    return np.stack([np.stack([wg[n], wu[n]]) for n in range(wg.shape[0])])
+
+
+def pin_activations(impl):
+    for wdtype in ("f32", "bf16"):
+        rng = np.random.default_rng(11)
+        wg, wu, wd, _ = _problem(12, 23, 10, wdtype)
+        X = (rng.standard_normal((5, 10)) * 0.7).astype(np.float32)
+        A = impl.activations(X, _gu(wg, wu))
+        assert A.shape == (5, 23)
+        assert _rel(A, _lib_activations(X, wg, wu)) <= 1e-13
+
+
+# hand example: per-token top-2 by |a| (ties to the lower index), frequency over the 3 tokens
+_HAND_A = np.array([[0.1, -5.0, 3.0, 0.0, 2.0, -0.5],    # top-2 {1, 2}
+                    [4.0, 1.0, -1.0, 6.0, 0.2, 0.3],     # top-2 {0, 3}
+                    [-2.0, 2.0, 0.5, 0.0, 7.0, 1.0]])    # top-2 {0, 4}: |-2| = |2|, lower wins
+_HAND_COUNTS = [2, 1, 1, 1, 1, 0]
+
+
+def _dyn_properties(impl, A, static, alpha, n_total):
+    """Checks of a dynamic-set result that do not restate the oracle's steps."""
+    out, counts = impl.select_dynamic(A, static, alpha, n_total)
+    out = [int(v) for v in out]
+    T, L = A.shape
+    ref = np.zeros(L, dtype=np.int64)
+    for t in range(T):
+        for j in _topk_bruteforce(A[t], alpha, "abs"):
+            ref[j] += 1
+    assert np.array_equal(np.asarray(counts), ref)
+    assert out == sorted(set(out)) and len(out) == n_total
+    assert set(static) <= set(out)
+    dyn = [j for j in out if j not in static]
+    rest = [j for j in range(L) if j not in out]
+    for i in dyn:
+        for j in rest:
+            assert (ref[i], -i) > (ref[j], -j)
+
+
+def pin_dynamic_set(impl):
+    out, counts = impl.select_dynamic(_HAND_A, [5], 2, 3)
+    assert [int(v) for v in out] == [0, 1, 5]
+    assert [int(v) for v in counts] == _HAND_COUNTS
+    out, _ = impl.select_dynamic(_HAND_A, [0], 2, 4)
+    assert [int(v) for v in out] == [0, 1, 2, 3]
+    out, _ = impl.select_dynamic(_HAND_A, [], 6, 6)          # alpha = L: every slot
+    assert [int(v) for v in out] == list(range(6))
+    rng = np.random.default_rng(5)
+    for T, L, alpha, ns, n_total in [(7, 20, 5, 3, 9), (1, 12, 4, 2, 5), (9, 16, 1, 0, 4)]:
+        A = rng.standard_normal((T, L))
+        A[:, rng.integers(0, L, 3)] = 0.5                      # exact ties in |a|
+        static = sorted(rng.permutation(L)[:ns].tolist())
+        _dyn_properties(impl, A, static, alpha, n_total)
+    # from a prompt: the activations are the library's
+    wg, wu, _, _ = _problem(13, 18, 8, "bf16")
+    X = (rng.standard_normal((6, 8))).astype(np.float32)
+    got, _ = impl.dynamic_set(X, _gu(wg, wu), [2, 9], 4, 7)
+    want, _ = impl.select_dynamic(_lib_activations(X, wg, wu), [2, 9], 4, 7)
+    assert np.array_equal(got, want)
+    for bad in (dict(static_slots=[1, 1], alpha=2, n_total=3),
+                dict(static_slots=[0, 1, 2], alpha=2, n_total=2),
+                dict(static_slots=[7], alpha=2, n_total=3)):
+        try:
+            impl.select_dynamic(_HAND_A, bad["static_slots"], bad["alpha"], bad["n_total"])
+        except Exception:
+            continue
+        raise AssertionError(f"accepted {bad}")
+
+
+def pin_profile_scores(impl):
+    wg, wu, _, _ = _problem(14, 21, 12, "bf16")
+    rng = np.random.default_rng(6)
+    X = rng.standard_normal((9, 12)).astype(np.float32)
+    s, T = impl.profile_scores(X, _gu(wg, wu))
+    assert T == 9
+    assert _rel(s, np.abs(_lib_activations(X, wg, wu)).sum(axis=0)) <= 1e-13
+    s2, T2 = impl.profile_scores(np.concatenate([X, X]), _gu(wg, wu))
+    assert T2 == 18 and _rel(s2, 2 * s) <= 1e-14
+    # merging normalises each file by its token count
+    m = impl.merge_scores([(np.array([2.0, 4.0]), 2), (np.array([3.0, 0.0]), 3)])
+    assert np.allclose(m, [2.0, 2.0], rtol=0, atol=1e-15)
+    assert _rel(impl.merge_scores([(s, T), (s2, T2)]), 2 * s / T) <= 1e-14
+    # ranking: decreasing score, ties to the lower index, NaN last
+    assert [int(v) for v in impl.rank_neurons([1.0, 3.0, 3.0, 0.5])] == [1, 2, 0, 3]
+    assert [int(v) for v in impl.rank_neurons([float("nan"), 0.0, -1.0])] == [1, 2, 0]
+
+
 ALL_PINS = [pin_silu, pin_topk, pin_compact, pin_remap, pin_ffn_invariants, pin_hand_integer,
-            pin_rmsnorm, pin_memory]
+            pin_rmsnorm, pin_memory, pin_activations, pin_dynamic_set, pin_profile_scores]

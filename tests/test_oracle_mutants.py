@@ -110,7 +110,58 @@ def _saving_wrong(n, rl, rlay, s):
     return n * rl * rlay * s
 
 
+from oracle import selection as S
+
+
+def _dyn_with(per_token_mode="abs", freq_high_ties=False, exclude_static=True, first_token_only=False):
+    def f(A, static_slots, alpha, n_total, mode="abs"):
+        A = np.asarray(A, float)
+        T, L = A.shape
+        static = [int(v) for v in np.asarray(static_slots).reshape(-1).tolist()]
+        if len(set(static)) != len(static) or any(v < 0 or v >= L for v in static):
+            raise ValueError
+        if n_total < len(static) or n_total > L:
+            raise ValueError
+        counts = np.zeros(L, np.int64)
+        for t in range(1 if first_token_only else T):
+            for j in O.select_topk(A[t], alpha, per_token_mode).tolist():
+                counts[j] += 1
+        keys = counts.astype(float)
+        if exclude_static:
+            keys[static] = -1.0
+        order = sorted(range(L), key=lambda j: (-keys[j], -j if freq_high_ties else j))
+        dyn = order[:n_total - len(static)]
+        return np.array(sorted(set(static) | set(dyn)), np.int32), counts
+    return f
+
+
+def _act_swapped(X, gate_up_c):
+    sw = gate_up_c[:, ::-1].copy()
+    return S.activations(X, sw)
+
+
+def _profile_signed(X, gate_up):
+    A = S.activations(X, gate_up)
+    return A.sum(axis=0), A.shape[0]
+
+
+def _merge_no_norm(files):
+    return sum(np.asarray(s, float) for s, _ in files)
+
+
+def _rank_ascending(scores):
+    return S.rank_neurons(scores)[::-1].copy()
+
+
 MUTANTS = {
+    "dyn_raw_key": dict(select_dynamic=_dyn_with(per_token_mode="raw")),
+    "dyn_freq_high_index_ties": dict(select_dynamic=_dyn_with(freq_high_ties=True)),
+    "dyn_static_not_excluded": dict(select_dynamic=_dyn_with(exclude_static=False)),
+    "dyn_first_token_only": dict(select_dynamic=_dyn_with(first_token_only=True)),
+    "activations_gate_up_swapped": dict(activations=_act_swapped),
+    "profile_signed": dict(profile_scores=_profile_signed),
+    "merge_not_normalised": dict(merge_scores=_merge_no_norm),
+    "rank_ascending": dict(rank_neurons=_rank_ascending),
     "silu_sign": dict(silu=_silu_wrong_sign,
                       selective_ffn=_ffn_with(lambda g, u: _silu_wrong_sign(g) * u)),
     "drop_up": dict(selective_ffn=_ffn_with(lambda g, u: O.silu(g))),
