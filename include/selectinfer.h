@@ -146,7 +146,8 @@ size_t si_selective_ffn_workspace(int64_t B, int64_t nnz, int64_t L, int64_t d,
  *     down rows into float32 partial sums that a second kernel adds in a fixed order;
  *   - union (B >= 2, bf16 weights and x): the union of the B active sets is built on the
  *     device and both projections run as bf16 MFMA gather-GEMMs over the union rows, with
- *     each token's h masked to its own set. Each union row is read from HBM once per call.
+ *     each token's h masked to its own set; below 128 tokens the union rows are streamed
+ *     once (bandwidth bound), from 128 tokens on the products are LDS-tiled (compute bound).
  * Requirements: d % 8 == 0 for bf16 data, d % 4 == 0 for f32; d <= 32768 (bf16) or 16384
  * (f32); 16-byte aligned x, gate_up_c, down_c, y and ws; B >= 0; nnz >= 0; L >= 1.
  * SI_FLAG_CHECK validates offsets (non-decreasing, within [0, nnz]), slot range and duplicates
@@ -179,6 +180,70 @@ int si_set_timing_events(void* start, void* stop);
  */
 int si_residual_rmsnorm(const void* x, si_dtype xdt, const float* y, int64_t B, int64_t d,
                         float eps, void* x_out, void* hip_stream);
+
+/*
+ * Dynamic-set construction (Selective Computation section) for one prompt of T tokens over a
+ * compacted layer:
+ *   1. a_t[j] = SiLU(gate_c[j] . x[t]) * (up_c[j] . x[t]) for every loaded slot j (float32);
+ *   2. per token, the alpha slots with the largest |a_t[j]| (equal keys to the lower slot,
+ *      -0 = +0, NaN last), as in si_select_topk;
+ *   3. counts[j] = number of the T per-token lists that hold j;
+ *   4. the n_total - n_static slots outside the static set with the largest count (equal
+ *      counts to the lower slot), joined with the static slots.
+ *
+ *   x            [T][d]     prompt activations, dtype xdt
+ *   gate_up_c    [L][2][d]  compacted layer, dtype wdt
+ *   static_slots [n_static] int32 slots always computed (the base neurons), unique, in [0, L)
+ *   out_slots    [n_total]  int32 out: the per-prompt active set, ascending
+ *   counts       [L]        int32 out, optional (NULL: kept in the workspace)
+ *   ws                      workspace of at least si_dynamic_set_workspace(...) bytes
+ *
+ * Requires 0 <= alpha <= L, 0 <= n_static <= n_total <= L <= 2^24, T >= 0, d >= 1, 16-byte
+ * aligned x and gate_up_c. Static slots out of range are ignored; repeated static slots leave
+ * the result shorter than n_total (unspecified tail). Asynchronous, stream-ordered.
+ */
+size_t si_dynamic_set_workspace(int64_t T, int64_t L, int64_t alpha, int64_t n_total);
+int si_dynamic_set(const void* x, si_dtype xdt, int64_t T, int64_t d,
+                   const void* gate_up_c, int64_t L, si_dtype wdt,
+                   const int32_t* static_slots, int64_t n_static,
+                   int64_t alpha, int64_t n_total,
+                   int32_t* out_slots, int32_t* counts,
+                   void* ws, size_t ws_bytes, void* hip_stream);
+
+/*
+ * Profiler scores (LLM Profiler section, Eq. 1): scores[n] += sum over the T tokens of
+ * |a_n(t)|, a_n(t) = SiLU(gate[n] . x[t]) * (up[n] . x[t]), for the N neurons of a full FFN
+ * layer held in the compacted layout (si_compact_ffn with every neuron loaded).
+ *
+ *   x [T][d] (xdt);  gate_up [N][2][d] (wdt);  scores [N] float32, accumulated in place, so
+ *   batches of tokens add up (the caller keeps the token count);  ws of at least
+ *   si_profile_scores_workspace(...) bytes.
+ *
+ * Sums are float32, in a fixed order (bitwise reproducible). Requires d >= 1, N >= 1, 16-byte
+ * aligned x and gate_up. Asynchronous, stream-ordered.
+ */
+size_t si_profile_scores_workspace(int64_t T, int64_t N, int64_t d, si_dtype xdt, si_dtype wdt);
+int si_profile_scores(const void* x, si_dtype xdt, int64_t T, int64_t d,
+                      const void* gate_up, int64_t N, si_dtype wdt,
+                      float* scores, void* ws, size_t ws_bytes, void* hip_stream);
+
+/*
+ * Merging score files (LLM Profiler section): out[n] = sum over files f of
+ * scores[f][n] / tokens[f], files added in order.
+ *
+ *   scores [F][N] float32 (device);  tokens [F] int64 token counts, HOST memory, each >= 1;
+ *   out [N] float32 (device; may not alias scores).  Requires F >= 1, N >= 1.
+ */
+int si_merge_scores(const float* scores, const int64_t* tokens, int64_t F, int64_t N,
+                    float* out, void* hip_stream);
+
+/*
+ * Ranking (LLM Profiler section): order[r] = the neuron with the r-th largest score; equal
+ * scores keep the lower index first, -0 = +0, NaN ranks last.
+ *
+ *   scores [N] float32;  order [N] int32 out.  Requires 1 <= N <= 2^24.
+ */
+int si_rank_neurons(const float* scores, int64_t N, int32_t* order, void* hip_stream);
 
 #ifdef __cplusplus
 }

@@ -14,6 +14,10 @@ from .api import (  # noqa: F401
     CompactLayer,
     SelectInferError,
     compact_ffn,
+    dynamic_set,
+    merge_scores,
+    profile_scores,
+    rank_neurons,
     remap_ids,
     residual_rmsnorm,
     select_topk,

@@ -29,6 +29,14 @@ SIGNATURES = {
     "si_set_timing_events": (c_int, [c_vp, c_vp]),
     "si_residual_rmsnorm": (c_int, [c_vp, c_int, c_vp, c_i64, c_i64, ctypes.c_float, c_vp,
                                     c_vp]),
+    "si_dynamic_set_workspace": (c_size, [c_i64, c_i64, c_i64, c_i64]),
+    "si_dynamic_set": (c_int, [c_vp, c_int, c_i64, c_i64, c_vp, c_i64, c_int, c_vp, c_i64, c_i64,
+                               c_i64, c_vp, c_vp, c_vp, c_size, c_vp]),
+    "si_profile_scores_workspace": (c_size, [c_i64, c_i64, c_i64, c_int, c_int]),
+    "si_profile_scores": (c_int, [c_vp, c_int, c_i64, c_i64, c_vp, c_i64, c_int, c_vp, c_vp,
+                                  c_size, c_vp]),
+    "si_merge_scores": (c_int, [c_vp, c_vp, c_i64, c_i64, c_vp, c_vp]),
+    "si_rank_neurons": (c_int, [c_vp, c_i64, c_vp, c_vp]),
 }
 
 _lib = None

@@ -197,3 +197,71 @@ def residual_rmsnorm(x: torch.Tensor, y: torch.Tensor, eps: float = 1e-5,
                                     _stream(dev))
     _check(st, "si_residual_rmsnorm")
     return out
+
+
+def dynamic_set(x: torch.Tensor, gate_up_c: torch.Tensor, static_slots: torch.Tensor,
+                alpha: int, n_total: int, workspace: torch.Tensor | None = None):
+    """si_dynamic_set: a prompt x [T][d] over a compacted layer -> (active slots [n_total]
+    ascending, counts [L]: how many of the T per-token top-alpha lists hold each slot)."""
+    dev = _dev(gate_up_c)
+    T, d = x.shape
+    L = gate_up_c.shape[0]
+    if gate_up_c.shape != (L, 2, d):
+        raise ValueError("gate_up_c must be [L][2][d]")
+    if static_slots.dtype != torch.int32:
+        raise ValueError("static_slots must be int32")
+    out = torch.empty(n_total, dtype=torch.int32, device=dev)
+    counts = torch.empty(L, dtype=torch.int32, device=dev)
+    lib = load()
+    need = int(lib.si_dynamic_set_workspace(T, L, alpha, n_total))
+    if workspace is None:
+        workspace = _workspace(dev, need)
+    st = lib.si_dynamic_set(_ptr(x), _dt(x), T, d, _ptr(gate_up_c), L, _dt(gate_up_c),
+                            _ptr(static_slots), static_slots.numel(), alpha, n_total, _ptr(out),
+                            _ptr(counts), _ptr(workspace), workspace.numel(), _stream(dev))
+    _check(st, "si_dynamic_set")
+    return out, counts
+
+
+def profile_scores(x: torch.Tensor, gate_up: torch.Tensor, scores: torch.Tensor | None = None,
+                   workspace: torch.Tensor | None = None) -> torch.Tensor:
+    """si_profile_scores: scores [N] += sum over the tokens x [T][d] of |a_n| (Eq. 1); a new
+    zeroed scores tensor when none is given."""
+    dev = _dev(gate_up)
+    T, d = x.shape
+    N = gate_up.shape[0]
+    if gate_up.shape != (N, 2, d):
+        raise ValueError("gate_up must be [N][2][d]")
+    if scores is None:
+        scores = torch.zeros(N, dtype=torch.float32, device=dev)
+    lib = load()
+    need = int(lib.si_profile_scores_workspace(T, N, d, _dt(x), _dt(gate_up)))
+    if workspace is None:
+        workspace = _workspace(dev, need)
+    st = lib.si_profile_scores(_ptr(x), _dt(x), T, d, _ptr(gate_up), N, _dt(gate_up),
+                               _ptr(scores), _ptr(workspace), workspace.numel(), _stream(dev))
+    _check(st, "si_profile_scores")
+    return scores
+
+
+def merge_scores(scores: torch.Tensor, tokens) -> torch.Tensor:
+    """si_merge_scores: scores [F][N] with token counts [F] (host ints) -> sum of s_f / T_f."""
+    import ctypes
+
+    dev = _dev(scores)
+    F, N = scores.shape
+    toks = (ctypes.c_int64 * F)(*[int(t) for t in tokens])
+    out = torch.empty(N, dtype=torch.float32, device=dev)
+    st = load().si_merge_scores(_ptr(scores), ctypes.cast(toks, ctypes.c_void_p), F, N,
+                                _ptr(out), _stream(dev))
+    _check(st, "si_merge_scores")
+    return out
+
+
+def rank_neurons(scores: torch.Tensor) -> torch.Tensor:
+    """si_rank_neurons: neuron indices by decreasing score (ties to the lower index)."""
+    dev = _dev(scores)
+    order = torch.empty(scores.numel(), dtype=torch.int32, device=dev)
+    st = load().si_rank_neurons(_ptr(scores), scores.numel(), _ptr(order), _stream(dev))
+    _check(st, "si_rank_neurons")
+    return order

@@ -210,4 +210,67 @@ int si_residual_rmsnorm(const void* x, si_dtype xdt, const float* y, int64_t B, 
                                                 static_cast<hipStream_t>(hip_stream)));
 }
 
+size_t si_dynamic_set_workspace(int64_t T, int64_t L, int64_t alpha, int64_t n_total) {
+    if (T < 0 || L < 1 || alpha < 0 || n_total < 0) return 0;
+    return si::dyn_plan(T, L, alpha, n_total).total;
+}
+
+int si_dynamic_set(const void* x, si_dtype xdt, int64_t T, int64_t d, const void* gate_up_c,
+                   int64_t L, si_dtype wdt, const int32_t* static_slots, int64_t n_static,
+                   int64_t alpha, int64_t n_total, int32_t* out_slots, int32_t* counts, void* ws,
+                   size_t ws_bytes, void* hip_stream) {
+    if (T < 0 || d < 1 || L < 1 || L > (1 << 24)) return SI_ERR_INVALID;
+    if (alpha < 0 || alpha > L || n_static < 0 || n_static > n_total || n_total > L)
+        return SI_ERR_INVALID;
+    if (!valid_dtype(xdt) || !valid_dtype(wdt)) return SI_ERR_UNSUPPORTED;
+    if ((T > 0 && !x) || !gate_up_c || (n_static > 0 && !static_slots)) return SI_ERR_INVALID;
+    if (n_total > 0 && !out_slots) return SI_ERR_INVALID;
+    if (!aligned16(x) || !aligned16(gate_up_c)) return SI_ERR_INVALID;
+    const size_t need = si_dynamic_set_workspace(T, L, alpha, n_total);
+    if (!ws || ws_bytes < need || !aligned16(ws)) return SI_ERR_WORKSPACE;
+    if (current_device() < 0) return SI_ERR_HIP;
+    return from_hip(si::launch_dynamic_set(x, xdt, T, d, gate_up_c, L, wdt, static_slots,
+                                           n_static, alpha, n_total, out_slots, counts, ws,
+                                           static_cast<hipStream_t>(hip_stream)));
+}
+
+size_t si_profile_scores_workspace(int64_t T, int64_t N, int64_t d, si_dtype xdt, si_dtype wdt) {
+    if (T < 0 || N < 1 || d < 1) return 0;
+    return si::score_workspace(T, N, d, xdt, wdt);
+}
+
+int si_profile_scores(const void* x, si_dtype xdt, int64_t T, int64_t d, const void* gate_up,
+                      int64_t N, si_dtype wdt, float* scores, void* ws, size_t ws_bytes,
+                      void* hip_stream) {
+    if (T < 0 || d < 1 || N < 1 || N > INT32_MAX) return SI_ERR_INVALID;
+    if (!valid_dtype(xdt) || !valid_dtype(wdt)) return SI_ERR_UNSUPPORTED;
+    if (T == 0) return SI_OK;
+    if (!x || !gate_up || !scores) return SI_ERR_INVALID;
+    if (!aligned16(x) || !aligned16(gate_up)) return SI_ERR_INVALID;
+    const size_t need = si_profile_scores_workspace(T, N, d, xdt, wdt);
+    if (!ws || ws_bytes < need || !aligned16(ws)) return SI_ERR_WORKSPACE;
+    if (current_device() < 0) return SI_ERR_HIP;
+    return from_hip(si::launch_scores(x, xdt, T, d, gate_up, N, wdt, scores, ws,
+                                      static_cast<hipStream_t>(hip_stream)));
+}
+
+int si_merge_scores(const float* scores, const int64_t* tokens, int64_t F, int64_t N, float* out,
+                    void* hip_stream) {
+    if (F < 1 || N < 1 || !scores || !tokens || !out) return SI_ERR_INVALID;
+    for (int64_t f = 0; f < F; ++f)
+        if (tokens[f] < 1) return SI_ERR_INVALID;
+    hipStream_t s = static_cast<hipStream_t>(hip_stream);
+    for (int64_t f = 0; f < F; ++f) {
+        const hipError_t e =
+            si::launch_merge_file(scores + f * N, N, (float)tokens[f], f == 0 ? 1 : 0, out, s);
+        if (e != hipSuccess) return from_hip(e);
+    }
+    return SI_OK;
+}
+
+int si_rank_neurons(const float* scores, int64_t N, int32_t* order, void* hip_stream) {
+    if (N < 1 || N > (1 << 24) || !scores || !order) return SI_ERR_INVALID;
+    return from_hip(si::launch_rank(scores, N, order, static_cast<hipStream_t>(hip_stream)));
+}
+
 }  // extern "C"

@@ -1,0 +1,293 @@
+// Neuron selection around the hot path: dynamic-set construction (Selective Computation
+// section) and the profiler's scores (LLM Profiler section, Eq. 1).
+//
+//  - act_rows: the activation a[t][j] = SiLU(gate_j . x_t) * (up_j . x_t) of every loaded slot
+//    for any storage type (one wave per (token, slot)); bf16 data use the MFMA tiles of
+//    k_tiled.hip instead;
+//  - col_abs_sum / add_rows: Eq. 1 sums |a| over tokens, and partial rows over token tiles,
+//    in ascending order;
+//  - count_slots: how many of the tokens' top-alpha lists hold each slot (integer atomics:
+//    the result does not depend on their order);
+//  - freq_keys, mask_static: the frequency of each slot as a float key (exact below 2^24),
+//    static slots below every frequency;
+//  - set_bits: a slot list as a bitmap (then listed in ascending order by the union scan);
+//  - merge_file: out += s / tokens for one score file, file by file;
+//  - rank_scores: the position of each neuron in decreasing score (ties to the lower index,
+//    NaN last), by counting the neurons ranked before it; exact and order-free.
+#include "common.h"
+#include "launch.h"
+
+namespace si {
+
+namespace {
+
+template <typename T>
+__device__ __forceinline__ float ldf(const T* p);
+template <>
+__device__ __forceinline__ float ldf<float>(const float* p) { return *p; }
+template <>
+__device__ __forceinline__ float ldf<bf16_t>(const bf16_t* p) { return bf16_to_f32(*p); }
+
+// Grid (ceil(L / 4), T), 256 threads: wave w takes slot 4 blockIdx.x + w of token blockIdx.y.
+template <typename WT, typename XT>
+__global__ __launch_bounds__(256) void act_rows(const XT* __restrict__ x, int64_t d,
+                                                const WT* __restrict__ gu, int64_t L,
+                                                float* __restrict__ out, int64_t ldo) {
+    const int lane = threadIdx.x & 63;
+    const int64_t j = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int64_t t = blockIdx.y;
+    if (j >= L) return;
+    const XT* xr = x + t * d;
+    const WT* gr = gu + j * 2 * d;
+    float g = 0.0f, u = 0.0f;
+    for (int64_t c = lane; c < d; c += kWave) {
+        const float xv = ldf(xr + c);
+        g = fmaf(ldf(gr + c), xv, g);
+        u = fmaf(ldf(gr + d + c), xv, u);
+    }
+    g = wave_sum(g);
+    u = wave_sum(u);
+    if (lane == 0) out[t * ldo + j] = silu_f32(g) * u;
+}
+
+// s[n] += sum over t = 0 .. T-1 of |A[t][n]| (A with row stride lda)
+__global__ __launch_bounds__(256) void col_abs_sum(const float* __restrict__ A, int64_t T,
+                                                   int64_t N, int64_t lda, float* __restrict__ s) {
+    const int64_t n = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (n >= N) return;
+    float v = 0.0f;
+    for (int64_t t = 0; t < T; ++t) v += fabsf(A[t * lda + n]);
+    s[n] += v;
+}
+
+// s[n] += sum over r = 0 .. R-1 of P[r][n] (P with row stride ldp)
+__global__ __launch_bounds__(256) void add_rows(const float* __restrict__ P, int64_t R, int64_t N,
+                                                int64_t ldp, float* __restrict__ s) {
+    const int64_t n = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (n >= N) return;
+    float v = 0.0f;
+    for (int64_t r = 0; r < R; ++r) v += P[r * ldp + n];
+    s[n] += v;
+}
+
+__global__ __launch_bounds__(256) void fill_u32(uint32_t* __restrict__ p, int64_t n, uint32_t v) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i < n) p[i] = v;
+}
+
+__global__ __launch_bounds__(256) void count_slots(const int32_t* __restrict__ ids, int64_t n,
+                                                   int64_t L, int* __restrict__ counts) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= n) return;
+    const int32_t v = ids[i];
+    if (v >= 0 && v < L) atomicAdd(&counts[v], 1);
+}
+
+__global__ __launch_bounds__(256) void freq_keys(const int* __restrict__ counts, int64_t L,
+                                                 float* __restrict__ keys) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i < L) keys[i] = (float)counts[i];
+}
+
+__global__ __launch_bounds__(256) void mask_static(const int32_t* __restrict__ st, int64_t n,
+                                                   int64_t L, float* __restrict__ keys) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= n) return;
+    const int32_t v = st[i];
+    if (v >= 0 && v < L) keys[v] = -1.0f;
+}
+
+__global__ __launch_bounds__(256) void set_bits(const int32_t* __restrict__ ids, int64_t n,
+                                                int64_t L, uint32_t* __restrict__ bits) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= n) return;
+    const int32_t v = ids[i];
+    if (v >= 0 && v < L) atomicOr(&bits[v >> 5], 1u << (v & 31));
+}
+
+__global__ __launch_bounds__(256) void merge_file(const float* __restrict__ s, int64_t N,
+                                                  float tokens, int first,
+                                                  float* __restrict__ out) {
+    const int64_t n = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (n >= N) return;
+    const float v = s[n] / tokens;
+    out[n] = first ? v : out[n] + v;
+}
+
+// Order key, larger first: -0 and +0 equal, NaN below every number.
+__device__ __forceinline__ uint32_t desc_key(float f) {
+    if (f != f) return 0u;
+    uint32_t u = __float_as_uint(f);
+    if ((u << 1) == 0u) u = 0u;
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Grid ceil(N / 256): thread n counts the neurons ranked before n over LDS tiles of keys.
+__global__ __launch_bounds__(256) void rank_scores(const float* __restrict__ s, int64_t N,
+                                                   int32_t* __restrict__ order) {
+    __shared__ uint32_t tk[256];
+    const int64_t n = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const uint32_t kn = n < N ? desc_key(s[n]) : 0u;
+    int64_t before = 0;
+    for (int64_t m0 = 0; m0 < N; m0 += 256) {
+        __syncthreads();
+        const int64_t m = m0 + threadIdx.x;
+        tk[threadIdx.x] = m < N ? desc_key(s[m]) : 0u;
+        __syncthreads();
+        const int64_t lim = (N - m0) < 256 ? (N - m0) : 256;
+        for (int q = 0; q < lim; ++q) {
+            const uint32_t km = tk[q];
+            before += (km > kn) || (km == kn && m0 + q < n);
+        }
+    }
+    if (n < N) order[before] = (int32_t)n;
+}
+
+inline unsigned blocks(int64_t n) { return (unsigned)((n + 255) / 256); }
+
+// bf16 data with whole 16-byte K chunks and 32-bit buffer offsets take the MFMA tiles
+inline bool mfma_ok(int xdt, int wdt, int64_t T, int64_t L, int64_t d) {
+    return xdt == 1 && wdt == 1 && d % 8 == 0 && tiled_supported(T, L, d);
+}
+
+}  // namespace
+
+hipError_t launch_activations(const void* x, int xdt, int64_t T, int64_t d, const void* gate_up_c,
+                              int64_t L, int wdt, float* out, int64_t ldo, hipStream_t s) {
+    if (T == 0 || L == 0) return hipSuccess;
+    if (mfma_ok(xdt, wdt, T, L, d))
+        return launch_activations_mfma(x, T, d, gate_up_c, L, out, ldo, 0, s);
+    // grid y holds the tokens: at most 65535 per launch
+    for (int64_t t0 = 0; t0 < T; t0 += 65535) {
+        const int64_t nt = (T - t0) < 65535 ? (T - t0) : 65535;
+        const dim3 grid((unsigned)((L + 3) / 4), (unsigned)nt);
+        const int64_t xo = t0 * d;
+        float* o = out + t0 * ldo;
+#define SI_ACT(WT, XT)                                                                          \
+    hipLaunchKernelGGL((act_rows<WT, XT>), grid, dim3(256), 0, s,                              \
+                       static_cast<const XT*>(x) + xo, d, static_cast<const WT*>(gate_up_c), L, \
+                       o, ldo)
+        if (wdt == 1 && xdt == 1)
+            SI_ACT(bf16_t, bf16_t);
+        else if (wdt == 1)
+            SI_ACT(bf16_t, float);
+        else if (xdt == 1)
+            SI_ACT(float, bf16_t);
+        else
+            SI_ACT(float, float);
+    }
+#undef SI_ACT
+    return hipGetLastError();
+}
+
+size_t score_workspace(int64_t T, int64_t N, int64_t d, int xdt, int wdt) {
+    const int64_t ldo = (N + 63) / 64 * 64;
+    if (mfma_ok(xdt, wdt, T, N, d)) return (size_t)activation_tiles(T) * ldo * 4;  // per tile
+    return (size_t)T * ldo * 4;                         // the activations themselves
+}
+
+hipError_t launch_scores(const void* x, int xdt, int64_t T, int64_t d, const void* gate_up,
+                         int64_t N, int wdt, float* scores, void* ws, hipStream_t s) {
+    if (T == 0 || N == 0) return hipSuccess;
+    const int64_t ldo = (N + 63) / 64 * 64;
+    float* buf = static_cast<float*>(ws);
+    hipError_t e;
+    if (mfma_ok(xdt, wdt, T, N, d)) {
+        e = launch_activations_mfma(x, T, d, gate_up, N, buf, ldo, 1, s);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(add_rows, dim3(blocks(N)), dim3(256), 0, s, buf,
+                           (int64_t)activation_tiles(T), N, ldo, scores);
+    } else {
+        e = launch_activations(x, xdt, T, d, gate_up, N, wdt, buf, ldo, s);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(col_abs_sum, dim3(blocks(N)), dim3(256), 0, s, buf, T, N, ldo, scores);
+    }
+    return hipGetLastError();
+}
+
+DynPlan dyn_plan(int64_t T, int64_t L, int64_t alpha, int64_t n_total) {
+    DynPlan p;
+    auto al = [](size_t v) { return (v + 255) & ~(size_t)255; };
+    p.lda = (L + 63) / 64 * 64;
+    p.W = (L + 31) / 32;
+    size_t o = 0;
+    p.off_act = o;
+    o = al(o + (size_t)T * p.lda * 4);
+    p.off_lists = o;
+    o = al(o + (size_t)T * alpha * 4);
+    p.off_counts = o;
+    o = al(o + (size_t)L * 4);
+    p.off_keys = o;
+    o = al(o + (size_t)L * 4);
+    p.off_dyn = o;
+    o = al(o + (size_t)(n_total > 0 ? n_total : 1) * 4);
+    p.off_bits = o;
+    o = al(o + (size_t)p.W * 4);
+    p.off_count = o;
+    o = al(o + 4);
+    p.total = o;
+    return p;
+}
+
+hipError_t launch_dynamic_set(const void* x, int xdt, int64_t T, int64_t d, const void* gate_up_c,
+                              int64_t L, int wdt, const int32_t* static_slots, int64_t n_static,
+                              int64_t alpha, int64_t n_total, int32_t* out, int32_t* counts_out,
+                              void* ws, hipStream_t s) {
+    const DynPlan p = dyn_plan(T, L, alpha, n_total);
+    uint8_t* base = static_cast<uint8_t*>(ws);
+    float* act = reinterpret_cast<float*>(base + p.off_act);
+    int32_t* lists = reinterpret_cast<int32_t*>(base + p.off_lists);
+    int* counts = counts_out ? counts_out : reinterpret_cast<int*>(base + p.off_counts);
+    float* keys = reinterpret_cast<float*>(base + p.off_keys);
+    int32_t* dyn = reinterpret_cast<int32_t*>(base + p.off_dyn);
+    uint32_t* bits = reinterpret_cast<uint32_t*>(base + p.off_bits);
+    int* cnt = reinterpret_cast<int*>(base + p.off_count);
+    hipError_t e;
+    // 1. activations of every loaded slot, per token
+    e = launch_activations(x, xdt, T, d, gate_up_c, L, wdt, act, p.lda, s);
+    if (e != hipSuccess) return e;
+    // 2. each token's top alpha by |a|
+    hipLaunchKernelGGL(fill_u32, dim3(blocks(L)), dim3(256), 0, s,
+                       reinterpret_cast<uint32_t*>(counts), L, 0u);
+    if (T > 0 && alpha > 0) {
+        e = launch_topk_strided(act, T, L, p.lda, alpha, 0, lists, s);
+        if (e != hipSuccess) return e;
+        // 3. frequency of each slot over the T lists
+        hipLaunchKernelGGL(count_slots, dim3(blocks(T * alpha)), dim3(256), 0, s, lists,
+                           T * alpha, L, counts);
+    }
+    // 4. the most frequent non-static slots, n_total - n_static of them
+    hipLaunchKernelGGL(freq_keys, dim3(blocks(L)), dim3(256), 0, s, counts, L, keys);
+    if (n_static > 0)
+        hipLaunchKernelGGL(mask_static, dim3(blocks(n_static)), dim3(256), 0, s, static_slots,
+                           n_static, L, keys);
+    const int64_t kd = n_total - n_static;
+    if (kd > 0) {
+        e = launch_topk(keys, 1, L, kd, 1, dyn, s);
+        if (e != hipSuccess) return e;
+    }
+    // 5. static u dynamic, ascending
+    hipLaunchKernelGGL(fill_u32, dim3(blocks(p.W)), dim3(256), 0, s, bits, p.W, 0u);
+    if (n_static > 0)
+        hipLaunchKernelGGL(set_bits, dim3(blocks(n_static)), dim3(256), 0, s, static_slots,
+                           n_static, L, bits);
+    if (kd > 0)
+        hipLaunchKernelGGL(set_bits, dim3(blocks(kd)), dim3(256), 0, s, dyn, kd, L, bits);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_bits_to_list(bits, p.W, out, cnt, s);
+}
+
+hipError_t launch_merge_file(const float* sc, int64_t N, float tokens, int first, float* out,
+                             hipStream_t s) {
+    hipLaunchKernelGGL(merge_file, dim3(blocks(N)), dim3(256), 0, s, sc, N, tokens, first, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_rank(const float* sc, int64_t N, int32_t* order, hipStream_t s) {
+    if (N == 0) return hipSuccess;
+    hipLaunchKernelGGL(rank_scores, dim3(blocks(N)), dim3(256), 0, s, sc, N, order);
+    return hipGetLastError();
+}
+
+}  // namespace si

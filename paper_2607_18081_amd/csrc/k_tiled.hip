@@ -118,15 +118,25 @@ __global__ __launch_bounds__(1024) void union_scan(const uint32_t* __restrict__ 
 // ---- GEMM1 ---------------------------------------------------------------------------------
 // Grid: 8 * ntm * ceil(nst / 8) work-groups of 256 threads. Work-groups 8 apart (same XCD)
 // share a slot tile, so its weight rows are fetched from HBM once per XCD.
+// MODE selects what the epilogue produces (the product itself is the same):
+//   kUnion:  h masked by the token bitmaps, over the union list, as bf16 hi/lo planes;
+//   kAct:    the activation of every slot (the union list is the identity, no mask), float32
+//            out[tok * Up + slot];
+//   kScore:  Eq. 1 for this work-group's tokens: sum over its 256 tokens of |a| per slot,
+//            added in a fixed order, float32 out[tm * Up + slot] (one partial row per token
+//            tile; the host-side reducer adds the rows in order).
+enum { kUnion = 0, kAct = 1, kScore = 2 };
+
+template <int MODE>
 __global__ __launch_bounds__(256) void gemm1_tiled(
     const bf16_t* __restrict__ x, int64_t B, int64_t d, const bf16_t* __restrict__ gu, int64_t L,
     const int32_t* __restrict__ ulist, const int* __restrict__ ucount,
     const uint32_t* __restrict__ bits, int64_t W, bf16_t* __restrict__ Hhi,
-    bf16_t* __restrict__ Hlo, int64_t Up, int ntm) {
+    bf16_t* __restrict__ Hlo, int64_t Up, int ntm, float* __restrict__ out) {
     const int id = blockIdx.x;
     const int st = (id / (8 * ntm)) * 8 + (id % 8);
     const int tm = (id / 8) % ntm;
-    const int nU = *ucount;
+    const int nU = MODE == kUnion ? *ucount : (int)L;
     const int64_t u0 = (int64_t)st * kT1S;
     if (u0 >= nU) return;  // uniform
     const int64_t m0 = (int64_t)tm * kT1M;
@@ -155,7 +165,7 @@ __global__ __launch_bounds__(256) void gemm1_tiled(
         const int r = r0 + 32 * j;              // weight row of the tile
         const int64_t u = u0 + 16 * (r / 32) + (r % 16);
         const int plane = (r % 32) / 16;        // 0 gate, 1 up
-        const int32_t slot = u < nU ? ulist[u] : -1;
+        const int32_t slot = u < nU ? (MODE == kUnion ? ulist[u] : (int32_t)u) : -1;
         boff[j] = (slot >= 0 && slot < L) ? (int)(((int64_t)slot * 2 + plane) * d * 2) : kOOB;
     }
     V16 pa[8], pb[5];
@@ -211,22 +221,49 @@ __global__ __launch_bounds__(256) void gemm1_tiled(
 
     // epilogue: register i of lane l of tile (mi, nj) is token 64 w + 16 mi + 4 g + i and
     // weight row 16 nj + nn; tiles 2q and 2q + 1 are gate and up of slots u0 + 16 q + nn
+    if (MODE == kScore) {
+        // |a| summed over this lane's 16 tokens, then over the 4 lane groups (64 tokens of the
+        // wave), then over the 4 waves in LDS, each in a fixed order
+        __shared__ float ssum[4][kT1S];
+#pragma unroll
+        for (int q = 0; q < 5; ++q) {
+            float v = 0.0f;
+#pragma unroll
+            for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int64_t tok = m0 + 64 * w + 16 * mi + 4 * g + i;
+                    if (tok < B) v += fabsf(silu_f32(acc[mi][2 * q][i]) * acc[mi][2 * q + 1][i]);
+                }
+            v += __shfl_xor(v, 16, kWave);
+            v += __shfl_xor(v, 32, kWave);
+            if (g == 0) ssum[w][16 * q + nn] = v;
+        }
+        __syncthreads();
+        if (t < kT1S && u0 + t < nU)
+            out[(int64_t)tm * Up + u0 + t] = ((ssum[0][t] + ssum[1][t]) + ssum[2][t]) + ssum[3][t];
+        return;
+    }
 #pragma unroll
     for (int q = 0; q < 5; ++q) {
         const int64_t u = u0 + 16 * q + nn;
-        const int32_t slot = u < nU ? ulist[u] : -1;
+        const int32_t slot = u < nU ? (MODE == kUnion ? ulist[u] : (int32_t)u) : -1;
 #pragma unroll
         for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int64_t tok = m0 + 64 * w + 16 * mi + 4 * g + i;
                 if (tok < B && slot >= 0) {
-                    const bool act = (bits[tok * W + slot / 32] >> (slot % 32)) & 1u;
-                    const float h = act ? silu_f32(acc[mi][2 * q][i]) * acc[mi][2 * q + 1][i]
-                                        : 0.0f;
-                    const uint32_t hb = f32_to_bf16_rne(h);
-                    Hhi[tok * Up + u] = (bf16_t)hb;
-                    Hlo[tok * Up + u] = (bf16_t)f32_to_bf16_rne(h - bf16_to_f32(hb));
+                    if (MODE == kAct) {
+                        out[tok * Up + u] = silu_f32(acc[mi][2 * q][i]) * acc[mi][2 * q + 1][i];
+                    } else {
+                        const bool act = (bits[tok * W + slot / 32] >> (slot % 32)) & 1u;
+                        const float h =
+                            act ? silu_f32(acc[mi][2 * q][i]) * acc[mi][2 * q + 1][i] : 0.0f;
+                        const uint32_t hb = f32_to_bf16_rne(h);
+                        Hhi[tok * Up + u] = (bf16_t)hb;
+                        Hlo[tok * Up + u] = (bf16_t)f32_to_bf16_rne(h - bf16_to_f32(hb));
+                    }
                 }
             }
     }
@@ -441,6 +478,14 @@ TPlan make_tplan(int64_t B, int64_t L, int64_t d, int num_cu) {
 
 }  // namespace
 
+hipError_t launch_bits_to_list(const uint32_t* bits, int64_t W, int32_t* list, int* count,
+                               hipStream_t s) {
+    hipLaunchKernelGGL(union_scan, dim3(1), dim3(1024), 0, s, bits, (int64_t)1, W, list, count);
+    return hipGetLastError();
+}
+
+int activation_tiles(int64_t T) { return (int)((T + kT1M - 1) / kT1M); }
+
 bool tiled_supported(int64_t B, int64_t L, int64_t d) {
     const int64_t Up = (L + kBK - 1) / kBK * kBK;
     const int64_t lim = (int64_t)1 << 31;
@@ -477,9 +522,9 @@ hipError_t launch_union_tiled(const void* x, int64_t B, int64_t d, const int32_t
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int nst8 = (p.nst + 7) / 8 * 8;
-    hipExtLaunchKernelGGL(gemm1_tiled, dim3((unsigned)(nst8 * p.ntm1)), dim3(256), 0, s, ev0,
-                          nullptr, 0, xx, B, d, gu, L, ulist, ucount, bits, p.W, hhi, hlo, p.Up,
-                          p.ntm1);
+    hipExtLaunchKernelGGL(gemm1_tiled<kUnion>, dim3((unsigned)(nst8 * p.ntm1)), dim3(256), 0, s,
+                          ev0, nullptr, 0, xx, B, d, gu, L, ulist, ucount, bits, p.W, hhi, hlo,
+                          p.Up, p.ntm1, nullptr);
     const int fast = (flags & 4) ? 1 : 0;
     hipExtLaunchKernelGGL(gemm2_tiled, dim3((unsigned)p.ntn2, (unsigned)p.ntm2, (unsigned)p.KS),
                           dim3(256), 0, s, nullptr, ev1, 0, hhi, hlo, p.Up, B, dc, d, L, ulist,
@@ -487,6 +532,25 @@ hipError_t launch_union_tiled(const void* x, int64_t B, int64_t d, const int32_t
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     return launch_reduce_partials(part, p.KS, B, d, y, s);
+}
+
+hipError_t launch_activations_mfma(const void* x, int64_t T, int64_t d, const void* gate_up_c,
+                                   int64_t L, float* out, int64_t ldo, int score, hipStream_t s) {
+    if (T == 0 || L == 0) return hipSuccess;
+    const int ntm = (int)((T + kT1M - 1) / kT1M);
+    const int nst = (int)((L + kT1S - 1) / kT1S);
+    const int nst8 = (nst + 7) / 8 * 8;
+    const bf16_t* xx = static_cast<const bf16_t*>(x);
+    const bf16_t* gu = static_cast<const bf16_t*>(gate_up_c);
+    if (score)
+        hipLaunchKernelGGL(gemm1_tiled<kScore>, dim3((unsigned)(nst8 * ntm)), dim3(256), 0, s, xx,
+                           T, d, gu, L, nullptr, nullptr, nullptr, (int64_t)0, nullptr, nullptr,
+                           ldo, ntm, out);
+    else
+        hipLaunchKernelGGL(gemm1_tiled<kAct>, dim3((unsigned)(nst8 * ntm)), dim3(256), 0, s, xx, T,
+                           d, gu, L, nullptr, nullptr, nullptr, (int64_t)0, nullptr, nullptr, ldo,
+                           ntm, out);
+    return hipGetLastError();
 }
 
 }  // namespace si

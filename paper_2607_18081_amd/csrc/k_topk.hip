@@ -54,10 +54,10 @@ __device__ __forceinline__ int block_prefix(bool flag, int* wave_cnt, int* total
 }
 
 __global__ __launch_bounds__(kTopkThreads) void topk_rows(const float* __restrict__ scores,
-                                                         int64_t L, int64_t k, int mode,
-                                                         int32_t* __restrict__ out) {
+                                                         int64_t L, int64_t ld, int64_t k,
+                                                         int mode, int32_t* __restrict__ out) {
     const int64_t b = blockIdx.x;
-    const float* row = scores + b * L;
+    const float* row = scores + b * ld;
     int32_t* orow = out + b * k;
     __shared__ int hist[256];
     __shared__ int wave_cnt[kTopkWaves];
@@ -116,12 +116,17 @@ __global__ __launch_bounds__(kTopkThreads) void topk_rows(const float* __restric
 
 }  // namespace
 
-hipError_t launch_topk(const float* scores, int64_t B, int64_t L, int64_t k, int mode,
-                       int32_t* out, hipStream_t s) {
+hipError_t launch_topk_strided(const float* scores, int64_t B, int64_t L, int64_t ld, int64_t k,
+                               int mode, int32_t* out, hipStream_t s) {
     if (B == 0 || k == 0) return hipSuccess;
-    hipLaunchKernelGGL(topk_rows, dim3((unsigned)B), dim3(kTopkThreads), 0, s, scores, L, k,
+    hipLaunchKernelGGL(topk_rows, dim3((unsigned)B), dim3(kTopkThreads), 0, s, scores, L, ld, k,
                        mode, out);
     return hipGetLastError();
+}
+
+hipError_t launch_topk(const float* scores, int64_t B, int64_t L, int64_t k, int mode,
+                       int32_t* out, hipStream_t s) {
+    return launch_topk_strided(scores, B, L, L, k, mode, out, s);
 }
 
 }  // namespace si

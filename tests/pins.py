@@ -363,7 +363,8 @@ def pin_dynamic_set(impl):
     wg, wu, _, _ = _problem(13, 18, 8, "bf16")
     X = (rng.standard_normal((6, 8))).astype(np.float32)
     got, _ = impl.dynamic_set(X, _gu(wg, wu), [2, 9], 4, 7)
-    want, _ = impl.select_dynamic(_lib_activations(X, wg, wu), [2, 9], 4, 7)
+    A32 = _lib_activations(X, wg, wu).astype(np.float32).astype(np.float64)
+    want, _ = impl.select_dynamic(A32, [2, 9], 4, 7)
     assert np.array_equal(got, want)
     for bad in (dict(static_slots=[1, 1], alpha=2, n_total=3),
                 dict(static_slots=[0, 1, 2], alpha=2, n_total=2),
