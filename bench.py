@@ -13,7 +13,10 @@ The oracle (fp64 NumPy, host) is timed on a bounded sample of the same workload.
 
 Other workloads (``--workload``) are available for measurement: tiny_f32, llama2_7b_b16
 (batch 16, union MFMA path), llama3_8b_stack (32 layers, residual RMSNorm between layers),
-llama2_13b_prefill (512 tokens, MFMA-bound union path).
+llama2_13b_prefill (512 tokens, MFMA-bound union path); and the selection steps around the
+path: dynset_llama2_13b (dynamic-set construction for a 512-token prompt on the 13B-shape
+layer, si_dynamic_set) and profile_llama3_8b (Eq. 1 scores of 512 tokens over a full
+8B-shape FFN layer, si_profile_scores).
 """
 from __future__ import annotations
 
@@ -320,6 +323,191 @@ def traffic_record(workload):
 
 
 
+# --------------------------------------------------------------------------------------------
+# Selection steps around the path: dynamic-set construction and profiler scores
+# --------------------------------------------------------------------------------------------
+SELECT_WORKLOADS = {
+    # a 512-token prompt of the 13B-shape layer; Table 1: 30% static (base) neurons, 40% of N
+    # computed in all; alpha = the computed total
+    "dynset_llama2_13b": dict(base="llama2_13b_prefill", kind="dynset", T=512,
+                              static_frac=0.3, total_frac=0.4),
+    # Eq. 1 over a full 8B-shape layer (every neuron loaded), 512 tokens per call
+    "profile_llama3_8b": dict(base="llama3_8b_stack", kind="profile", T=512),
+}
+
+
+class _SelCfg:
+    def __init__(self, name, base, T):
+        self.name = name
+        self.layers = 1
+        self.steps = 1
+        self.B = T
+        self.base = base
+
+
+class SelectWork:
+    """Device state and step launcher of a selection workload (one step = one call)."""
+
+    def __init__(self, name, copies, dev):
+        import numpy as np
+        import torch
+
+        import paper_2607_18081_amd as si
+        from workloads import CONFIGS, layer_weights, loaded_ids, tokens_x
+
+        spec = SELECT_WORKLOADS[name]
+        base = CONFIGS[spec["base"]]
+        self.kind = spec["kind"]
+        self.T = spec["T"]
+        self.cfg = _SelCfg(name, base, self.T)
+        self.si, self.np, self.torch = si, np, torch
+        wg, wu, wd = layer_weights(base, 0)
+        N, d = base.N, base.d
+        loaded = loaded_ids(base, 0) if self.kind == "dynset" else np.arange(N, dtype=np.int32)
+        self.host = (wg, wu, wd, loaded)
+        self.x_host = tokens_x(base, range(self.T))
+        to_dev = lambda a: (torch.from_numpy(a.view(np.int16)).to(dev).view(torch.bfloat16)
+                            if a.dtype == np.uint16 else torch.from_numpy(a).to(dev))
+        c0 = si.compact_ffn(to_dev(wg), to_dev(wu), to_dev(wd), torch.from_numpy(loaded))
+        self.orig_to_slot = c0.orig_to_slot
+        self.gu = [c0.gate_up_c] + [c0.gate_up_c.clone() for _ in range(copies - 1)]
+        del c0
+        self.x = to_dev(self.x_host)
+        self.L = len(loaded)
+        self.d, self.N = d, N
+        if self.kind == "dynset":
+            n_static = int(round(spec["static_frac"] * N))
+            self.n_total = int(round(spec["total_frac"] * N))
+            self.alpha = self.n_total
+            # static (base) neurons: the most popular loaded ones, as slots
+            st_orig = torch.from_numpy(loaded[:n_static].copy()).to(dev)
+            self.static = si.remap_ids(self.orig_to_slot, st_orig, check=True)
+            self.static_host = self.static.cpu().numpy()
+            self.out = torch.empty(self.n_total, dtype=torch.int32, device=dev)
+            self.counts = torch.empty(self.L, dtype=torch.int32, device=dev)
+            need = int(si._lib.load().si_dynamic_set_workspace(self.T, self.L, self.alpha,
+                                                                self.n_total))
+        else:
+            self.scores = torch.zeros(N, dtype=torch.float32, device=dev)
+            need = int(si._lib.load().si_profile_scores_workspace(self.T, N, d, si.BF16,
+                                                                   si.BF16))
+        self.ws = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+
+    def launch(self, step, timing=None):
+        si = self.si
+        gu = self.gu[step % len(self.gu)]
+        if timing:
+            si.set_timing_events(*timing[0])
+        if self.kind == "dynset":
+            si.dynamic_set(self.x, gu, self.static, self.alpha, self.n_total, workspace=self.ws,
+                           out=self.out, counts=self.counts)
+        else:
+            si.profile_scores(self.x, gu, scores=self.scores, workspace=self.ws)
+        if timing:
+            si.set_timing_events(None, None)
+
+    def launch_flops(self, step):
+        """MFMA flops of the activation GEMM: gate and up rows of every slot, every token."""
+        return 2.0 * self.T * 2 * self.L * self.d
+
+    def check(self):
+        np = self.np
+        if self.kind == "dynset":
+            out = self.out.cpu().numpy()
+            cnt = self.counts.cpu().numpy()
+            st = set(self.static_host.tolist())
+            ok = (len(out) == self.n_total and bool(np.all(np.diff(out) > 0))
+                  and st <= set(out.tolist()) and int(cnt.sum()) == self.T * self.alpha)
+            if ok:
+                inset = set(out.tolist())
+                dyn = [j for j in out.tolist() if j not in st]
+                rest = [j for j in range(self.L) if j not in inset]
+                if dyn and rest:
+                    ok = min((cnt[j], -j) for j in dyn) > max((cnt[j], -j) for j in rest)
+            return {"valid": bool(ok), "checks": "size, ascending, static included, counts sum "
+                    "to T*alpha, dynamic slots the most frequent (ties to the lower slot)"}
+        # scores of a 16-token sample against the oracle
+        import oracle
+        wg, wu, wd, loaded = self.host
+        ref = oracle.compact(wg, wu, wd, loaded)
+        want, _ = oracle.profile_scores(self.x_host[:16], ref["gate_up_c"])
+        got = self.si.profile_scores(self.x[:16], self.gu[0]).cpu().numpy().astype(np.float64)
+        err = float(np.linalg.norm(got - want) / np.linalg.norm(want))
+        return {"tokens_checked": 16, "max_rel_l2": err, "tol": 1e-5, "valid": err <= 1e-5}
+
+    def cpu_baseline(self, seconds):
+        from threadpoolctl import threadpool_limits
+
+        import oracle
+        wg, wu, wd, loaded = self.host
+        ref = oracle.compact(wg, wu, wd, loaded)
+        n = 2
+        with threadpool_limits(limits=1):
+            while True:
+                t0 = time.perf_counter()
+                if self.kind == "dynset":
+                    oracle.dynamic_set(self.x_host[:n], ref["gate_up_c"], self.static_host,
+                                       self.alpha, self.n_total)
+                else:
+                    oracle.profile_scores(self.x_host[:n], ref["gate_up_c"])
+                el = time.perf_counter() - t0
+                if el >= seconds / 3 or n >= self.T:
+                    break
+                n = min(self.T, n * 2)
+        what = "si_dynamic_set-equivalent" if self.kind == "dynset" else "Eq. 1 scores"
+        return {"value": n / el, "unit": "prompt tokens/s/layer", "cores": 1, "kind": "oracle",
+                "sample": f"first {n} of the {self.T} prompt tokens, one {what} oracle call "
+                          f"(fp64 NumPy), single thread, {el:.1f} s on {os.cpu_count()} "
+                          f"visible host CPUs"}
+
+
+def main_select(args):
+    import numpy as np
+    import torch
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    steps = args.steps if args.steps is not None else 16
+    copies = max(1, min(args.copies, 4))
+    work = SelectWork(args.workload, copies, dev)
+    log(f"workload {args.workload}: T={work.T} L={work.L} d={work.d}; steps={steps}")
+    wall, kern_ms, graphed, launches = run_gpu(work, steps, min(args.warmup, 8),
+                                               not args.no_graph, args.timed_launches)
+    kern_ms = np.array(kern_ms)
+    flops = work.launch_flops(0)
+    achieved = flops / (kern_ms.mean() * 1e-3) / 1e12
+    roof = {"bound": "mfma", "achieved": achieved, "peak": MFMA_BF16_PEAK_TFLOPS,
+            "unit": "TFLOP/s", "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": None,
+            "kernel_ms_mean": float(kern_ms.mean()), "kernel_ms_p50": float(np.median(kern_ms)),
+            "kernel_launches_timed": int(len(kern_ms)), "flops_per_launch": flops}
+    torch.cuda.synchronize()
+    parity = work.check()
+    if not parity["valid"]:
+        log(f"PARITY FAILURE: {parity}")
+        sys.exit(1)
+    cpu = None if args.no_cpu_baseline else work.cpu_baseline(args.cpu_seconds)
+    out = {
+        "metric": ("dynamic-set construction prompt tokens/s per layer" if work.kind == "dynset"
+                   else "profiler scoring (Eq. 1) tokens/s per layer"),
+        "value": steps * work.T / wall,
+        "unit": "prompt tokens/s/layer" if work.kind == "dynset" else "tokens/s/layer",
+        "n_gpus": 1, "steps": steps, "warmup": min(args.warmup, 8),
+        "ms_per_step": wall * 1e3 / steps, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded; weights N(0,0.02), x N(0,1), Zipf(1.1) popularity)",
+        "config": {"workload": args.workload, "d": work.d, "N": work.N, "loaded": work.L,
+                   "tokens_per_step": work.T,
+                   **({"static": int(len(work.static_host)), "alpha": work.alpha,
+                       "n_total": work.n_total} if work.kind == "dynset" else {}),
+                   "weight_copies": len(work.gu), "hip_graph": graphed,
+                   "parallelism": "single GPU"},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "parity": parity,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -333,6 +521,8 @@ def main():
 
     from workloads import CONFIGS
 
+    if args.workload in SELECT_WORKLOADS:
+        return main_select(args)
     cfg = CONFIGS[args.workload]
     steps = args.steps if args.steps is not None else (
         cfg.steps if cfg.B == 1 and cfg.layers == 1 else (64 if cfg.layers > 1 else

@@ -168,7 +168,8 @@ int si_selective_ffn(const void* x, si_dtype xdt, int64_t B, int64_t d,
  * dispatch (hipExtLaunchKernelGGL): `start` takes the start time of the first of them and
  * `stop` the end time of the last (per-token path: the gather-GEMV kernel; union path: GEMM1
  * through GEMM2), so hipEventElapsedTime(start, stop) is their device time, without queueing
- * or marker overheads. Meant for eager timing runs, not for graph capture. Returns
+ * or marker overheads. si_dynamic_set and si_profile_scores attach them in the same way to
+ * their MFMA activation kernel (bf16 data). Meant for eager timing runs, not for graph capture. Returns
  * SI_ERR_INVALID if exactly one of the two is NULL.
  */
 int si_set_timing_events(void* start, void* stop);

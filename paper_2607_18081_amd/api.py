@@ -200,7 +200,8 @@ def residual_rmsnorm(x: torch.Tensor, y: torch.Tensor, eps: float = 1e-5,
 
 
 def dynamic_set(x: torch.Tensor, gate_up_c: torch.Tensor, static_slots: torch.Tensor,
-                alpha: int, n_total: int, workspace: torch.Tensor | None = None):
+                alpha: int, n_total: int, workspace: torch.Tensor | None = None,
+                out: torch.Tensor | None = None, counts: torch.Tensor | None = None):
     """si_dynamic_set: a prompt x [T][d] over a compacted layer -> (active slots [n_total]
     ascending, counts [L]: how many of the T per-token top-alpha lists hold each slot)."""
     dev = _dev(gate_up_c)
@@ -210,8 +211,12 @@ def dynamic_set(x: torch.Tensor, gate_up_c: torch.Tensor, static_slots: torch.Te
         raise ValueError("gate_up_c must be [L][2][d]")
     if static_slots.dtype != torch.int32:
         raise ValueError("static_slots must be int32")
-    out = torch.empty(n_total, dtype=torch.int32, device=dev)
-    counts = torch.empty(L, dtype=torch.int32, device=dev)
+    if out is None:
+        out = torch.empty(n_total, dtype=torch.int32, device=dev)
+    if counts is None:
+        counts = torch.empty(L, dtype=torch.int32, device=dev)
+    if out.numel() < n_total or counts.numel() < L:
+        raise ValueError("out needs n_total entries and counts L")
     lib = load()
     need = int(lib.si_dynamic_set_workspace(T, L, alpha, n_total))
     if workspace is None:

@@ -231,7 +231,8 @@ int si_dynamic_set(const void* x, si_dtype xdt, int64_t T, int64_t d, const void
     if (current_device() < 0) return SI_ERR_HIP;
     return from_hip(si::launch_dynamic_set(x, xdt, T, d, gate_up_c, L, wdt, static_slots,
                                            n_static, alpha, n_total, out_slots, counts, ws,
-                                           static_cast<hipStream_t>(hip_stream)));
+                                           static_cast<hipStream_t>(hip_stream), t_ev_start,
+                                           t_ev_stop));
 }
 
 size_t si_profile_scores_workspace(int64_t T, int64_t N, int64_t d, si_dtype xdt, si_dtype wdt) {
@@ -251,7 +252,8 @@ int si_profile_scores(const void* x, si_dtype xdt, int64_t T, int64_t d, const v
     if (!ws || ws_bytes < need || !aligned16(ws)) return SI_ERR_WORKSPACE;
     if (current_device() < 0) return SI_ERR_HIP;
     return from_hip(si::launch_scores(x, xdt, T, d, gate_up, N, wdt, scores, ws,
-                                      static_cast<hipStream_t>(hip_stream)));
+                                      static_cast<hipStream_t>(hip_stream), t_ev_start,
+                                      t_ev_stop));
 }
 
 int si_merge_scores(const float* scores, const int64_t* tokens, int64_t F, int64_t N, float* out,

@@ -153,10 +153,11 @@ inline bool mfma_ok(int xdt, int wdt, int64_t T, int64_t L, int64_t d) {
 }  // namespace
 
 hipError_t launch_activations(const void* x, int xdt, int64_t T, int64_t d, const void* gate_up_c,
-                              int64_t L, int wdt, float* out, int64_t ldo, hipStream_t s) {
+                              int64_t L, int wdt, float* out, int64_t ldo, hipStream_t s,
+                              hipEvent_t ev0, hipEvent_t ev1) {
     if (T == 0 || L == 0) return hipSuccess;
     if (mfma_ok(xdt, wdt, T, L, d))
-        return launch_activations_mfma(x, T, d, gate_up_c, L, out, ldo, 0, s);
+        return launch_activations_mfma(x, T, d, gate_up_c, L, out, ldo, 0, s, ev0, ev1);
     // grid y holds the tokens: at most 65535 per launch
     for (int64_t t0 = 0; t0 < T; t0 += 65535) {
         const int64_t nt = (T - t0) < 65535 ? (T - t0) : 65535;
@@ -187,13 +188,14 @@ size_t score_workspace(int64_t T, int64_t N, int64_t d, int xdt, int wdt) {
 }
 
 hipError_t launch_scores(const void* x, int xdt, int64_t T, int64_t d, const void* gate_up,
-                         int64_t N, int wdt, float* scores, void* ws, hipStream_t s) {
+                         int64_t N, int wdt, float* scores, void* ws, hipStream_t s,
+                         hipEvent_t ev0, hipEvent_t ev1) {
     if (T == 0 || N == 0) return hipSuccess;
     const int64_t ldo = (N + 63) / 64 * 64;
     float* buf = static_cast<float*>(ws);
     hipError_t e;
     if (mfma_ok(xdt, wdt, T, N, d)) {
-        e = launch_activations_mfma(x, T, d, gate_up, N, buf, ldo, 1, s);
+        e = launch_activations_mfma(x, T, d, gate_up, N, buf, ldo, 1, s, ev0, ev1);
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL(add_rows, dim3(blocks(N)), dim3(256), 0, s, buf,
                            (int64_t)activation_tiles(T), N, ldo, scores);
@@ -232,7 +234,7 @@ DynPlan dyn_plan(int64_t T, int64_t L, int64_t alpha, int64_t n_total) {
 hipError_t launch_dynamic_set(const void* x, int xdt, int64_t T, int64_t d, const void* gate_up_c,
                               int64_t L, int wdt, const int32_t* static_slots, int64_t n_static,
                               int64_t alpha, int64_t n_total, int32_t* out, int32_t* counts_out,
-                              void* ws, hipStream_t s) {
+                              void* ws, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
     const DynPlan p = dyn_plan(T, L, alpha, n_total);
     uint8_t* base = static_cast<uint8_t*>(ws);
     float* act = reinterpret_cast<float*>(base + p.off_act);
@@ -244,7 +246,7 @@ hipError_t launch_dynamic_set(const void* x, int xdt, int64_t T, int64_t d, cons
     int* cnt = reinterpret_cast<int*>(base + p.off_count);
     hipError_t e;
     // 1. activations of every loaded slot, per token
-    e = launch_activations(x, xdt, T, d, gate_up_c, L, wdt, act, p.lda, s);
+    e = launch_activations(x, xdt, T, d, gate_up_c, L, wdt, act, p.lda, s, ev0, ev1);
     if (e != hipSuccess) return e;
     // 2. each token's top alpha by |a|
     hipLaunchKernelGGL(fill_u32, dim3(blocks(L)), dim3(256), 0, s,

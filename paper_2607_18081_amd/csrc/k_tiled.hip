@@ -535,7 +535,8 @@ hipError_t launch_union_tiled(const void* x, int64_t B, int64_t d, const int32_t
 }
 
 hipError_t launch_activations_mfma(const void* x, int64_t T, int64_t d, const void* gate_up_c,
-                                   int64_t L, float* out, int64_t ldo, int score, hipStream_t s) {
+                                   int64_t L, float* out, int64_t ldo, int score, hipStream_t s,
+                                   hipEvent_t ev0, hipEvent_t ev1) {
     if (T == 0 || L == 0) return hipSuccess;
     const int ntm = (int)((T + kT1M - 1) / kT1M);
     const int nst = (int)((L + kT1S - 1) / kT1S);
@@ -543,13 +544,13 @@ hipError_t launch_activations_mfma(const void* x, int64_t T, int64_t d, const vo
     const bf16_t* xx = static_cast<const bf16_t*>(x);
     const bf16_t* gu = static_cast<const bf16_t*>(gate_up_c);
     if (score)
-        hipLaunchKernelGGL(gemm1_tiled<kScore>, dim3((unsigned)(nst8 * ntm)), dim3(256), 0, s, xx,
-                           T, d, gu, L, nullptr, nullptr, nullptr, (int64_t)0, nullptr, nullptr,
-                           ldo, ntm, out);
+        hipExtLaunchKernelGGL(gemm1_tiled<kScore>, dim3((unsigned)(nst8 * ntm)), dim3(256), 0, s,
+                              ev0, ev1, 0, xx, T, d, gu, L, nullptr, nullptr, nullptr, (int64_t)0,
+                              nullptr, nullptr, ldo, ntm, out);
     else
-        hipLaunchKernelGGL(gemm1_tiled<kAct>, dim3((unsigned)(nst8 * ntm)), dim3(256), 0, s, xx, T,
-                           d, gu, L, nullptr, nullptr, nullptr, (int64_t)0, nullptr, nullptr, ldo,
-                           ntm, out);
+        hipExtLaunchKernelGGL(gemm1_tiled<kAct>, dim3((unsigned)(nst8 * ntm)), dim3(256), 0, s,
+                              ev0, ev1, 0, xx, T, d, gu, L, nullptr, nullptr, nullptr, (int64_t)0,
+                              nullptr, nullptr, ldo, ntm, out);
     return hipGetLastError();
 }
 

@@ -47,7 +47,8 @@ hipError_t launch_union_tiled(const void* x, int64_t B, int64_t d, const int32_t
 // all-slots modes of the tiled GEMM1 (bf16): activations out[t * ldo + j] (score = 0) or one
 // Eq. 1 partial row per 256-token tile, out[tile * ldo + j] (score = 1)
 hipError_t launch_activations_mfma(const void* x, int64_t T, int64_t d, const void* gate_up_c,
-                                   int64_t L, float* out, int64_t ldo, int score, hipStream_t s);
+                                   int64_t L, float* out, int64_t ldo, int score, hipStream_t s,
+                                   hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 int activation_tiles(int64_t T);
 // ascending list of the set bits of bits[0..W) and their number
 hipError_t launch_bits_to_list(const uint32_t* bits, int64_t W, int32_t* list, int* count,
@@ -60,11 +61,14 @@ hipError_t launch_topk_strided(const float* scores, int64_t B, int64_t L, int64_
                                int mode, int32_t* out, hipStream_t s);
 
 // ---- k_select.hip: dynamic-set construction and profiler scores ----------------------------
+// ev0/ev1 (optional) are attached to the MFMA activation kernel's dispatch when it is used
 hipError_t launch_activations(const void* x, int xdt, int64_t T, int64_t d, const void* gate_up_c,
-                              int64_t L, int wdt, float* out, int64_t ldo, hipStream_t s);
+                              int64_t L, int wdt, float* out, int64_t ldo, hipStream_t s,
+                              hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 size_t score_workspace(int64_t T, int64_t N, int64_t d, int xdt, int wdt);
 hipError_t launch_scores(const void* x, int xdt, int64_t T, int64_t d, const void* gate_up,
-                         int64_t N, int wdt, float* scores, void* ws, hipStream_t s);
+                         int64_t N, int wdt, float* scores, void* ws, hipStream_t s,
+                         hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 struct DynPlan {
     int64_t lda, W;
     size_t off_act, off_lists, off_counts, off_keys, off_dyn, off_bits, off_count, total;
@@ -73,7 +77,8 @@ DynPlan dyn_plan(int64_t T, int64_t L, int64_t alpha, int64_t n_total);
 hipError_t launch_dynamic_set(const void* x, int xdt, int64_t T, int64_t d, const void* gate_up_c,
                               int64_t L, int wdt, const int32_t* static_slots, int64_t n_static,
                               int64_t alpha, int64_t n_total, int32_t* out, int32_t* counts_out,
-                              void* ws, hipStream_t s);
+                              void* ws, hipStream_t s, hipEvent_t ev0 = nullptr,
+                              hipEvent_t ev1 = nullptr);
 hipError_t launch_merge_file(const float* sc, int64_t N, float tokens, int first, float* out,
                              hipStream_t s);
 hipError_t launch_rank(const float* sc, int64_t N, int32_t* order, hipStream_t s);
