@@ -15,8 +15,9 @@ Other workloads (``--workload``) are available for measurement: tiny_f32, llama2
 (batch 16, union MFMA path), llama3_8b_stack (32 layers, residual RMSNorm between layers),
 llama2_13b_prefill (512 tokens, MFMA-bound union path); and the selection steps around the
 path: dynset_llama2_13b (dynamic-set construction for a 512-token prompt on the 13B-shape
-layer, si_dynamic_set) and profile_llama3_8b (Eq. 1 scores of 512 tokens over a full
-8B-shape FFN layer, si_profile_scores).
+layer, si_dynamic_set), profile_llama3_8b (Eq. 1 scores of 512 tokens over a full
+8B-shape FFN layer, si_profile_scores) and load_llama2_7b (selective loading of the 7B-shape
+layer from host memory, si_load_selected).
 """
 from __future__ import annotations
 
@@ -508,6 +509,87 @@ def main_select(args):
     print(json.dumps(out), flush=True)
 
 
+# --------------------------------------------------------------------------------------------
+# Selective loading from host memory
+# --------------------------------------------------------------------------------------------
+LOAD_WORKLOADS = {"load_llama2_7b": "llama2_7b_decode"}
+PCIE_PEAK_GBS = 64.0  # PCIe 5.0 x16, one direction (the MI355X host link)
+
+
+def main_load(args):
+    import numpy as np
+    import torch
+
+    import paper_2607_18081_amd as si
+    from workloads import CONFIGS, layer_weights, loaded_ids
+
+    cfg = CONFIGS[LOAD_WORKLOADS[args.workload]]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    wg, wu, wd = layer_weights(cfg, 0)          # the full layer, in host memory
+    loaded = loaded_ids(cfg, 0)
+    es = 2 if cfg.wdtype == "bf16" else 4
+    moved = 3 * cfg.d * len(loaded) * es        # Eq. 2: compacted bytes
+    steps = args.steps if args.steps is not None else 5
+    for _ in range(2):
+        layer = si.load_selected(wg, wu, wd, loaded)
+    del layer
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(steps):
+        t0 = time.perf_counter()
+        layer = si.load_selected(wg, wu, wd, loaded)
+        times.append(time.perf_counter() - t0)
+        del layer
+    wall = float(np.sum(times))
+    gbs = moved * steps / wall / 1e9
+    # measured ceiling: one pinned host-to-device copy of the same byte count
+    src = torch.empty(moved, dtype=torch.uint8).pin_memory()
+    dst = torch.empty(moved, dtype=torch.uint8, device=dev)
+    dst.copy_(src, non_blocking=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(3):
+        dst.copy_(src, non_blocking=True)
+    torch.cuda.synchronize()
+    ceil = 3 * moved / (time.perf_counter() - t0) / 1e9
+    # parity: the loaded layer against the oracle's compaction, bit for bit
+    import oracle
+    ref = oracle.compact(wg, wu, wd, loaded)
+    layer = si.load_selected(wg, wu, wd, loaded)
+    ok = all(np.array_equal(a, b) for a, b in (
+        (layer.gate_up_c.view(torch.int16).cpu().numpy().view(np.uint16), ref["gate_up_c"]),
+        (layer.down_c.view(torch.int16).cpu().numpy().view(np.uint16), ref["down_c"]),
+        (layer.slot_to_orig.cpu().numpy(), ref["slot_to_orig"])))
+    if not ok:
+        log("PARITY FAILURE: loaded layer differs from the oracle's compaction")
+        sys.exit(1)
+    cpu = None
+    if not args.no_cpu_baseline:
+        t0 = time.perf_counter()
+        oracle.compact(wg, wu, wd, loaded)
+        el = time.perf_counter() - t0
+        cpu = {"value": moved / el / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
+               "sample": f"one oracle compaction of the whole layer (Python loop over the {len(loaded)} "
+                         f"slots, host memory only), {el:.1f} s"}
+    out = {
+        "metric": "selective loading of one FFN layer from host memory, compacted GB/s",
+        "value": gbs, "unit": "GB/s", "n_gpus": 1, "steps": steps, "warmup": 2,
+        "ms_per_step": wall * 1e3 / steps, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": cfg.wdtype,
+        "data": "synthetic (seeded; weights N(0,0.02), Zipf(1.1) popularity)",
+        "config": {"workload": args.workload, "d": cfg.d, "N": cfg.N, "loaded": len(loaded),
+                   "bytes_moved": moved, "full_layer_bytes": 3 * cfg.d * cfg.N * es,
+                   "host_threads": min(os.cpu_count() or 4, 16), "parallelism": "single GPU"},
+        "roofline": {"bound": "pcie", "achieved": gbs, "peak": PCIE_PEAK_GBS, "unit": "GB/s",
+                     "frac": gbs / PCIE_PEAK_GBS, "traffic": None,
+                     "measured_h2d_copy_gbs": ceil, "bytes_per_launch": moved},
+        "cpu_baseline": cpu,
+        "parity": {"bit_exact": True},
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -523,6 +605,8 @@ def main():
 
     if args.workload in SELECT_WORKLOADS:
         return main_select(args)
+    if args.workload in LOAD_WORKLOADS:
+        return main_load(args)
     cfg = CONFIGS[args.workload]
     steps = args.steps if args.steps is not None else (
         cfg.steps if cfg.B == 1 and cfg.layers == 1 else (64 if cfg.layers > 1 else

@@ -246,6 +246,42 @@ int si_merge_scores(const float* scores, const int64_t* tokens, int64_t F, int64
  */
 int si_rank_neurons(const float* scores, int64_t N, int32_t* order, void* hip_stream);
 
+/*
+ * Loaded-set construction (Selective Loading section): the base neurons are the first n_base
+ * entries of the task-specific ranking; secondary neurons follow the model-level ranking, most
+ * relevant first, skipping neurons already chosen, until n_loaded neurons in all.
+ *
+ *   task_rank, model_rank [N] int32, HOST memory: each lists every neuron exactly once, most
+ *                             relevant first (si_rank_neurons of merged score files)
+ *   loaded     [n_loaded]     int32 out, HOST memory, in the order filled (base first)
+ *
+ * Host only: no device work. Requires 0 <= n_base <= n_loaded <= N. SI_ERR_INVALID when a
+ * ranking is not a permutation of [0, N).
+ */
+int si_build_loaded_set(const int32_t* task_rank, const int32_t* model_rank, int64_t N,
+                        int64_t n_base, int64_t n_loaded, int32_t* loaded);
+
+/*
+ * Selective loading from host memory (Selective Loading section): the same outputs as
+ * si_compact_ffn, but the full layer stays in host memory (any host buffer, e.g. a weight file
+ * mapped into memory) and only the loaded neurons' slices are read and moved to the device:
+ * 3 * d * L * s bytes (Eq. 2's compacted size) instead of 3 * d * N * s.
+ *
+ *   w_gate, w_up [N][d], w_down [d][N]  HOST memory, dtype wdt (PyTorch [out, in] storage)
+ *   loaded       [L]     int32 original ids, HOST memory, any order, unique, in [0, N)
+ *   gate_up_c    [L][2][d], down_c [L][d], slot_to_orig [L], orig_to_slot [N]  DEVICE out, as
+ *                        for si_compact_ffn (slots in ascending original id)
+ *
+ * Host threads gather the rows and the transposed down columns into two pinned staging
+ * buffers in turn while their copies to the device run on the stream. SYNCHRONOUS: returns
+ * after the copies have finished. SI_ERR_RANGE / SI_ERR_DUPLICATE for bad ids (nothing is
+ * moved). Calls are serialised within the process.
+ */
+int si_load_selected(const void* w_gate, const void* w_up, const void* w_down, int64_t N,
+                     int64_t d, si_dtype wdt, const int32_t* loaded, int64_t L,
+                     void* gate_up_c, void* down_c, int32_t* slot_to_orig, int32_t* orig_to_slot,
+                     void* hip_stream);
+
 #ifdef __cplusplus
 }
 #endif

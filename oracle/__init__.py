@@ -26,9 +26,11 @@ from .ffn import (  # noqa: F401
 )
 from .selection import (  # noqa: F401
     activations,
+    build_loaded_set,
     dynamic_set,
     merge_scores,
     profile_scores,
     rank_neurons,
     select_dynamic,
+    selective_layers,
 )

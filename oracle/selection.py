@@ -16,6 +16,11 @@ path; it shares no code with the GPU library or its binding.
 * ``merge_scores`` (LLM Profiler section): score files are merged by dividing each by its token
   count and summing.
 * ``rank_neurons`` (LLM Profiler section): neuron indices in decreasing order of importance.
+* ``build_loaded_set`` (Selective Loading section): the base neurons are the top delta of the
+  task-specific ranking; secondary neurons are added from the model-level ranking, most
+  relevant first, until the loading threshold gamma is reached.
+* ``selective_layers`` (Table 1): selective loading applies to the FFN layers from the fifth
+  to the second-to-last, 0-based [5, n - 2).
 
 Readings taken where the paper is silent (each is listed in the design notes):
 
@@ -27,7 +32,9 @@ Readings taken where the paper is silent (each is listed in the design notes):
 * "combine until phi is reached": the result holds every static slot plus the
   n_total - n_static most frequent non-static slots, so its size is exactly n_total; a slot
   that no token selected can fill the remainder (count 0, lower slots first);
-* ties in the importance ranking go to the lower neuron index.
+* ties in the importance ranking go to the lower neuron index;
+* the loaded set is returned in the order it is filled (base, then secondary); a secondary
+  neuron already in the base set is skipped, not counted.
 """
 from __future__ import annotations
 
@@ -118,3 +125,32 @@ def rank_neurons(scores) -> np.ndarray:
     v = np.asarray(scores, dtype=np.float64).reshape(-1)
     keys = [((1, 0.0) if math.isnan(v[n]) else (0, -float(v[n])), n) for n in range(v.shape[0])]
     return np.array([n for _, n in sorted(keys)], dtype=np.int32)
+
+
+def build_loaded_set(task_rank, model_rank, n_base: int, n_loaded: int) -> np.ndarray:
+    """Base = task_rank[:n_base]; then model_rank in order, skipping chosen neurons, until
+    n_loaded neurons in all. Both rankings list every neuron once."""
+    task = [int(v) for v in np.asarray(task_rank).reshape(-1).tolist()]
+    model = [int(v) for v in np.asarray(model_rank).reshape(-1).tolist()]
+    N = len(task)
+    if len(model) != N:
+        raise OracleError("rankings of different lengths")
+    for r in (task, model):
+        if sorted(r) != list(range(N)):
+            raise OracleError("a ranking must list every neuron exactly once")
+    if n_base < 0 or n_loaded < n_base or n_loaded > N:
+        raise OracleError(f"n_base={n_base}, n_loaded={n_loaded}, N={N}")
+    chosen = task[:n_base]
+    seen = set(chosen)
+    for n in model:
+        if len(chosen) == n_loaded:
+            break
+        if n not in seen:
+            chosen.append(n)
+            seen.add(n)
+    return np.array(chosen, dtype=np.int32)
+
+
+def selective_layers(n_layers: int, first: int = 5, last: int = -2) -> list:
+    """0-based indices of the layers whose FFN is loaded selectively: [first, n + last)."""
+    return [i for i in range(n_layers) if first <= i < n_layers + last]

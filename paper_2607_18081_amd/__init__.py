@@ -13,7 +13,9 @@ from .api import (  # noqa: F401
     TOPK_RAW,
     CompactLayer,
     SelectInferError,
+    build_loaded_set,
     compact_ffn,
+    load_selected,
     dynamic_set,
     merge_scores,
     profile_scores,

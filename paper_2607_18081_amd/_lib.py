@@ -37,6 +37,9 @@ SIGNATURES = {
                                   c_size, c_vp]),
     "si_merge_scores": (c_int, [c_vp, c_vp, c_i64, c_i64, c_vp, c_vp]),
     "si_rank_neurons": (c_int, [c_vp, c_i64, c_vp, c_vp]),
+    "si_build_loaded_set": (c_int, [c_vp, c_vp, c_i64, c_i64, c_i64, c_vp]),
+    "si_load_selected": (c_int, [c_vp, c_vp, c_vp, c_i64, c_i64, c_int, c_vp, c_i64, c_vp, c_vp,
+                                 c_vp, c_vp, c_vp]),
 }
 
 _lib = None

@@ -270,3 +270,51 @@ def rank_neurons(scores: torch.Tensor) -> torch.Tensor:
     st = load().si_rank_neurons(_ptr(scores), scores.numel(), _ptr(order), _stream(dev))
     _check(st, "si_rank_neurons")
     return order
+
+
+def build_loaded_set(task_rank, model_rank, n_base: int, n_loaded: int):
+    """si_build_loaded_set (host only): base = task_rank[:n_base], then model-ranked neurons
+    not yet chosen, until n_loaded. Rankings and result are int32 NumPy arrays."""
+    import numpy as np
+
+    t = np.ascontiguousarray(task_rank, dtype=np.int32)
+    m = np.ascontiguousarray(model_rank, dtype=np.int32)
+    if t.shape != m.shape or t.ndim != 1:
+        raise ValueError("rankings must be 1-D and of one length")
+    out = np.empty(max(int(n_loaded), 0), dtype=np.int32)
+    st = load().si_build_loaded_set(t.ctypes.data, m.ctypes.data, t.size, n_base, n_loaded,
+                                    out.ctypes.data if out.size else None)
+    _check(st, "si_build_loaded_set")
+    return out
+
+
+def load_selected(w_gate, w_up, w_down, loaded, device=None) -> CompactLayer:
+    """si_load_selected: full layer in HOST memory (NumPy arrays or memory maps; bf16 as uint16
+    bit patterns or float32) -> compacted layer on the device, moving only the loaded slices."""
+    import numpy as np
+
+    dev = torch.device(device or "cuda")
+    wg, wu, wd = (np.asarray(w) for w in (w_gate, w_up, w_down))
+    for w in (wg, wu, wd):
+        if not w.flags.c_contiguous:
+            raise ValueError("weights must be C-contiguous")
+    N, d = wg.shape
+    if wu.shape != (N, d) or wd.shape != (d, N) or wg.dtype != wu.dtype or wg.dtype != wd.dtype:
+        raise ValueError("expect W_gate, W_up [N][d] and W_down [d][N] of one dtype")
+    if wg.dtype == np.uint16:
+        wdt, tdt = BF16, torch.bfloat16
+    elif wg.dtype == np.float32:
+        wdt, tdt = F32, torch.float32
+    else:
+        raise TypeError(f"unsupported dtype {wg.dtype}")
+    ids = np.ascontiguousarray(loaded, dtype=np.int32).reshape(-1)
+    L = ids.size
+    gu = torch.empty((L, 2, d), dtype=tdt, device=dev)
+    dc = torch.empty((L, d), dtype=tdt, device=dev)
+    s2o = torch.empty(L, dtype=torch.int32, device=dev)
+    o2s = torch.empty(N, dtype=torch.int32, device=dev)
+    st = load().si_load_selected(wg.ctypes.data, wu.ctypes.data, wd.ctypes.data, N, d, wdt,
+                                 ids.ctypes.data, L, _ptr(gu), _ptr(dc), _ptr(s2o), _ptr(o2s),
+                                 _stream(dev))
+    _check(st, "si_load_selected")
+    return CompactLayer(gu, dc, s2o, o2s)

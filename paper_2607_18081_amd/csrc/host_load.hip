@@ -1,0 +1,210 @@
+// Selective loading from host memory (Selective Loading section): build the loaded set of a
+// layer from the profiler's rankings, and move only the loaded neurons' slices of a full FFN
+// layer held in host memory (a weight file mapped into memory, or any host buffer) into the
+// compacted, neuron-major device layout. The full layer never sits on the device; the bytes
+// moved are the compacted size of Eq. 2, 3 * d * L * s.
+//
+// Host side: a pool of threads gathers the loaded rows of W_gate and W_up, and the loaded
+// columns of W_down (a blocked transpose), into two pinned staging buffers in turn; each
+// buffer's host-to-device copy runs on the caller's stream while the other is being filled.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+#include <mutex>
+#include <thread>
+#include <vector>
+
+#include "selectinfer.h"
+
+namespace {
+
+constexpr size_t kStage = (size_t)64 << 20;  // bytes per pinned staging buffer
+
+struct Staging {
+    void* buf[2] = {nullptr, nullptr};
+    hipEvent_t done[2] = {nullptr, nullptr};
+    bool pending[2] = {false, false};
+};
+
+std::mutex g_mu;  // one staging pair per process, one loading call at a time
+Staging g_st;
+
+int workers() {
+    const unsigned n = std::thread::hardware_concurrency();
+    return n == 0 ? 4 : (int)std::min(n, 16u);
+}
+
+// f(lo, hi) on contiguous pieces of [0, n), one per worker
+template <class F>
+void parallel_for(int64_t n, F f) {
+    int w = workers();
+    if (n < w) w = (int)std::max<int64_t>(n, 1);
+    std::vector<std::thread> th;
+    th.reserve(w);
+    for (int i = 0; i < w; ++i)
+        th.emplace_back([=] { f(n * i / w, n * (i + 1) / w); });
+    for (auto& t : th) t.join();
+}
+
+hipError_t ensure_staging() {
+    for (int b = 0; b < 2; ++b) {
+        if (!g_st.buf[b]) {
+            hipError_t e = hipHostMalloc(&g_st.buf[b], kStage, hipHostMallocDefault);
+            if (e != hipSuccess) return e;
+        }
+        if (!g_st.done[b]) {
+            hipError_t e = hipEventCreateWithFlags(&g_st.done[b], hipEventDisableTiming);
+            if (e != hipSuccess) return e;
+        }
+    }
+    return hipSuccess;
+}
+
+// wait until staging buffer b's previous copy has finished
+hipError_t claim(int b) {
+    if (!g_st.pending[b]) return hipSuccess;
+    g_st.pending[b] = false;
+    return hipEventSynchronize(g_st.done[b]);
+}
+
+hipError_t ship(int b, void* dst, size_t bytes, hipStream_t s) {
+    hipError_t e = hipMemcpyAsync(dst, g_st.buf[b], bytes, hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) return e;
+    e = hipEventRecord(g_st.done[b], s);
+    g_st.pending[b] = (e == hipSuccess);
+    return e;
+}
+
+// down_c[s][i] = w_down[i][S[s]] for s in [s0, s1), into dst (slot-major, d per slot)
+template <typename T>
+void gather_down(const T* wd, int64_t N, int64_t d, const int32_t* S, int64_t s0, int64_t s1,
+                 T* dst) {
+    constexpr int64_t kRows = 16;  // rows of W_down per block: 16 elements per slot written
+    parallel_for((d + kRows - 1) / kRows, [&](int64_t b0, int64_t b1) {
+        for (int64_t blk = b0; blk < b1; ++blk) {
+            const int64_t i0 = blk * kRows;
+            const int64_t i1 = std::min(d, i0 + kRows);
+            for (int64_t s = s0; s < s1; ++s) {
+                const int64_t n = S[s];
+                T* o = dst + (s - s0) * d;
+                for (int64_t i = i0; i < i1; ++i) o[i] = wd[i * N + n];
+            }
+        }
+    });
+}
+
+}  // namespace
+
+extern "C" {
+
+int si_build_loaded_set(const int32_t* task_rank, const int32_t* model_rank, int64_t N,
+                        int64_t n_base, int64_t n_loaded, int32_t* loaded) {
+    if (N < 1 || !task_rank || !model_rank || !loaded) return SI_ERR_INVALID;
+    if (n_base < 0 || n_loaded < n_base || n_loaded > N) return SI_ERR_INVALID;
+    std::vector<uint8_t> seen((size_t)N, 0);
+    for (const int32_t* r : {task_rank, model_rank}) {  // each ranking lists every neuron once
+        std::fill(seen.begin(), seen.end(), 0);
+        for (int64_t i = 0; i < N; ++i) {
+            const int32_t v = r[i];
+            if (v < 0 || v >= N || seen[v]) return SI_ERR_INVALID;
+            seen[v] = 1;
+        }
+    }
+    std::fill(seen.begin(), seen.end(), 0);
+    int64_t m = 0;
+    for (int64_t i = 0; i < n_base; ++i) {
+        loaded[m++] = task_rank[i];
+        seen[task_rank[i]] = 1;
+    }
+    for (int64_t i = 0; i < N && m < n_loaded; ++i) {
+        const int32_t v = model_rank[i];
+        if (!seen[v]) {
+            loaded[m++] = v;
+            seen[v] = 1;
+        }
+    }
+    return SI_OK;
+}
+
+int si_load_selected(const void* w_gate, const void* w_up, const void* w_down, int64_t N,
+                     int64_t d, si_dtype wdt, const int32_t* loaded, int64_t L, void* gate_up_c,
+                     void* down_c, int32_t* slot_to_orig, int32_t* orig_to_slot,
+                     void* hip_stream) {
+    if (N < 1 || d < 1 || L < 1 || L > N || N > INT32_MAX) return SI_ERR_INVALID;
+    if (wdt != SI_F32 && wdt != SI_BF16) return SI_ERR_UNSUPPORTED;
+    if (!w_gate || !w_up || !w_down || !loaded || !gate_up_c || !down_c || !slot_to_orig ||
+        !orig_to_slot)
+        return SI_ERR_INVALID;
+    const int64_t es = wdt == SI_BF16 ? 2 : 4;
+    const size_t row = (size_t)(d * es);
+    if (2 * row > kStage) return SI_ERR_UNSUPPORTED;
+    // slots in ascending original id; reject ids out of range or repeated
+    std::vector<int32_t> S(loaded, loaded + L);
+    std::sort(S.begin(), S.end());
+    if (S.front() < 0 || S.back() >= N) return SI_ERR_RANGE;
+    for (int64_t i = 1; i < L; ++i)
+        if (S[i] == S[i - 1]) return SI_ERR_DUPLICATE;
+    std::vector<int32_t> o2s((size_t)N, -1);
+    for (int64_t s = 0; s < L; ++s) o2s[S[s]] = (int32_t)s;
+
+    std::lock_guard<std::mutex> lock(g_mu);
+    hipStream_t st = static_cast<hipStream_t>(hip_stream);
+    hipError_t e = ensure_staging();
+    int b = 0;
+    auto fail = [&](hipError_t err) {
+        (void)hipStreamSynchronize(st);
+        g_st.pending[0] = g_st.pending[1] = false;
+        return err == hipSuccess ? SI_OK : SI_ERR_HIP;
+    };
+    if (e != hipSuccess) return fail(e);
+
+    // the two maps
+    e = hipMemcpyAsync(slot_to_orig, S.data(), (size_t)L * 4, hipMemcpyHostToDevice, st);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(orig_to_slot, o2s.data(), (size_t)N * 4, hipMemcpyHostToDevice, st);
+    if (e != hipSuccess) return fail(e);
+
+    // gate_up_c[s] = (W_gate[S[s]], W_up[S[s]])
+    const char* wg = static_cast<const char*>(w_gate);
+    const char* wu = static_cast<const char*>(w_up);
+    const int64_t cs_gu = (int64_t)(kStage / (2 * row));
+    for (int64_t s0 = 0; s0 < L; s0 += cs_gu) {
+        const int64_t s1 = std::min(L, s0 + cs_gu);
+        if ((e = claim(b)) != hipSuccess) return fail(e);
+        char* dst = static_cast<char*>(g_st.buf[b]);
+        parallel_for(s1 - s0, [&](int64_t a, int64_t z) {
+            for (int64_t s = a; s < z; ++s) {
+                const int64_t n = S[s0 + s];
+                std::memcpy(dst + s * 2 * row, wg + n * row, row);
+                std::memcpy(dst + s * 2 * row + row, wu + n * row, row);
+            }
+        });
+        if ((e = ship(b, static_cast<char*>(gate_up_c) + s0 * 2 * row, (s1 - s0) * 2 * row,
+                      st)) != hipSuccess)
+            return fail(e);
+        b ^= 1;
+    }
+    // down_c[s] = column S[s] of W_down
+    const int64_t cs_d = (int64_t)(kStage / row);
+    for (int64_t s0 = 0; s0 < L; s0 += cs_d) {
+        const int64_t s1 = std::min(L, s0 + cs_d);
+        if ((e = claim(b)) != hipSuccess) return fail(e);
+        if (es == 2)
+            gather_down(static_cast<const uint16_t*>(w_down), N, d, S.data(), s0, s1,
+                        static_cast<uint16_t*>(g_st.buf[b]));
+        else
+            gather_down(static_cast<const uint32_t*>(w_down), N, d, S.data(), s0, s1,
+                        static_cast<uint32_t*>(g_st.buf[b]));
+        if ((e = ship(b, static_cast<char*>(down_c) + s0 * row, (s1 - s0) * row, st)) !=
+            hipSuccess)
+            return fail(e);
+        b ^= 1;
+    }
+    // the maps' host vectors and the staging buffers must outlive the copies
+    e = hipStreamSynchronize(st);
+    g_st.pending[0] = g_st.pending[1] = false;
+    return e == hipSuccess ? SI_OK : SI_ERR_HIP;
+}
+
+}  // extern "C"

@@ -394,5 +394,39 @@ def pin_profile_scores(impl):
     assert [int(v) for v in impl.rank_neurons([float("nan"), 0.0, -1.0])] == [1, 2, 0]
 
 
+def pin_loaded_set(impl):
+    task = [4, 1, 7, 0, 2, 6, 5, 3]
+    model = [1, 2, 4, 3, 0, 7, 6, 5]
+    got = [int(v) for v in impl.build_loaded_set(task, model, 2, 5)]
+    assert got == [4, 1, 2, 3, 0]          # 1 and 4 are already base: skipped, not counted
+    assert [int(v) for v in impl.build_loaded_set(task, model, 3, 3)] == [4, 1, 7]
+    assert [int(v) for v in impl.build_loaded_set(task, model, 0, 2)] == [1, 2]
+    assert sorted(int(v) for v in impl.build_loaded_set(task, model, 3, 8)) == list(range(8))
+    rng = np.random.default_rng(9)
+    for _ in range(5):
+        N = 50
+        t, m = rng.permutation(N), rng.permutation(N)
+        nb, nl = int(rng.integers(0, 20)), int(rng.integers(20, 40))
+        got = [int(v) for v in impl.build_loaded_set(t, m, nb, nl)]
+        assert len(got) == nl == len(set(got))
+        assert got[:nb] == t[:nb].tolist()
+        # the secondary neurons are the most relevant model-level ones outside the base
+        rest = [int(v) for v in m if int(v) not in set(t[:nb].tolist())]
+        assert got[nb:] == rest[:nl - nb]
+    for bad in ((task, model, 3, 2), (task, model, 1, 9), ([0, 0, 1], [0, 1, 2], 1, 2)):
+        try:
+            impl.build_loaded_set(*bad)
+        except Exception:
+            continue
+        raise AssertionError(f"accepted {bad}")
+    # Table 1 layer range: 21 of 28 layers (r_layer = 0.75 in Eq. 2) and 9 of 16
+    with open(os.path.join(GOLDEN, "table1_parameters.json")) as f:
+        t1 = json.load(f)
+    assert len(impl.selective_layers(t1["n_layers_llama32_3b"])) == 21
+    assert len(impl.selective_layers(t1["n_layers_llama32_1b"])) == t1["selected_layers_llama32_1b"]
+    assert impl.selective_layers(8) == [5]
+
+
 ALL_PINS = [pin_silu, pin_topk, pin_compact, pin_remap, pin_ffn_invariants, pin_hand_integer,
-            pin_rmsnorm, pin_memory, pin_activations, pin_dynamic_set, pin_profile_scores]
+            pin_rmsnorm, pin_memory, pin_activations, pin_dynamic_set, pin_profile_scores,
+            pin_loaded_set]

@@ -153,7 +153,27 @@ def _rank_ascending(scores):
     return S.rank_neurons(scores)[::-1].copy()
 
 
+def _loaded_counts_skips(task_rank, model_rank, n_base, n_loaded):
+    task = [int(v) for v in task_rank]
+    chosen = task[:n_base]
+    for n in [int(v) for v in model_rank][:n_loaded - n_base]:   # mistake: skips use up slots
+        if n not in chosen:
+            chosen.append(n)
+    return np.array(chosen, np.int32)
+
+
+def _loaded_model_first(task_rank, model_rank, n_base, n_loaded):
+    return S.build_loaded_set(model_rank, task_rank, n_base, n_loaded)
+
+
+def _layers_inclusive(n_layers, first=5, last=-2):
+    return [i for i in range(n_layers) if first <= i <= n_layers + last]
+
+
 MUTANTS = {
+    "loaded_skips_count": dict(build_loaded_set=_loaded_counts_skips),
+    "loaded_model_first": dict(build_loaded_set=_loaded_model_first),
+    "layers_inclusive": dict(selective_layers=_layers_inclusive),
     "dyn_raw_key": dict(select_dynamic=_dyn_with(per_token_mode="raw")),
     "dyn_freq_high_index_ties": dict(select_dynamic=_dyn_with(freq_high_ties=True)),
     "dyn_static_not_excluded": dict(select_dynamic=_dyn_with(exclude_static=False)),
