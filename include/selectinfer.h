@@ -37,7 +37,9 @@
 extern "C" {
 #endif
 
-typedef enum { SI_F32 = 0, SI_BF16 = 1 } si_dtype;
+/* element types: float32, bfloat16, IEEE half (the paper's float16 storage, Memory Footprint
+   section) */
+typedef enum { SI_F32 = 0, SI_BF16 = 1, SI_F16 = 2 } si_dtype;
 
 typedef enum {
     SI_OK = 0,
@@ -133,7 +135,8 @@ size_t si_selective_ffn_workspace(int64_t B, int64_t nnz, int64_t L, int64_t d,
  *
  *   y[b] = sum_{j in A_b} SiLU(gate_c[j] . x[b]) * (up_c[j] . x[b]) * down_c[j]
  *
- *   x         [B][d]   token activations, dtype xdt (SI_F32 or SI_BF16)
+ *   x         [B][d]   token activations, dtype xdt: SI_F32, or the weights' type (f32
+ *                      weights also take SI_BF16 x)
  *   offsets   [B+1]    int32: token b's active slots are idx[offsets[b] .. offsets[b+1])
  *   idx       [nnz]    int32 slot ids in [0, L), any order, no duplicates within a token
  *   gate_up_c [L][2][d], down_c [L][d]  compacted layer from si_compact_ffn, dtype wdt
@@ -144,12 +147,13 @@ size_t si_selective_ffn_workspace(int64_t B, int64_t nnz, int64_t L, int64_t d,
  *   - per-token (B == 1, fp32 weights or x, or SI_FLAG_PER_TOKEN): a gather-GEMV streams only
  *     the active rows with 16-byte loads and a fused SiLU*up epilogue, then accumulates the
  *     down rows into float32 partial sums that a second kernel adds in a fixed order;
- *   - union (B >= 2, bf16 weights and x): the union of the B active sets is built on the
- *     device and both projections run as bf16 MFMA gather-GEMMs over the union rows, with
+ *   - union (B >= 2, x and weights both bf16 or both half): the union of the B active sets
+ *     is built on the device and both projections run as MFMA gather-GEMMs over the union
+ *     rows, with
  *     each token's h masked to its own set; below 128 tokens the union rows are streamed
  *     once (bandwidth bound), from 128 tokens on the products are LDS-tiled (compute bound).
- * Requirements: d % 8 == 0 for bf16 data, d % 4 == 0 for f32; d <= 32768 (bf16) or 16384
- * (f32); 16-byte aligned x, gate_up_c, down_c, y and ws; B >= 0; nnz >= 0; L >= 1.
+ * Requirements: d % 8 == 0 for 16-bit data, d % 4 == 0 for f32; d <= 32768 (16-bit) or
+ * 16384 (f32); 16-byte aligned x, gate_up_c, down_c, y and ws; B >= 0; nnz >= 0; L >= 1.
  * SI_FLAG_CHECK validates offsets (non-decreasing, within [0, nnz]), slot range and duplicates
  * on the device, synchronises and returns SI_ERR_RANGE / SI_ERR_DUPLICATE before computing.
  */
@@ -177,7 +181,8 @@ int si_set_timing_events(void* start, void* stop);
 /*
  * Layer step of a stacked FFN: x_out[b] = RMSNorm(x[b] + y[b]) with unit gain,
  * r / sqrt(mean(r^2) + eps), computed in float32 and stored in xdt (bf16: round to nearest
- * even). x [B][d] (xdt), y [B][d] float32, x_out [B][d] (xdt); x_out may alias x.
+ * even). x [B][d] (xdt: SI_F32 or SI_BF16), y [B][d] float32, x_out [B][d] (xdt); x_out may
+ * alias x.
  */
 int si_residual_rmsnorm(const void* x, si_dtype xdt, const float* y, int64_t B, int64_t d,
                         float eps, void* x_out, void* hip_stream);

@@ -28,8 +28,8 @@ Readings taken where the paper is silent (each is listed in the design notes):
 * the stack workload's layer step is x' = bf16_RNE(r / sqrt(mean(r^2) + 1e-5)) with
   r = x + y and unit gain.
 
-Inputs are the exact storage arrays the GPU receives: float32, or bf16 bit patterns held in
-uint16. ``decode`` widens them to float64 exactly, so there is no input-rounding ambiguity.
+Inputs are the exact storage arrays the GPU receives: float32, IEEE half (float16), or bf16
+bit patterns held in uint16. ``decode`` widens them to float64 exactly, so there is no input-rounding ambiguity.
 All arithmetic is float64.
 """
 from __future__ import annotations
@@ -59,11 +59,13 @@ class NotLoadedError(OracleError):
 # storage <-> float64
 # --------------------------------------------------------------------------------------------
 def decode(a: np.ndarray) -> np.ndarray:
-    """Storage array -> float64. uint16 is read as bf16 bits (the upper half of a float32)."""
+    """Storage array -> float64. uint16 is read as bf16 bits (the upper half of a float32);
+    float16 (the paper's weight storage, 2 bytes per parameter in the Memory Footprint section)
+    and float32 widen exactly."""
     a = np.asarray(a)
     if a.dtype == np.uint16:
         return (a.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
-    if a.dtype == np.float32:
+    if a.dtype == np.float32 or a.dtype == np.float16:
         return a.astype(np.float64)
     raise TypeError(f"unsupported storage dtype {a.dtype}")
 

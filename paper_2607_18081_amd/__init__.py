@@ -5,6 +5,7 @@ The C ABI (include/selectinfer.h) is implemented in HIP for gfx950 in ``csrc/`` 
 """
 from .api import (  # noqa: F401
     BF16,
+    F16,
     F32,
     FLAG_CHECK,
     FLAG_FAST_H,

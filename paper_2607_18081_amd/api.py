@@ -12,11 +12,11 @@ import torch
 
 from ._lib import load
 
-F32, BF16 = 0, 1
+F32, BF16, F16 = 0, 1, 2
 TOPK_ABS, TOPK_RAW = 0, 1
 FLAG_CHECK, FLAG_PER_TOKEN, FLAG_FAST_H = 1, 2, 4
 
-_DT = {torch.float32: F32, torch.bfloat16: BF16}
+_DT = {torch.float32: F32, torch.bfloat16: BF16, torch.float16: F16}
 
 
 class SelectInferError(RuntimeError):
@@ -303,6 +303,8 @@ def load_selected(w_gate, w_up, w_down, loaded, device=None) -> CompactLayer:
         raise ValueError("expect W_gate, W_up [N][d] and W_down [d][N] of one dtype")
     if wg.dtype == np.uint16:
         wdt, tdt = BF16, torch.bfloat16
+    elif wg.dtype == np.float16:
+        wdt, tdt = F16, torch.float16
     elif wg.dtype == np.float32:
         wdt, tdt = F32, torch.float32
     else:

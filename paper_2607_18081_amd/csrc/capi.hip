@@ -69,14 +69,20 @@ int checked(hipStream_t s, int dev, F enqueue) {
 thread_local hipEvent_t t_ev_start = nullptr;
 thread_local hipEvent_t t_ev_stop = nullptr;
 
-bool valid_dtype(int t) { return t == SI_F32 || t == SI_BF16; }
+bool valid_dtype(int t) { return t == SI_F32 || t == SI_BF16 || t == SI_F16; }
+
+// x and weight types used together: x is float32 or of the weights' type (and f32 weights
+// also take bf16 or half x)
+bool valid_pair(int xdt, int wdt) {
+    return valid_dtype(xdt) && valid_dtype(wdt) && (xdt == SI_F32 || wdt == SI_F32 || xdt == wdt);
+}
 
 bool use_union(int64_t B, int64_t L, int64_t d, si_dtype xdt, si_dtype wdt, int flags) {
     // Reading the union once costs |U| rows instead of nnz >= |U|, and the dense-over-union
     // MFMA work stays far below the HBM time of those rows for any overlap (see the design
     // notes), so B >= 2 always takes it when the dtypes allow bf16 MFMA.
-    return B >= 2 && xdt == SI_BF16 && wdt == SI_BF16 && !(flags & SI_FLAG_PER_TOKEN) &&
-           si::union_supported(B, L, d);
+    return B >= 2 && xdt == wdt && (wdt == SI_BF16 || wdt == SI_F16) &&
+           !(flags & SI_FLAG_PER_TOKEN) && si::union_supported(B, L, d);
 }
 
 }  // namespace
@@ -108,7 +114,7 @@ int si_compact_ffn(const void* w_gate, const void* w_up, const void* w_down, int
         return SI_ERR_INVALID;
     if (!valid_dtype(wdt)) return SI_ERR_UNSUPPORTED;
     if (N < 1 || d < 1 || L < 1 || L > N || N > INT32_MAX) return SI_ERR_INVALID;
-    const int es = wdt == SI_BF16 ? 2 : 4;
+    const int es = wdt == SI_F32 ? 4 : 2;
     if ((d * es) % 16 != 0) return SI_ERR_UNSUPPORTED;
     if (!aligned16(w_gate) || !aligned16(w_up) || !aligned16(gate_up_c)) return SI_ERR_INVALID;
     const int dev = current_device();
@@ -164,7 +170,7 @@ int si_selective_ffn(const void* x, si_dtype xdt, int64_t B, int64_t d, const in
                      int64_t L, si_dtype wdt, float* y, void* ws, size_t ws_bytes, int flags,
                      void* hip_stream) {
     if (B < 0 || d < 1 || L < 1 || nnz < 0) return SI_ERR_INVALID;
-    if (!valid_dtype(xdt) || !valid_dtype(wdt)) return SI_ERR_UNSUPPORTED;
+    if (!valid_pair(xdt, wdt)) return SI_ERR_UNSUPPORTED;
     if (B > 65535 || nnz > INT32_MAX || L > INT32_MAX) return SI_ERR_UNSUPPORTED;
     if (si::decode_supported(xdt, wdt, d)) return SI_ERR_UNSUPPORTED;
     if (B == 0) return SI_OK;
@@ -186,8 +192,8 @@ int si_selective_ffn(const void* x, si_dtype xdt, int64_t B, int64_t d, const in
     }
     const int ncu = num_cu(dev);
     if (use_union(B, L, d, xdt, wdt, flags))
-        return from_hip(si::launch_union(x, B, d, offsets, idx, nnz, gate_up_c, down_c, L, y, ws,
-                                         flags, ncu, s, t_ev_start, t_ev_stop));
+        return from_hip(si::launch_union(x, B, d, offsets, idx, nnz, gate_up_c, down_c, L, wdt, y,
+                                         ws, flags, ncu, s, t_ev_start, t_ev_stop));
     const int P = si::decode_chunks(B, nnz, ncu);
     return from_hip(si::launch_decode(x, xdt, B, d, offsets, idx, nnz, gate_up_c, down_c, L, wdt,
                                       static_cast<float*>(ws), P, y, s, t_ev_start, t_ev_stop));
@@ -203,7 +209,7 @@ int si_set_timing_events(void* start, void* stop) {
 int si_residual_rmsnorm(const void* x, si_dtype xdt, const float* y, int64_t B, int64_t d,
                         float eps, void* x_out, void* hip_stream) {
     if (B < 0 || d < 1 || !(eps >= 0.0f)) return SI_ERR_INVALID;
-    if (!valid_dtype(xdt)) return SI_ERR_UNSUPPORTED;
+    if (xdt != SI_F32 && xdt != SI_BF16) return SI_ERR_UNSUPPORTED;
     if (B == 0) return SI_OK;
     if (!x || !y || !x_out) return SI_ERR_INVALID;
     return from_hip(si::launch_residual_rmsnorm(x, xdt, y, B, d, eps, x_out,
@@ -222,7 +228,7 @@ int si_dynamic_set(const void* x, si_dtype xdt, int64_t T, int64_t d, const void
     if (T < 0 || d < 1 || L < 1 || L > (1 << 24)) return SI_ERR_INVALID;
     if (alpha < 0 || alpha > L || n_static < 0 || n_static > n_total || n_total > L)
         return SI_ERR_INVALID;
-    if (!valid_dtype(xdt) || !valid_dtype(wdt)) return SI_ERR_UNSUPPORTED;
+    if (!valid_pair(xdt, wdt)) return SI_ERR_UNSUPPORTED;
     if ((T > 0 && !x) || !gate_up_c || (n_static > 0 && !static_slots)) return SI_ERR_INVALID;
     if (n_total > 0 && !out_slots) return SI_ERR_INVALID;
     if (!aligned16(x) || !aligned16(gate_up_c)) return SI_ERR_INVALID;
@@ -244,7 +250,7 @@ int si_profile_scores(const void* x, si_dtype xdt, int64_t T, int64_t d, const v
                       int64_t N, si_dtype wdt, float* scores, void* ws, size_t ws_bytes,
                       void* hip_stream) {
     if (T < 0 || d < 1 || N < 1 || N > INT32_MAX) return SI_ERR_INVALID;
-    if (!valid_dtype(xdt) || !valid_dtype(wdt)) return SI_ERR_UNSUPPORTED;
+    if (!valid_pair(xdt, wdt)) return SI_ERR_UNSUPPORTED;
     if (T == 0) return SI_OK;
     if (!x || !gate_up || !scores) return SI_ERR_INVALID;
     if (!aligned16(x) || !aligned16(gate_up)) return SI_ERR_INVALID;

@@ -9,6 +9,7 @@ namespace si {
 constexpr int kWave = 64;
 
 typedef uint16_t bf16_t;  // bfloat16 bit pattern
+typedef _Float16 f16_t;   // IEEE half precision
 
 // Error word layout written by device-side checks (first nonzero code wins).
 struct ErrWord {
@@ -34,6 +35,14 @@ __device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
     uint32_t u = __float_as_uint(f);
     u += 0x7fffu + ((u >> 16) & 1u);
     return u >> 16;
+}
+
+// half precision <-> float32 (hardware conversion, round to nearest even)
+__device__ __forceinline__ float f16_to_f32(uint32_t bits16) {
+    return (float)__builtin_bit_cast(_Float16, (uint16_t)bits16);
+}
+__device__ __forceinline__ uint32_t f32_to_f16_rne(float f) {
+    return __builtin_bit_cast(uint16_t, (_Float16)f);
 }
 
 // 16-byte vector types
@@ -91,6 +100,17 @@ struct Elem<float> {
     __device__ __forceinline__ static void unpack(const V16& v, float* f) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) f[e] = __uint_as_float(v.w[e]);
+    }
+};
+template <>
+struct Elem<f16_t> {
+    static constexpr int V = 8;
+    __device__ __forceinline__ static void unpack(const V16& v, float* f) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            f[2 * e] = f16_to_f32(v.w[e] & 0xffffu);
+            f[2 * e + 1] = f16_to_f32(v.w[e] >> 16);
+        }
     }
 };
 template <>

@@ -132,11 +132,11 @@ int si_load_selected(const void* w_gate, const void* w_up, const void* w_down, i
                      void* down_c, int32_t* slot_to_orig, int32_t* orig_to_slot,
                      void* hip_stream) {
     if (N < 1 || d < 1 || L < 1 || L > N || N > INT32_MAX) return SI_ERR_INVALID;
-    if (wdt != SI_F32 && wdt != SI_BF16) return SI_ERR_UNSUPPORTED;
+    if (wdt != SI_F32 && wdt != SI_BF16 && wdt != SI_F16) return SI_ERR_UNSUPPORTED;
     if (!w_gate || !w_up || !w_down || !loaded || !gate_up_c || !down_c || !slot_to_orig ||
         !orig_to_slot)
         return SI_ERR_INVALID;
-    const int64_t es = wdt == SI_BF16 ? 2 : 4;
+    const int64_t es = wdt == SI_F32 ? 4 : 2;
     const size_t row = (size_t)(d * es);
     if (2 * row > kStage) return SI_ERR_UNSUPPORTED;
     // slots in ascending original id; reject ids out of range or repeated

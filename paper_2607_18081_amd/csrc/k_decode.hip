@@ -71,6 +71,10 @@ struct XSlice {
     __device__ __forceinline__ static float xval(const uint32_t (&wd)[N], int e, const bf16_t*) {
         return (e & 1) ? bf16hi(wd[e >> 1]) : bf16lo(wd[e >> 1]);
     }
+    template <int N>
+    __device__ __forceinline__ static float xval(const uint32_t (&wd)[N], int e, const f16_t*) {
+        return f16_to_f32((e & 1) ? (wd[e >> 1] >> 16) : (wd[e >> 1] & 0xffffu));
+    }
     __device__ __forceinline__ float dot(const V16& w, float acc) const {
         float f[V];
         Elem<WT>::unpack(w, f);
@@ -93,6 +97,25 @@ struct XSlice<bf16_t, bf16_t> {
         for (int q = 0; q < 4; ++q)
             acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w.w[q]),
                                                   __builtin_bit_cast(bf16x2_t, v[q]), acc, false);
+        return acc;
+    }
+};
+
+typedef __attribute__((ext_vector_type(2))) _Float16 f16x2_t;
+
+template <>
+struct XSlice<f16_t, f16_t> {
+    uint32_t v[4];
+    __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t r, int off) {
+        const V16 t = bload16(r, off);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[q] = t.w[q];
+    }
+    __device__ __forceinline__ float dot(const V16& w, float acc) const {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            acc = __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2_t, w.w[q]),
+                                         __builtin_bit_cast(f16x2_t, v[q]), acc, false);
         return acc;
     }
 };
@@ -449,9 +472,13 @@ hipError_t launch_rows_t(const void* x, int64_t B, int64_t d, const int32_t* off
 }  // namespace
 
 int decode_supported(int xdt, int wdt, int64_t d) {
-    const int V = wdt == 1 ? 8 : 4;
+    // x is float32 or has the weights' type; half-precision weights pair with half or f32 x,
+    // bf16 weights with bf16 or f32 x, f32 weights with f32 or bf16 x
+    if (wdt == 2 && xdt != 2 && xdt != 0) return 1;
+    if (xdt == 2 && wdt != 2) return 1;
+    const int V = wdt == 0 ? 4 : 8;
     if (d <= 0 || d % V != 0) return 1;
-    if (xdt == 1 && d % 8 != 0) return 1;
+    if (xdt != 0 && d % 8 != 0) return 1;
     if (d > (int64_t)4 * kThreads * V) return 1;
     return 0;
 }
@@ -476,7 +503,7 @@ hipError_t launch_decode(const void* x, int xdt, int64_t B, int64_t d, const int
     if (B == 0) return hipSuccess;
     hipError_t e;
     // buffer loads take 32-bit byte offsets: both compacted tensors must stay below 2 GiB
-    const int64_t es = wdt == 1 ? 2 : 4;
+    const int64_t es = wdt == 0 ? 4 : 2;
     const bool buf = L * 2 * d * es < ((int64_t)1 << 31);
 #define SI_DEC(WT, XT)                                                                        \
     (buf ? launch_rows_t<WT, XT, true>(x, B, d, offsets, idx, nnz, gate_up_c, down_c, L,      \
@@ -489,8 +516,14 @@ hipError_t launch_decode(const void* x, int xdt, int64_t B, int64_t d, const int
         e = SI_DEC(bf16_t, float);
     else if (wdt == 0 && xdt == 1)
         e = SI_DEC(float, bf16_t);
-    else
+    else if (wdt == 2 && xdt == 2)
+        e = SI_DEC(f16_t, f16_t);
+    else if (wdt == 2 && xdt == 0)
+        e = SI_DEC(f16_t, float);
+    else if (wdt == 0 && xdt == 0)
         e = SI_DEC(float, float);
+    else
+        return hipErrorInvalidValue;  // excluded by decode_supported
 #undef SI_DEC
     if (e != hipSuccess) return e;
     return launch_reduce_partials(partials, P, B, d, y, s);

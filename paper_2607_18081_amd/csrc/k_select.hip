@@ -27,6 +27,8 @@ template <>
 __device__ __forceinline__ float ldf<float>(const float* p) { return *p; }
 template <>
 __device__ __forceinline__ float ldf<bf16_t>(const bf16_t* p) { return bf16_to_f32(*p); }
+template <>
+__device__ __forceinline__ float ldf<f16_t>(const f16_t* p) { return (float)*p; }
 
 // Grid (ceil(L / 4), T), 256 threads: wave w takes slot 4 blockIdx.x + w of token blockIdx.y.
 template <typename WT, typename XT>
@@ -145,9 +147,10 @@ __global__ __launch_bounds__(256) void rank_scores(const float* __restrict__ s, 
 
 inline unsigned blocks(int64_t n) { return (unsigned)((n + 255) / 256); }
 
-// bf16 data with whole 16-byte K chunks and 32-bit buffer offsets take the MFMA tiles
+// 16-bit data (bf16 or half, x and weights alike) with whole 16-byte K chunks and 32-bit
+// buffer offsets take the MFMA tiles
 inline bool mfma_ok(int xdt, int wdt, int64_t T, int64_t L, int64_t d) {
-    return xdt == 1 && wdt == 1 && d % 8 == 0 && tiled_supported(T, L, d);
+    return xdt == wdt && (wdt == 1 || wdt == 2) && d % 8 == 0 && tiled_supported(T, L, d);
 }
 
 }  // namespace
@@ -157,7 +160,7 @@ hipError_t launch_activations(const void* x, int xdt, int64_t T, int64_t d, cons
                               hipEvent_t ev0, hipEvent_t ev1) {
     if (T == 0 || L == 0) return hipSuccess;
     if (mfma_ok(xdt, wdt, T, L, d))
-        return launch_activations_mfma(x, T, d, gate_up_c, L, out, ldo, 0, s, ev0, ev1);
+        return launch_activations_mfma(x, T, d, gate_up_c, L, wdt, out, ldo, 0, s, ev0, ev1);
     // grid y holds the tokens: at most 65535 per launch
     for (int64_t t0 = 0; t0 < T; t0 += 65535) {
         const int64_t nt = (T - t0) < 65535 ? (T - t0) : 65535;
@@ -170,12 +173,20 @@ hipError_t launch_activations(const void* x, int xdt, int64_t T, int64_t d, cons
                        o, ldo)
         if (wdt == 1 && xdt == 1)
             SI_ACT(bf16_t, bf16_t);
-        else if (wdt == 1)
+        else if (wdt == 1 && xdt == 0)
             SI_ACT(bf16_t, float);
-        else if (xdt == 1)
+        else if (wdt == 0 && xdt == 1)
             SI_ACT(float, bf16_t);
-        else
+        else if (wdt == 2 && xdt == 2)
+            SI_ACT(f16_t, f16_t);
+        else if (wdt == 2 && xdt == 0)
+            SI_ACT(f16_t, float);
+        else if (wdt == 0 && xdt == 2)
+            SI_ACT(float, f16_t);
+        else if (wdt == 0 && xdt == 0)
             SI_ACT(float, float);
+        else
+            return hipErrorInvalidValue;  // bf16 with half: not a supported pair
     }
 #undef SI_ACT
     return hipGetLastError();
@@ -195,7 +206,7 @@ hipError_t launch_scores(const void* x, int xdt, int64_t T, int64_t d, const voi
     float* buf = static_cast<float*>(ws);
     hipError_t e;
     if (mfma_ok(xdt, wdt, T, N, d)) {
-        e = launch_activations_mfma(x, T, d, gate_up, N, buf, ldo, 1, s, ev0, ev1);
+        e = launch_activations_mfma(x, T, d, gate_up, N, wdt, buf, ldo, 1, s, ev0, ev1);
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL(add_rows, dim3(blocks(N)), dim3(256), 0, s, buf,
                            (int64_t)activation_tiles(T), N, ldo, scores);

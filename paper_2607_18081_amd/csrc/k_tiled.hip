@@ -26,25 +26,13 @@
 
 #include "common.h"
 #include "launch.h"
+#include "mfma.h"
 
 namespace si {
 
 namespace {
 
-typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
-typedef __attribute__((ext_vector_type(4))) float f32x4_t;
-typedef __attribute__((ext_vector_type(4))) unsigned int u32x4_t;
 typedef __attribute__((ext_vector_type(4))) short s16x4_t;
-
-__device__ __forceinline__ bf16x8_t as_bf16x8(const V16& v) {
-    const u32x4_t t = {v.w[0], v.w[1], v.w[2], v.w[3]};
-    return __builtin_bit_cast(bf16x8_t, t);
-}
-
-__device__ __forceinline__ f32x4_t mfma16x16x32(const bf16x8_t& a, const bf16x8_t& b,
-                                                const f32x4_t& c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-}
 
 constexpr int kBK = 64;          // K step (elements)
 constexpr int kKP = kBK + 8;     // LDS pitch (bf16) of K-contiguous tiles: 144 bytes
@@ -127,12 +115,12 @@ __global__ __launch_bounds__(1024) void union_scan(const uint32_t* __restrict__ 
 //            tile; the host-side reducer adds the rows in order).
 enum { kUnion = 0, kAct = 1, kScore = 2 };
 
-template <int MODE>
+template <typename ET, int MODE>
 __global__ __launch_bounds__(256) void gemm1_tiled(
-    const bf16_t* __restrict__ x, int64_t B, int64_t d, const bf16_t* __restrict__ gu, int64_t L,
+    const uint16_t* __restrict__ x, int64_t B, int64_t d, const uint16_t* __restrict__ gu, int64_t L,
     const int32_t* __restrict__ ulist, const int* __restrict__ ucount,
-    const uint32_t* __restrict__ bits, int64_t W, bf16_t* __restrict__ Hhi,
-    bf16_t* __restrict__ Hlo, int64_t Up, int ntm, float* __restrict__ out) {
+    const uint32_t* __restrict__ bits, int64_t W, uint16_t* __restrict__ Hhi,
+    uint16_t* __restrict__ Hlo, int64_t Up, int ntm, float* __restrict__ out) {
     const int id = blockIdx.x;
     const int st = (id / (8 * ntm)) * 8 + (id % 8);
     const int tm = (id / 8) % ntm;
@@ -146,8 +134,8 @@ __global__ __launch_bounds__(256) void gemm1_tiled(
     const int nn = lane & 15;
     const int g = lane >> 4;
 
-    __shared__ __align__(16) bf16_t sA[kT1M][kKP];
-    __shared__ __align__(16) bf16_t sB[kT1N][kKP];
+    __shared__ __align__(16) uint16_t sA[kT1M][kKP];
+    __shared__ __align__(16) uint16_t sB[kT1N][kKP];
 
     // staging: thread t moves 16-byte chunk t % 8 of rows t / 8 + 32 j
     const int ch = t & 7;
@@ -200,21 +188,21 @@ __global__ __launch_bounds__(256) void gemm1_tiled(
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
-            bf16x8_t a[4];
+            typename Mfma<ET>::vec8 a[4];
 #pragma unroll
             for (int mi = 0; mi < 4; ++mi)
-                a[mi] = as_bf16x8(ld16(&sA[64 * w + 16 * mi + nn][32 * ks + 8 * g]));
+                a[mi] = Mfma<ET>::vec(ld16(&sA[64 * w + 16 * mi + nn][32 * ks + 8 * g]));
             // B fragments one ahead: the next one's LDS read is in flight during this one's
             // four MFMAs
-            bf16x8_t bq[2];
-            bq[0] = as_bf16x8(ld16(&sB[nn][32 * ks + 8 * g]));
+            typename Mfma<ET>::vec8 bq[2];
+            bq[0] = Mfma<ET>::vec(ld16(&sB[nn][32 * ks + 8 * g]));
 #pragma unroll
             for (int nj = 0; nj < 10; ++nj) {
                 if (nj + 1 < 10)
-                    bq[(nj + 1) & 1] = as_bf16x8(ld16(&sB[16 * (nj + 1) + nn][32 * ks + 8 * g]));
-                const bf16x8_t b = bq[nj & 1];
+                    bq[(nj + 1) & 1] = Mfma<ET>::vec(ld16(&sB[16 * (nj + 1) + nn][32 * ks + 8 * g]));
+                const typename Mfma<ET>::vec8 b = bq[nj & 1];
 #pragma unroll
-                for (int mi = 0; mi < 4; ++mi) acc[mi][nj] = mfma16x16x32(a[mi], b, acc[mi][nj]);
+                for (int mi = 0; mi < 4; ++mi) acc[mi][nj] = Mfma<ET>::mma(a[mi], b, acc[mi][nj]);
             }
         }
     }
@@ -260,9 +248,9 @@ __global__ __launch_bounds__(256) void gemm1_tiled(
                         const bool act = (bits[tok * W + slot / 32] >> (slot % 32)) & 1u;
                         const float h =
                             act ? silu_f32(acc[mi][2 * q][i]) * acc[mi][2 * q + 1][i] : 0.0f;
-                        const uint32_t hb = f32_to_bf16_rne(h);
-                        Hhi[tok * Up + u] = (bf16_t)hb;
-                        Hlo[tok * Up + u] = (bf16_t)f32_to_bf16_rne(h - bf16_to_f32(hb));
+                        const uint32_t hb = Mfma<ET>::rne(h);
+                        Hhi[tok * Up + u] = (uint16_t)hb;
+                        Hlo[tok * Up + u] = (uint16_t)Mfma<ET>::rne(h - Mfma<ET>::widen(hb));
                     }
                 }
             }
@@ -271,9 +259,10 @@ __global__ __launch_bounds__(256) void gemm1_tiled(
 
 // ---- GEMM2 ---------------------------------------------------------------------------------
 // Grid: (ceil(d / 128), ceil(B / 256), KS), 256 threads. Partials in the chunked layout.
+template <typename ET>
 __global__ __launch_bounds__(256) void gemm2_tiled(
-    const bf16_t* __restrict__ Hhi, const bf16_t* __restrict__ Hlo, int64_t Up, int64_t B,
-    const bf16_t* __restrict__ dc, int64_t d, int64_t L, const int32_t* __restrict__ ulist,
+    const uint16_t* __restrict__ Hhi, const uint16_t* __restrict__ Hlo, int64_t Up, int64_t B,
+    const uint16_t* __restrict__ dc, int64_t d, int64_t L, const int32_t* __restrict__ ulist,
     const int* __restrict__ ucount, float* __restrict__ part, int KS, int fast) {
     const int nU = *ucount;
     const int ks = blockIdx.z;
@@ -290,8 +279,8 @@ __global__ __launch_bounds__(256) void gemm2_tiled(
     const int nn = lane & 15;
     const int g = lane >> 4;
 
-    __shared__ __align__(16) bf16_t sH[2][kT2M][kKP];
-    __shared__ __align__(16) bf16_t sD[kBK][kT2P];
+    __shared__ __align__(16) uint16_t sH[2][kT2M][kKP];
+    __shared__ __align__(16) uint16_t sD[kBK][kT2P];
 
     // staging of H: chunk t % 8 of rows t / 8 + 32 j; of the down rows: 16-byte chunk t % 16
     // of union positions t / 16 + 16 j
@@ -378,7 +367,7 @@ __global__ __launch_bounds__(256) void gemm2_tiled(
             // 16-column subtile; ds_read_b64_tr_b16 hands lane i of a 16-lane group element
             // i % 4 of the 8-byte pieces addressed by lanes i / 4 + 4 j, so lane nn addresses
             // position 8 g + nn / 4 (and + 4), columns 4 (nn % 4) .. + 3 of the subtile.
-            bf16x8_t bop[4];
+            typename Mfma<ET>::vec8 bop[4];
 #pragma unroll
             for (int nj = 0; nj < 4; ++nj) {
                 const int col = 64 * wn + 16 * nj + 4 * (nn & 3);
@@ -391,26 +380,26 @@ __global__ __launch_bounds__(256) void gemm2_tiled(
                 const uint32_t p1 = (uint16_t)lo4[2] | ((uint32_t)(uint16_t)lo4[3] << 16);
                 const uint32_t p2 = (uint16_t)hi4[0] | ((uint32_t)(uint16_t)hi4[1] << 16);
                 const uint32_t p3 = (uint16_t)hi4[2] | ((uint32_t)(uint16_t)hi4[3] << 16);
-                bop[nj] = as_bf16x8(V16{{p0, p1, p2, p3}});
+                bop[nj] = Mfma<ET>::vec(V16{{p0, p1, p2, p3}});
             }
             // A fragments (hi, lo) one row-tile ahead of their MFMAs
-            bf16x8_t ah[2], al[2];
-            ah[0] = as_bf16x8(ld16(&sH[0][128 * wm + nn][32 * ks2 + 8 * g]));
-            al[0] = as_bf16x8(ld16(&sH[1][128 * wm + nn][32 * ks2 + 8 * g]));
+            typename Mfma<ET>::vec8 ah[2], al[2];
+            ah[0] = Mfma<ET>::vec(ld16(&sH[0][128 * wm + nn][32 * ks2 + 8 * g]));
+            al[0] = Mfma<ET>::vec(ld16(&sH[1][128 * wm + nn][32 * ks2 + 8 * g]));
 #pragma unroll
             for (int mi = 0; mi < 8; ++mi) {
                 if (mi + 1 < 8) {
                     const int row = 128 * wm + 16 * (mi + 1) + nn;
-                    ah[(mi + 1) & 1] = as_bf16x8(ld16(&sH[0][row][32 * ks2 + 8 * g]));
-                    al[(mi + 1) & 1] = as_bf16x8(ld16(&sH[1][row][32 * ks2 + 8 * g]));
+                    ah[(mi + 1) & 1] = Mfma<ET>::vec(ld16(&sH[0][row][32 * ks2 + 8 * g]));
+                    al[(mi + 1) & 1] = Mfma<ET>::vec(ld16(&sH[1][row][32 * ks2 + 8 * g]));
                 }
 #pragma unroll
                 for (int nj = 0; nj < 4; ++nj)
-                    acc[mi][nj] = mfma16x16x32(ah[mi & 1], bop[nj], acc[mi][nj]);
+                    acc[mi][nj] = Mfma<ET>::mma(ah[mi & 1], bop[nj], acc[mi][nj]);
                 if (!fast) {
 #pragma unroll
                     for (int nj = 0; nj < 4; ++nj)
-                        acc[mi][nj] = mfma16x16x32(al[mi & 1], bop[nj], acc[mi][nj]);
+                        acc[mi][nj] = Mfma<ET>::mma(al[mi & 1], bop[nj], acc[mi][nj]);
                 }
             }
         }
@@ -497,22 +486,23 @@ size_t tiled_workspace(int64_t B, int64_t L, int64_t d, int num_cu) {
     return make_tplan(B, L, d, num_cu).total;
 }
 
-hipError_t launch_union_tiled(const void* x, int64_t B, int64_t d, const int32_t* offsets,
-                              const int32_t* idx, int64_t nnz, const void* gate_up_c,
-                              const void* down_c, int64_t L, float* y, void* ws, int flags,
-                              int num_cu, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+template <typename ET>
+hipError_t launch_union_tiled_t(const void* x, int64_t B, int64_t d, const int32_t* offsets,
+                                const int32_t* idx, int64_t nnz, const void* gate_up_c,
+                                const void* down_c, int64_t L, float* y, void* ws, int flags,
+                                int num_cu, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
     const TPlan p = make_tplan(B, L, d, num_cu);
     uint8_t* base = static_cast<uint8_t*>(ws);
     uint32_t* bits = reinterpret_cast<uint32_t*>(base + p.off_bits);
     uint32_t* words = reinterpret_cast<uint32_t*>(base + p.off_words);
     int32_t* ulist = reinterpret_cast<int32_t*>(base + p.off_ulist);
     int* ucount = reinterpret_cast<int*>(base + p.off_count);
-    bf16_t* hhi = reinterpret_cast<bf16_t*>(base + p.off_hhi);
-    bf16_t* hlo = reinterpret_cast<bf16_t*>(base + p.off_hlo);
+    uint16_t* hhi = reinterpret_cast<uint16_t*>(base + p.off_hhi);
+    uint16_t* hlo = reinterpret_cast<uint16_t*>(base + p.off_hlo);
     float* part = reinterpret_cast<float*>(base + p.off_part);
-    const bf16_t* xx = static_cast<const bf16_t*>(x);
-    const bf16_t* gu = static_cast<const bf16_t*>(gate_up_c);
-    const bf16_t* dc = static_cast<const bf16_t*>(down_c);
+    const uint16_t* xx = static_cast<const uint16_t*>(x);
+    const uint16_t* gu = static_cast<const uint16_t*>(gate_up_c);
+    const uint16_t* dc = static_cast<const uint16_t*>(down_c);
 
     hipError_t e = launch_token_bitmaps(offsets, idx, nnz, B, L, p.W, bits, s);
     if (e != hipSuccess) return e;
@@ -522,11 +512,11 @@ hipError_t launch_union_tiled(const void* x, int64_t B, int64_t d, const int32_t
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int nst8 = (p.nst + 7) / 8 * 8;
-    hipExtLaunchKernelGGL(gemm1_tiled<kUnion>, dim3((unsigned)(nst8 * p.ntm1)), dim3(256), 0, s,
+    hipExtLaunchKernelGGL((gemm1_tiled<ET, kUnion>), dim3((unsigned)(nst8 * p.ntm1)), dim3(256), 0, s,
                           ev0, nullptr, 0, xx, B, d, gu, L, ulist, ucount, bits, p.W, hhi, hlo,
                           p.Up, p.ntm1, nullptr);
     const int fast = (flags & 4) ? 1 : 0;
-    hipExtLaunchKernelGGL(gemm2_tiled, dim3((unsigned)p.ntn2, (unsigned)p.ntm2, (unsigned)p.KS),
+    hipExtLaunchKernelGGL((gemm2_tiled<ET>), dim3((unsigned)p.ntn2, (unsigned)p.ntm2, (unsigned)p.KS),
                           dim3(256), 0, s, nullptr, ev1, 0, hhi, hlo, p.Up, B, dc, d, L, ulist,
                           ucount, part, p.KS, fast);
     e = hipGetLastError();
@@ -534,24 +524,46 @@ hipError_t launch_union_tiled(const void* x, int64_t B, int64_t d, const int32_t
     return launch_reduce_partials(part, p.KS, B, d, y, s);
 }
 
-hipError_t launch_activations_mfma(const void* x, int64_t T, int64_t d, const void* gate_up_c,
-                                   int64_t L, float* out, int64_t ldo, int score, hipStream_t s,
-                                   hipEvent_t ev0, hipEvent_t ev1) {
+template <typename ET>
+hipError_t launch_activations_mfma_t(const void* x, int64_t T, int64_t d, const void* gate_up_c,
+                                     int64_t L, float* out, int64_t ldo, int score, hipStream_t s,
+                                     hipEvent_t ev0, hipEvent_t ev1) {
     if (T == 0 || L == 0) return hipSuccess;
     const int ntm = (int)((T + kT1M - 1) / kT1M);
     const int nst = (int)((L + kT1S - 1) / kT1S);
     const int nst8 = (nst + 7) / 8 * 8;
-    const bf16_t* xx = static_cast<const bf16_t*>(x);
-    const bf16_t* gu = static_cast<const bf16_t*>(gate_up_c);
+    const uint16_t* xx = static_cast<const uint16_t*>(x);
+    const uint16_t* gu = static_cast<const uint16_t*>(gate_up_c);
     if (score)
-        hipExtLaunchKernelGGL(gemm1_tiled<kScore>, dim3((unsigned)(nst8 * ntm)), dim3(256), 0, s,
+        hipExtLaunchKernelGGL((gemm1_tiled<ET, kScore>), dim3((unsigned)(nst8 * ntm)), dim3(256), 0, s,
                               ev0, ev1, 0, xx, T, d, gu, L, nullptr, nullptr, nullptr, (int64_t)0,
                               nullptr, nullptr, ldo, ntm, out);
     else
-        hipExtLaunchKernelGGL(gemm1_tiled<kAct>, dim3((unsigned)(nst8 * ntm)), dim3(256), 0, s,
+        hipExtLaunchKernelGGL((gemm1_tiled<ET, kAct>), dim3((unsigned)(nst8 * ntm)), dim3(256), 0, s,
                               ev0, ev1, 0, xx, T, d, gu, L, nullptr, nullptr, nullptr, (int64_t)0,
                               nullptr, nullptr, ldo, ntm, out);
     return hipGetLastError();
+}
+
+hipError_t launch_union_tiled(const void* x, int64_t B, int64_t d, const int32_t* offsets,
+                              const int32_t* idx, int64_t nnz, const void* gate_up_c,
+                              const void* down_c, int64_t L, int et, float* y, void* ws,
+                              int flags, int num_cu, hipStream_t s, hipEvent_t ev0,
+                              hipEvent_t ev1) {
+    if (et == 2)
+        return launch_union_tiled_t<f16_t>(x, B, d, offsets, idx, nnz, gate_up_c, down_c, L, y,
+                                           ws, flags, num_cu, s, ev0, ev1);
+    return launch_union_tiled_t<bf16_t>(x, B, d, offsets, idx, nnz, gate_up_c, down_c, L, y, ws,
+                                        flags, num_cu, s, ev0, ev1);
+}
+
+hipError_t launch_activations_mfma(const void* x, int64_t T, int64_t d, const void* gate_up_c,
+                                   int64_t L, int et, float* out, int64_t ldo, int score,
+                                   hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+    if (et == 2)
+        return launch_activations_mfma_t<f16_t>(x, T, d, gate_up_c, L, out, ldo, score, s, ev0,
+                                                ev1);
+    return launch_activations_mfma_t<bf16_t>(x, T, d, gate_up_c, L, out, ldo, score, s, ev0, ev1);
 }
 
 }  // namespace si

@@ -32,25 +32,13 @@
 
 #include "common.h"
 #include "launch.h"
+#include "mfma.h"
 
 namespace si {
 
-typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
-typedef __attribute__((ext_vector_type(4))) float f32x4_t;
-typedef __attribute__((ext_vector_type(4))) unsigned int u32x4_t;
 typedef __attribute__((ext_vector_type(4))) short s16x4_t;
 
 namespace {
-
-__device__ __forceinline__ bf16x8_t as_bf16x8(const V16& v) {
-    const u32x4_t t = {v.w[0], v.w[1], v.w[2], v.w[3]};
-    return __builtin_bit_cast(bf16x8_t, t);
-}
-
-__device__ __forceinline__ f32x4_t mfma16x16x32(const bf16x8_t& a, const bf16x8_t& b,
-                                                const f32x4_t& c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-}
 
 constexpr int kG2Cols = 256;               // GEMM2 columns per work-group
 constexpr int kG2Pitch = kG2Cols + 16;     // LDS row pitch (bf16): rows 32 bytes apart in bank
@@ -139,9 +127,9 @@ __global__ __launch_bounds__(256) void token_bitmaps(const int32_t* __restrict__
 }
 
 // GEMM1 + SiLU*up*mask epilogue (see the file comment). Grid: (W, ceil(B/(16*MT1))).
-template <int MT1>
+template <typename ET, int MT1>
 __global__ __launch_bounds__(64 * kGemm1Waves) void union_gemm1(
-    const bf16_t* __restrict__ x, int64_t B, int64_t d, const bf16_t* __restrict__ gu,
+    const uint16_t* __restrict__ x, int64_t B, int64_t d, const uint16_t* __restrict__ gu,
     int64_t L, const uint32_t* __restrict__ bits, int64_t W, uint32_t* __restrict__ words,
     float* __restrict__ H, int64_t Lp) {
     constexpr int MTOK = 16 * MT1;
@@ -228,12 +216,12 @@ __global__ __launch_bounds__(64 * kGemm1Waves) void union_gemm1(
             }
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                const bf16x8_t a = as_bf16x8(xv[e]);
+                const typename Mfma<ET>::vec8 a = Mfma<ET>::vec(xv[e]);
 #pragma unroll
                 for (int st = 0; st < 2; ++st) {
                     if (st < ntile) {
-                        accg[mt][st] = mfma16x16x32(a, as_bf16x8(gv[st][e]), accg[mt][st]);
-                        accu[mt][st] = mfma16x16x32(a, as_bf16x8(uv[st][e]), accu[mt][st]);
+                        accg[mt][st] = Mfma<ET>::mma(a, Mfma<ET>::vec(gv[st][e]), accg[mt][st]);
+                        accu[mt][st] = Mfma<ET>::mma(a, Mfma<ET>::vec(uv[st][e]), accu[mt][st]);
                     }
                 }
             }
@@ -275,9 +263,9 @@ __global__ __launch_bounds__(64 * kGemm1Waves) void union_gemm1(
 }
 
 // GEMM2 (see the file comment). Grid: (ceil(d/256), ceil(B/(16*MT)), KS); 4 waves.
-template <int MT>
+template <typename ET, int MT>
 __global__ __launch_bounds__(256) void union_gemm2(const float* __restrict__ H, int64_t Lp,
-                                                   int64_t B, const bf16_t* __restrict__ dc,
+                                                   int64_t B, const uint16_t* __restrict__ dc,
                                                    int64_t d, int64_t L,
                                                    const uint32_t* __restrict__ words, int64_t W,
                                                    float* __restrict__ part, int KS, int fast) {
@@ -321,7 +309,7 @@ __global__ __launch_bounds__(256) void union_gemm2(const float* __restrict__ H, 
         // ds_read_b64_tr_b16 hands lane i of a 16-lane group element i%4 of the 8-byte pieces
         // addressed by lanes i/4 + 4j, so lane nn addresses row 8g + nn/4 (+4), columns
         // 4*(nn%4) .. +3 of the subtile.
-        bf16x8_t bop[4];
+        typename Mfma<ET>::vec8 bop[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int col = w * 64 + j * 16 + 4 * (nn & 3);
@@ -334,7 +322,7 @@ __global__ __launch_bounds__(256) void union_gemm2(const float* __restrict__ H, 
             const uint32_t p1 = (uint16_t)lo4[2] | ((uint32_t)(uint16_t)lo4[3] << 16);
             const uint32_t p2 = (uint16_t)hi4[0] | ((uint32_t)(uint16_t)hi4[1] << 16);
             const uint32_t p3 = (uint16_t)hi4[2] | ((uint32_t)(uint16_t)hi4[3] << 16);
-            bop[j] = as_bf16x8(V16{{p0, p1, p2, p3}});
+            bop[j] = Mfma<ET>::vec(V16{{p0, p1, p2, p3}});
         }
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
@@ -360,19 +348,19 @@ __global__ __launch_bounds__(256) void union_gemm2(const float* __restrict__ H, 
             uint32_t hi[4], lo[4];
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-                const uint32_t h0 = f32_to_bf16_rne(hv[2 * q]);
-                const uint32_t h1 = f32_to_bf16_rne(hv[2 * q + 1]);
+                const uint32_t h0 = Mfma<ET>::rne(hv[2 * q]);
+                const uint32_t h1 = Mfma<ET>::rne(hv[2 * q + 1]);
                 hi[q] = h0 | (h1 << 16);
-                const uint32_t l0 = f32_to_bf16_rne(hv[2 * q] - bf16_to_f32(h0));
-                const uint32_t l1 = f32_to_bf16_rne(hv[2 * q + 1] - bf16_to_f32(h1));
+                const uint32_t l0 = Mfma<ET>::rne(hv[2 * q] - Mfma<ET>::widen(h0));
+                const uint32_t l1 = Mfma<ET>::rne(hv[2 * q + 1] - Mfma<ET>::widen(h1));
                 lo[q] = l0 | (l1 << 16);
             }
-            const bf16x8_t ahi = as_bf16x8(V16{{hi[0], hi[1], hi[2], hi[3]}});
-            const bf16x8_t alo = as_bf16x8(V16{{lo[0], lo[1], lo[2], lo[3]}});
+            const typename Mfma<ET>::vec8 ahi = Mfma<ET>::vec(V16{{hi[0], hi[1], hi[2], hi[3]}});
+            const typename Mfma<ET>::vec8 alo = Mfma<ET>::vec(V16{{lo[0], lo[1], lo[2], lo[3]}});
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                acc[mt][j] = mfma16x16x32(ahi, bop[j], acc[mt][j]);
-                if (!fast) acc[mt][j] = mfma16x16x32(alo, bop[j], acc[mt][j]);
+                acc[mt][j] = Mfma<ET>::mma(ahi, bop[j], acc[mt][j]);
+                if (!fast) acc[mt][j] = Mfma<ET>::mma(alo, bop[j], acc[mt][j]);
             }
         }
     };
@@ -436,29 +424,29 @@ size_t union_workspace(int64_t B, int64_t L, int64_t d, int num_cu) {
     return make_plan(B, L, d, num_cu).total;
 }
 
-hipError_t launch_union(const void* x, int64_t B, int64_t d, const int32_t* offsets,
-                        const int32_t* idx, int64_t nnz, const void* gate_up_c,
-                        const void* down_c, int64_t L, float* y, void* ws, int flags,
-                        int num_cu, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
-    if (use_tiled(B, L, d))
-        return launch_union_tiled(x, B, d, offsets, idx, nnz, gate_up_c, down_c, L, y, ws, flags,
-                                  num_cu, s, ev0, ev1);
+namespace {
+
+template <typename ET>
+hipError_t launch_union_t(const void* x, int64_t B, int64_t d, const int32_t* offsets,
+                          const int32_t* idx, int64_t nnz, const void* gate_up_c,
+                          const void* down_c, int64_t L, float* y, void* ws, int flags,
+                          int num_cu, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
     const Plan p = make_plan(B, L, d, num_cu);
     uint8_t* base = static_cast<uint8_t*>(ws);
     uint32_t* bits = reinterpret_cast<uint32_t*>(base + p.off_bits);
     uint32_t* words = reinterpret_cast<uint32_t*>(base + p.off_words);
     float* H = reinterpret_cast<float*>(base + p.off_h);
     float* part = reinterpret_cast<float*>(base + p.off_part);
-    const bf16_t* xx = static_cast<const bf16_t*>(x);
-    const bf16_t* gu = static_cast<const bf16_t*>(gate_up_c);
-    const bf16_t* dc = static_cast<const bf16_t*>(down_c);
+    const uint16_t* xx = static_cast<const uint16_t*>(x);
+    const uint16_t* gu = static_cast<const uint16_t*>(gate_up_c);
+    const uint16_t* dc = static_cast<const uint16_t*>(down_c);
 
     hipError_t e = launch_token_bitmaps(offsets, idx, nnz, B, L, p.W, bits, s);
     if (e != hipSuccess) return e;
     const dim3 g1((unsigned)p.W, (unsigned)((B + 16 * p.MT1 - 1) / (16 * p.MT1)));
-#define SI_G1(M)                                                                                \
-    hipExtLaunchKernelGGL(union_gemm1<M>, g1, dim3(64 * kGemm1Waves), 0, s, ev0, nullptr, 0, xx, \
-                          B, d, gu, L, bits, p.W, words, H, p.Lp)
+#define SI_G1(M)                                                                               \
+    hipExtLaunchKernelGGL((union_gemm1<ET, M>), g1, dim3(64 * kGemm1Waves), 0, s, ev0, nullptr, \
+                          0, xx, B, d, gu, L, bits, p.W, words, H, p.Lp)
     switch (p.MT1) {
         case 4: SI_G1(4); break;
         case 2: SI_G1(2); break;
@@ -468,9 +456,9 @@ hipError_t launch_union(const void* x, int64_t B, int64_t d, const int32_t* offs
     const int fast = (flags & 4) ? 1 : 0;
     dim3 g2((unsigned)((d + kG2Cols - 1) / kG2Cols),
             (unsigned)((B + 16 * p.MT - 1) / (16 * p.MT)), (unsigned)p.KS);
-#define SI_G2(MTV)                                                                             \
-    hipExtLaunchKernelGGL(union_gemm2<MTV>, g2, dim3(256), 0, s, nullptr, ev1, 0, H, p.Lp, B, dc, \
-                          d, L, words, p.W, part, p.KS, fast)
+#define SI_G2(MTV)                                                                              \
+    hipExtLaunchKernelGGL((union_gemm2<ET, MTV>), g2, dim3(256), 0, s, nullptr, ev1, 0, H, p.Lp, \
+                          B, dc, d, L, words, p.W, part, p.KS, fast)
     switch (p.MT) {
         case 8: SI_G2(8); break;
         case 4: SI_G2(4); break;
@@ -481,6 +469,22 @@ hipError_t launch_union(const void* x, int64_t B, int64_t d, const int32_t* offs
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     return launch_reduce_partials(part, p.KS, B, d, y, s);
+}
+
+}  // namespace
+
+hipError_t launch_union(const void* x, int64_t B, int64_t d, const int32_t* offsets,
+                        const int32_t* idx, int64_t nnz, const void* gate_up_c,
+                        const void* down_c, int64_t L, int et, float* y, void* ws, int flags,
+                        int num_cu, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+    if (use_tiled(B, L, d))
+        return launch_union_tiled(x, B, d, offsets, idx, nnz, gate_up_c, down_c, L, et, y, ws,
+                                  flags, num_cu, s, ev0, ev1);
+    if (et == 2)
+        return launch_union_t<f16_t>(x, B, d, offsets, idx, nnz, gate_up_c, down_c, L, y, ws,
+                                     flags, num_cu, s, ev0, ev1);
+    return launch_union_t<bf16_t>(x, B, d, offsets, idx, nnz, gate_up_c, down_c, L, y, ws, flags,
+                                  num_cu, s, ev0, ev1);
 }
 
 }  // namespace si

@@ -26,9 +26,10 @@ hipError_t launch_decode(const void* x, int xdt, int64_t B, int64_t d, const int
 // sizes the union kernels handle (their buffer loads take 32-bit byte offsets)
 bool union_supported(int64_t B, int64_t L, int64_t d);
 size_t union_workspace(int64_t B, int64_t L, int64_t d, int num_cu);
+// et: the 16-bit element type of x and the weights (1 = bf16, 2 = IEEE half)
 hipError_t launch_union(const void* x, int64_t B, int64_t d, const int32_t* offsets,
                         const int32_t* idx, int64_t nnz, const void* gate_up_c,
-                        const void* down_c, int64_t L, float* y, void* ws, int flags,
+                        const void* down_c, int64_t L, int et, float* y, void* ws, int flags,
                         int num_cu, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 
 // one bitmap of L bits per token (W = ceil(L / 32) words): bit s of token b is set iff slot s
@@ -41,14 +42,16 @@ bool tiled_supported(int64_t B, int64_t L, int64_t d);
 size_t tiled_workspace(int64_t B, int64_t L, int64_t d, int num_cu);
 hipError_t launch_union_tiled(const void* x, int64_t B, int64_t d, const int32_t* offsets,
                               const int32_t* idx, int64_t nnz, const void* gate_up_c,
-                              const void* down_c, int64_t L, float* y, void* ws, int flags,
-                              int num_cu, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
+                              const void* down_c, int64_t L, int et, float* y, void* ws,
+                              int flags, int num_cu, hipStream_t s, hipEvent_t ev0,
+                              hipEvent_t ev1);
 
 // all-slots modes of the tiled GEMM1 (bf16): activations out[t * ldo + j] (score = 0) or one
 // Eq. 1 partial row per 256-token tile, out[tile * ldo + j] (score = 1)
 hipError_t launch_activations_mfma(const void* x, int64_t T, int64_t d, const void* gate_up_c,
-                                   int64_t L, float* out, int64_t ldo, int score, hipStream_t s,
-                                   hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+                                   int64_t L, int et, float* out, int64_t ldo, int score,
+                                   hipStream_t s, hipEvent_t ev0 = nullptr,
+                                   hipEvent_t ev1 = nullptr);
 int activation_tiles(int64_t T);
 // ascending list of the set bits of bits[0..W) and their number
 hipError_t launch_bits_to_list(const uint32_t* bits, int64_t W, int32_t* list, int* count,

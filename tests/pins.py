@@ -427,6 +427,27 @@ def pin_loaded_set(impl):
     assert impl.selective_layers(8) == [5]
 
 
+def pin_decode(impl):
+    # storage formats widen exactly: bf16 bits, IEEE half (closed-form values), float32
+    # 0x7F7F: exponent 254 - 127, mantissa 1 + 127/128 -> 255 * 2^120
+    assert impl.decode(np.array([0x3F80, 0xBF40, 0x7F7F], np.uint16)).tolist() == \
+        [1.0, -0.75, 255.0 * 2.0 ** 120]
+    h = impl.decode(np.array([1 / 3, 65504.0, 2.0 ** -24, -2.5], np.float16))
+    assert h.tolist() == [0.333251953125, 65504.0, 5.960464477539063e-08, -2.5]
+    assert impl.decode(np.array([0.1], np.float32)).tolist() == [float(np.float32(0.1))]
+    # a half-precision layer computes like its float64 widening (compaction copies bits)
+    wg, wu, wd, x = _problem(21, 9, 8, "f32")
+    c16 = impl.compact(wg.astype(np.float16), wu.astype(np.float16), wd.astype(np.float16),
+                       range(9))
+    assert c16["gate_up_c"].dtype == np.float16
+    y = impl.selective_ffn(x.astype(np.float16), [0, 3, 8], c16["gate_up_c"], c16["down_c"])
+    mask = np.isin(np.arange(9), [0, 3, 8]).astype(float)
+    ref = _masked_dense(x.astype(np.float16).astype(np.float32), wg.astype(np.float16).astype(
+        np.float32), wu.astype(np.float16).astype(np.float32),
+        wd.astype(np.float16).astype(np.float32), mask)
+    assert _rel(y, ref) <= 1e-13
+
+
 ALL_PINS = [pin_silu, pin_topk, pin_compact, pin_remap, pin_ffn_invariants, pin_hand_integer,
             pin_rmsnorm, pin_memory, pin_activations, pin_dynamic_set, pin_profile_scores,
-            pin_loaded_set]
+            pin_loaded_set, pin_decode]

@@ -84,6 +84,8 @@ def _rand_problem(seed, N, d, L, wdtype):
     rng = np.random.default_rng(seed)
     def draw(*shape, scale=0.02):
         a = (rng.standard_normal(shape) * scale).astype(np.float32)
+        if wdtype == "f16":
+            return a.astype(np.float16)
         return (a.view(np.uint32) >> 16).astype(np.uint16) if wdtype == "bf16" else a
     wg, wu, wd = draw(N, d), draw(N, d), draw(d, N)
     loaded = rng.permutation(N)[:L].astype(np.int32)
@@ -163,6 +165,31 @@ def test_union_tiled_ragged(B, d, L, sparse):
     assert errf <= TOL["bf16"]
     again = _run(x, sets, gpu)
     assert np.array_equal(got, again)   # fixed-order reductions: bitwise reproducible
+
+
+@pytest.mark.parametrize("B,d,xdt", [(1, 264, "f16"), (1, 4104, "f16"), (3, 1000, "f32"),
+                                      (17, 264, "f16"), (70, 1000, "f16"), (130, 264, "f16")])
+def test_fp16_weights(B, d, xdt):
+    """IEEE-half weights (the paper's storage precision): per-token path with half or float32
+    x, union paths (row-word below 128 tokens, tiled from 128) with half x."""
+    N, L = 900, 613
+    say(f"fp16 weights B={B} d={d} x={xdt}")
+    rng, draw, ref, gpu = _rand_problem(B * 31 + d, N, d, L, "f16")
+    sets = [rng.permutation(L)[:int(rng.integers(0, L + 1)) if b % 5 else 40].astype(np.int32)
+            for b in range(B)]
+    x = draw(B, d, scale=1.0)
+    if xdt == "f32":
+        x = x.astype(np.float32)
+    want = _oracle(x, sets, ref)
+    got = _run(x, sets, gpu)
+    err = max_rel_l2(got, want)
+    say(f"  rel L2 {err:.2e}")
+    assert err <= ALARM_PER_TOKEN       # float32 sums; union: h as a half hi + lo pair
+    if B > 1 and xdt == "f16":
+        fast = _run(x, sets, gpu, flags=si.FLAG_FAST_H)
+        assert max_rel_l2(fast, want) <= TOL["bf16"]
+        per = _run(x, sets, gpu, flags=si.FLAG_PER_TOKEN)
+        assert max_rel_l2(per, want) <= ALARM_PER_TOKEN
 
 
 def test_llama2_7b_batch16_union():

@@ -23,12 +23,14 @@ def _same(layer, ref):
 
 
 @pytest.mark.parametrize("wdtype,N,d,L", [("bf16", 900, 264, 613), ("f32", 300, 100, 1),
-                                          ("f32", 257, 12, 257)])
+                                          ("f32", 257, 12, 257), ("f16", 500, 72, 333)])
 def test_load_selected_ragged(wdtype, N, d, L):
     say(f"load_selected {wdtype} N={N} d={d} L={L}")
     rng = np.random.default_rng(N + d)
     def draw(*s):
         a = rng.standard_normal(s).astype(np.float32)
+        if wdtype == "f16":
+            return a.astype(np.float16)
         return (a.view(np.uint32) >> 16).astype(np.uint16) if wdtype == "bf16" else a
     wg, wu, wd = draw(N, d), draw(N, d), draw(d, N)
     loaded = rng.permutation(N)[:L].astype(np.int32)

@@ -37,6 +37,8 @@ def _int_problem(seed, N, d, L, T, wdtype):
     x = rng.integers(-4, 5, (T, d)).astype(np.float32)
     if wdtype == "bf16":
         wg, wu, wd, x = _bf16(wg), _bf16(wu), _bf16(wd), _bf16(x)
+    elif wdtype == "f16":
+        wg, wu, wd, x = (a.astype(np.float16) for a in (wg, wu, wd, x))
     loaded = rng.permutation(N)[:L].astype(np.int32)
     ref = oracle.compact(wg, wu, wd, loaded)
     gpu = si.compact_ffn(dev_tensor(wg), dev_tensor(wu), dev_tensor(wd), torch.from_numpy(loaded))
@@ -56,7 +58,7 @@ def _margins_ok(A32, alpha):
     return True
 
 
-@pytest.mark.parametrize("wdtype,T", [("bf16", 37), ("bf16", 300), ("f32", 23)])
+@pytest.mark.parametrize("wdtype,T", [("bf16", 37), ("bf16", 300), ("f32", 23), ("f16", 300)])
 def test_dynamic_set_exact(wdtype, T):
     N, d, L = 700, 64, 530
     say(f"dynamic set exact {wdtype} T={T}")
@@ -112,7 +114,8 @@ def test_dynamic_set_realistic_shape():
     assert (diff > 0).sum() <= L // 100 and diff.max() <= 2
 
 
-@pytest.mark.parametrize("wdtype,T,d", [("bf16", 300, 256), ("bf16", 40, 264), ("f32", 50, 96)])
+@pytest.mark.parametrize("wdtype,T,d", [("bf16", 300, 256), ("bf16", 40, 264), ("f32", 50, 96),
+                                        ("f16", 300, 256)])
 def test_profile_scores(wdtype, T, d):
     N = 700
     say(f"profile scores {wdtype} T={T} d={d}")
@@ -121,6 +124,8 @@ def test_profile_scores(wdtype, T, d):
     wg, wu, wd, x = a(N, d), a(N, d), a(d, N), (rng.standard_normal((T, d))).astype(np.float32)
     if wdtype == "bf16":
         wg, wu, wd, x = _bf16(wg), _bf16(wu), _bf16(wd), _bf16(x)
+    elif wdtype == "f16":
+        wg, wu, wd, x = (a.astype(np.float16) for a in (wg, wu, wd, x))
     full = si.compact_ffn(dev_tensor(wg), dev_tensor(wu), dev_tensor(wd),
                           torch.arange(N, dtype=torch.int32))
     ref = oracle.compact(wg, wu, wd, np.arange(N))
