@@ -236,19 +236,28 @@ __global__ __launch_bounds__(kThreads) void sffn_rows(
     // system returns the gate/up rows first, so the dot products and the cross-wave exchange
     // finish while the down rows are still streaming in. Ids are wave-uniform, so the row
     // bases stay in scalar registers.
+    // Rows past the batch's end (or with an invalid id) issue no load at all: a uniform
+    // branch per row. Out-of-range loads would read no memory but still take issue slots in
+    // the load pipeline, which is the bottleneck while the batch is being issued.
+    // okr[r]: row r of the current batch exists and has a valid slot id (wave-uniform); the
+    // dot products and the down-row FMAs use only such rows, so an invalid id adds nothing
     V16 gv[R][NI], uv[R][NI], dv[R][NI];
+    bool okr[R];
     auto issue = [&](const int32_t (&sl)[R]) {
-        bool okr[R];
 #pragma unroll
         for (int r = 0; r < R; ++r) okr[r] = (sl[r] >= 0) && (sl[r] < L);
 #pragma unroll
         for (int r = 0; r < R; ++r)
+            if (okr[r]) {
 #pragma unroll
-            for (int i = 0; i < NI; ++i) ldr.load_gu(okr[r], sl[r], i, gv[r][i], uv[r][i]);
+                for (int i = 0; i < NI; ++i) ldr.load_gu(true, sl[r], i, gv[r][i], uv[r][i]);
+            }
 #pragma unroll
         for (int r = 0; r < R; ++r)
+            if (okr[r]) {
 #pragma unroll
-            for (int i = 0; i < NI; ++i) ldr.load_dn(okr[r], sl[r], i, dv[r][i]);
+                for (int i = 0; i < NI; ++i) ldr.load_dn(true, sl[r], i, dv[r][i]);
+            }
     };
 
     // x first: vector loads complete in issue order, so the dot products of the first rows
@@ -290,10 +299,12 @@ __global__ __launch_bounds__(kThreads) void sffn_rows(
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             float g = 0.0f, u = 0.0f;
+            if (okr[r]) {  // uniform; other rows were not loaded and add nothing
 #pragma unroll
-            for (int i = 0; i < NI; ++i) {
-                g = xs[i].dot(gv[r][i], g);
-                u = xs[i].dot(uv[r][i], u);
+                for (int i = 0; i < NI; ++i) {
+                    g = xs[i].dot(gv[r][i], g);
+                    u = xs[i].dot(uv[r][i], u);
+                }
             }
             vals[r] = g;
             vals[R + r] = u;
@@ -312,7 +323,7 @@ __global__ __launch_bounds__(kThreads) void sffn_rows(
         const float hv = silu_f32(t) * uu;  // valid in lanes 0 .. R-1
 #pragma unroll
         for (int r = 0; r < R; ++r) {
-            if (r < nr) {
+            if (okr[r]) {
                 const float h = __builtin_bit_cast(
                     float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, hv), r));
 #pragma unroll

@@ -290,11 +290,31 @@ __global__ __launch_bounds__(256) void union_gemm2(const float* __restrict__ H, 
     const __amdgpu_buffer_rsrc_t rd = make_rsrc(dc, L * d * 2);
     const int sr = threadIdx.x >> 3;         // staging: tile row (slot 32 wd + sr)
     const int sc = (threadIdx.x & 7) * 32;   // staging: first of 32 columns
-    // three words' down rows in flight in registers ahead of the LDS tile being consumed
-    constexpr int kDepth = 3;
+    // kDepth words' down rows in flight in registers ahead of the LDS tile being consumed
+    // words of down rows in flight in registers: deeper for few tokens, where the kernel only
+    // streams rows and register room is plentiful
+    constexpr int kDepth = MT == 1 ? 8 : (MT == 2 ? 6 : 3);
     V16 nxt[kDepth][4];
-    auto fetch = [&](int64_t wd, V16 (&v)[4]) {
-        const uint32_t u = wd < w1 ? words[wd] : 0u;
+    // The union word, the lane's chunk of the word's down rows and the lane's H values (the A
+    // operand of its MT token tiles) all travel kDepth words ahead: consuming a word then waits
+    // for no memory access.
+    // The union words themselves run a further kDepth words ahead, as vector loads through a
+    // descriptor over this chunk (0 past its end): a row fetch never waits for its word, and
+    // vector loads complete in order, so no scalar-load wait serialises the pipeline.
+    float nh[kDepth][MT][8];
+    uint32_t nw[kDepth], wv[kDepth];
+    const __amdgpu_buffer_rsrc_t rh = make_rsrc(H, B * Lp * 4);
+    const __amdgpu_buffer_rsrc_t rw = make_rsrc(words + w0, (w1 - w0) * 4);
+    auto load_word = [&](int64_t wd) {
+        return (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(rw, (int)((wd - w0) * 4), 0, 0);
+    };
+#pragma unroll
+    for (int q = 0; q < kDepth; ++q) wv[q] = load_word(w0 + q);
+    auto fetch = [&](int64_t wd, V16 (&v)[4], float (&hv)[MT][8], uint32_t& word,
+                     uint32_t& wnext) {
+        const uint32_t u = wnext;  // words[wd], loaded kDepth words ago (0 past the chunk)
+        wnext = load_word(wd + kDepth);
+        word = u;
         const bool rok = (u >> sr) & 1u;
         const int64_t slot = wd * 32 + sr;
 #pragma unroll
@@ -302,9 +322,22 @@ __global__ __launch_bounds__(256) void union_gemm2(const float* __restrict__ H, 
             const int64_t col = c0 + sc + e * 8;
             v[e] = bload16(rd, (rok && col < d) ? (int)((slot * d + col) * 2) : kOOB);
         }
+        // H of token tok at slots 32 wd + 8 g .. +7 (contiguous, 32-byte aligned)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            const int64_t tok = m0 + mt * 16 + nn;
+            const int off = (tok < B && u != 0u) ? (int)((tok * Lp + wd * 32 + g * 8) * 4) : kOOB;
+            const V16 lo = bload16(rh, off);
+            const V16 hi = bload16(rh, off == kOOB ? kOOB : off + 16);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                hv[mt][e] = __uint_as_float(lo.w[e]);
+                hv[mt][4 + e] = __uint_as_float(hi.w[e]);
+            }
+        }
     };
-    // consume the LDS tile `bsel` holding slots 32 wd .. 32 wd + 31
-    auto consume = [&](int64_t wd, int bsel) {
+    // consume the LDS tile `bsel` holding slots 32 wd .. 32 wd + 31, with the word's H values
+    auto consume = [&](int bsel, const float (&hvs)[MT][8]) {
         // B operand: lane (nn, g) needs rows 8g..8g+7 of column nn of each 16-column subtile;
         // ds_read_b64_tr_b16 hands lane i of a 16-lane group element i%4 of the 8-byte pieces
         // addressed by lanes i/4 + 4j, so lane nn addresses row 8g + nn/4 (+4), columns
@@ -326,25 +359,7 @@ __global__ __launch_bounds__(256) void union_gemm2(const float* __restrict__ H, 
         }
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
-            const int64_t tok = m0 + mt * 16 + nn;
-            // A operand: H of token tok at slots 32 wd + 8 g .. +7 (contiguous, 32-byte aligned)
-            float hv[8];
-            if (tok < B) {
-                const float* hrow = H + tok * Lp + wd * 32 + g * 8;
-                const float4 a = *reinterpret_cast<const float4*>(hrow);
-                const float4 b = *reinterpret_cast<const float4*>(hrow + 4);
-                hv[0] = a.x;
-                hv[1] = a.y;
-                hv[2] = a.z;
-                hv[3] = a.w;
-                hv[4] = b.x;
-                hv[5] = b.y;
-                hv[6] = b.z;
-                hv[7] = b.w;
-            } else {
-#pragma unroll
-                for (int e = 0; e < 8; ++e) hv[e] = 0.0f;
-            }
+            const float* hv = hvs[mt];
             uint32_t hi[4], lo[4];
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
@@ -365,7 +380,7 @@ __global__ __launch_bounds__(256) void union_gemm2(const float* __restrict__ H, 
         }
     };
 #pragma unroll
-    for (int q = 0; q < kDepth; ++q) fetch(w0 + q, nxt[q]);
+    for (int q = 0; q < kDepth; ++q) fetch(w0 + q, nxt[q], nh[q], nw[q], wv[q]);
     int buf = 0;
     for (int64_t wg = w0; wg < w1; wg += kDepth) {
 #pragma unroll
@@ -374,9 +389,15 @@ __global__ __launch_bounds__(256) void union_gemm2(const float* __restrict__ H, 
             if (wd >= w1) break;                      // uniform over the work-group
 #pragma unroll
             for (int e = 0; e < 4; ++e) st16(&tile[buf][sr][sc + e * 8], nxt[q][e]);
+            const uint32_t word = nw[q];
+            float hcur[MT][8];
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int e = 0; e < 8; ++e) hcur[mt][e] = nh[q][mt][e];
             __syncthreads();
-            fetch(wd + kDepth, nxt[q]);               // refill: kDepth words ahead
-            if (words[wd] != 0u) consume(wd, buf);    // uniform: empty words add nothing
+            fetch(wd + kDepth, nxt[q], nh[q], nw[q], wv[q]);  // refill: kDepth words ahead
+            if (word != 0u) consume(buf, hcur);       // uniform: empty words add nothing
             buf ^= 1;
         }
     }

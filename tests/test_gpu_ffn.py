@@ -192,6 +192,20 @@ def test_fp16_weights(B, d, xdt):
         assert max_rel_l2(per, want) <= ALARM_PER_TOKEN
 
 
+def test_invalid_slots_add_nothing():
+    """Without SI_FLAG_CHECK an invalid slot id (negative or >= L) in a set is skipped: the result
+    is the FFN over the valid slots, on the per-token and the union path."""
+    N, d, L = 500, 256, 300
+    rng, draw, ref, gpu = _rand_problem(77, N, d, L, "bf16")
+    x = draw(3, d, scale=1.0)
+    valid = [rng.permutation(L)[:k].astype(np.int32) for k in (9, 20, 5)]
+    bad = [np.concatenate([v[:3], [L + 5, -1], v[3:]]).astype(np.int32) for v in valid]
+    want = _oracle(x, valid, ref)
+    one = np.stack([_run(x[b:b + 1], [bad[b]], gpu)[0] for b in range(3)])
+    assert max_rel_l2(one, want) <= ALARM_PER_TOKEN
+    assert max_rel_l2(_run(x, bad, gpu), want) <= TOL["bf16"]
+
+
 def test_llama2_7b_batch16_union():
     cfg, ref, gpu = _layer("llama2_7b_b16")
     say("7B batch-16 union path: 2 steps of 16 tokens")
