@@ -63,6 +63,13 @@ __device__ __forceinline__ void st16(void* p, const V16& v) {
 // read this way must be smaller than 2 GiB.
 typedef __attribute__((ext_vector_type(4))) int i32x4_t;
 constexpr int kOOB = (int)0x80000000;
+
+// 16-byte store with the non-temporal hint: for data written once and read once by the next
+// kernel (partial sums), which need not stay in this XCD's L2
+__device__ __forceinline__ void st16_nt(void* p, const V16& v) {
+    const i32x4_t t = {(int)v.w[0], (int)v.w[1], (int)v.w[2], (int)v.w[3]};
+    __builtin_nontemporal_store(t, reinterpret_cast<i32x4_t*>(p));
+}
 constexpr int kBufWord3 = 0x00020000;  // dword 3 of a raw gfx9 descriptor: 32-bit data format
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {

@@ -17,6 +17,8 @@
 // is deterministic and no global atomics are used.
 #include <hip/hip_ext.h>
 
+#include <type_traits>
+
 #include "common.h"
 #include "launch.h"
 
@@ -184,6 +186,18 @@ struct RowLoader<WT, false, NI> {
     }
 };
 
+// f(std::integral_constant<int, n>) for a run-time n in [N, R]: code that must know a row
+// count at compile time, reached through a chain of uniform compares
+template <int N, int R, class F>
+__device__ __forceinline__ void with_rows(int n, F& f) {
+    if constexpr (N <= R) {
+        if (n == N)
+            f(std::integral_constant<int, N>());
+        else
+            with_rows<N + 1, R>(n, f);
+    }
+}
+
 // floor(n * p / P) for 0 <= n, 0 <= p <= P: the first row of chunk p when n rows are dealt to
 // P chunks. The host keeps nnz * P below 2^32 (decode_chunks), so 32-bit arithmetic is exact;
 // the GPU has no integer divide instruction and a 64-bit emulation is several times longer.
@@ -218,6 +232,13 @@ __global__ __launch_bounds__(kThreads) void sffn_rows(
     }
     const RowLoader<WT, BUF, NI> ldr(gate_up_c, down_c, L, d, col, cok);
 
+    // x first: vector loads complete in issue order, so the dot products of the first rows
+    // wait only for x and their own rows
+    XSlice<WT, XT> xs[NI];
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(x + (int64_t)b * d, d * (int64_t)sizeof(XT));
+#pragma unroll
+    for (int i = 0; i < NI; ++i) xs[i].load(rx, cok[i] ? (int)(col[i] * (int64_t)sizeof(XT)) : kOOB);
+
     // Slot ids of batch [rb, rb + nr): a batch that lies inside idx is read with unconditional
     // scalar loads, which the compiler merges into one wide load (separate conditional loads
     // would each wait for the previous one). Rows past nr get -1.
@@ -232,74 +253,43 @@ __global__ __launch_bounds__(kThreads) void sffn_rows(
 #pragma unroll
         for (int r = 0; r < R; ++r) sl[r] = r < nr ? sl[r] : -1;
     };
-    // Issues the row loads of a batch: every gate/up load, then the down loads. The memory
-    // system returns the gate/up rows first, so the dot products and the cross-wave exchange
-    // finish while the down rows are still streaming in. Ids are wave-uniform, so the row
-    // bases stay in scalar registers.
-    // Rows past the batch's end (or with an invalid id) issue no load at all: a uniform
-    // branch per row. Out-of-range loads would read no memory but still take issue slots in
-    // the load pipeline, which is the bottleneck while the batch is being issued.
-    // okr[r]: row r of the current batch exists and has a valid slot id (wave-uniform); the
-    // dot products and the down-row FMAs use only such rows, so an invalid id adds nothing
+    // A batch of N rows (N <= R, a constant in each instance, see with_rows), start to end:
+    // every gate/up load, then every down load, the gate/up dot products, their exchange
+    // across the waves, SiLU * up, and the down-row FMAs. The memory system returns the
+    // gate/up rows first, so the dot products and the exchange finish while the down rows are
+    // still streaming in. Ids are wave-uniform, so the row bases stay in scalar registers.
+    // Each of the N rows issues its loads whatever its id (an invalid id loads nothing through
+    // an out-of-range offset), and rows past N issue none: the number of loads still in
+    // flight at each use is then known when the kernel is compiled, and each use waits for
+    // its own row only. (Loads behind a run-time condition make the compiler wait for every
+    // load, down rows included, before the first dot product; and out-of-range loads for the
+    // rows past N would still take issue slots in the load pipeline, the bottleneck while a
+    // batch is being issued.)
+    // okr[r]: row r exists and has a valid slot id (wave-uniform)
     V16 gv[R][NI], uv[R][NI], dv[R][NI];
     bool okr[R];
-    auto issue = [&](const int32_t (&sl)[R]) {
-#pragma unroll
-        for (int r = 0; r < R; ++r) okr[r] = (sl[r] >= 0) && (sl[r] < L);
-#pragma unroll
-        for (int r = 0; r < R; ++r)
-            if (okr[r]) {
-#pragma unroll
-                for (int i = 0; i < NI; ++i) ldr.load_gu(true, sl[r], i, gv[r][i], uv[r][i]);
-            }
-#pragma unroll
-        for (int r = 0; r < R; ++r)
-            if (okr[r]) {
-#pragma unroll
-                for (int i = 0; i < NI; ++i) ldr.load_dn(true, sl[r], i, dv[r][i]);
-            }
-    };
-
-    // x first: vector loads complete in issue order, so the dot products of the first rows
-    // wait only for x and their own rows
-    XSlice<WT, XT> xs[NI];
-    const __amdgpu_buffer_rsrc_t rx = make_rsrc(x + (int64_t)b * d, d * (int64_t)sizeof(XT));
-#pragma unroll
-    for (int i = 0; i < NI; ++i) xs[i].load(rx, cok[i] ? (int)(col[i] * (int64_t)sizeof(XT)) : kOOB);
-
-    // The first batch's slot ids are fetched together with the token's offsets, from the
-    // range this work-group gets when the B tokens hold nnz / B rows each from index 0 (a
-    // top-k output, or one token with offsets {0, nnz}): the row loads then wait for one
-    // memory round trip instead of two (offsets, then ids). The guess is checked before the
-    // ids are used; a wrong guess fetches them again and costs only that round trip.
-    const int64_t per = split(nnz, 1, (int)gridDim.y);
-    const int64_t g0 = (int64_t)b * per + split(per, p, P);
     int32_t sl[R];
-    fetch_ids(g0, R, sl);
-
-    int64_t lo = offsets[b], hi = offsets[b + 1];
-    lo = lo < 0 ? 0 : (lo > nnz ? nnz : lo);
-    hi = hi < lo ? lo : (hi > nnz ? nnz : hi);
-    const int64_t n = hi - lo;
-    int64_t rb = lo + split(n, p, P);
-    const int64_t r1 = lo + split(n, p + 1, P);
-    int nr = (int)((r1 - rb) < R ? (r1 - rb) : R);
-    if (rb == g0) {
-#pragma unroll
-        for (int r = 0; r < R; ++r) sl[r] = r < nr ? sl[r] : -1;
-    } else {
-        fetch_ids(rb, nr, sl);
-    }
-    issue(sl);
-
     __shared__ float red[2][NVAL][kWaves];
     int buf = 0;
-    while (nr > 0) {
+    auto batch = [&](auto ncst) {
+        constexpr int N = decltype(ncst)::value;
+#pragma unroll
+        for (int r = 0; r < R; ++r) okr[r] = r < N && sl[r] >= 0 && sl[r] < L;
+#pragma unroll
+        for (int r = 0; r < N; ++r)
+#pragma unroll
+            for (int i = 0; i < NI; ++i) ldr.load_gu(okr[r], sl[r], i, gv[r][i], uv[r][i]);
+#pragma unroll
+        for (int r = 0; r < N; ++r)
+#pragma unroll
+            for (int i = 0; i < NI; ++i) ldr.load_dn(okr[r], sl[r], i, dv[r][i]);
+        // all N rows, without a branch (a load used only inside a branch is moved into it,
+        // behind the other loads); a row with an invalid id gives a value nobody uses
         float vals[NVAL];
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             float g = 0.0f, u = 0.0f;
-            if (okr[r]) {  // uniform; other rows were not loaded and add nothing
+            if (r < N) {
 #pragma unroll
                 for (int i = 0; i < NI; ++i) {
                     g = xs[i].dot(gv[r][i], g);
@@ -321,26 +311,54 @@ __global__ __launch_bounds__(kThreads) void sffn_rows(
         }
         const float uu = __shfl_down(t, R, kWave);
         const float hv = silu_f32(t) * uu;  // valid in lanes 0 .. R-1
+        // h_r * down_r for the N rows, again without a branch: a row with an invalid id has
+        // h = 0 and a zero down row, and adds exactly nothing. Every load of the batch is
+        // consumed here, so none is in flight where the instances of this code meet.
 #pragma unroll
-        for (int r = 0; r < R; ++r) {
-            if (okr[r]) {
-                const float h = __builtin_bit_cast(
-                    float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, hv), r));
+        for (int r = 0; r < N; ++r) {
+            float h = __builtin_bit_cast(
+                float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, hv), r));
+            h = okr[r] ? h : 0.0f;
 #pragma unroll
-                for (int i = 0; i < NI; ++i) {
-                    float df[V];
-                    Elem<WT>::unpack(dv[r][i], df);
+            for (int i = 0; i < NI; ++i) {
+                float df[V];
+                Elem<WT>::unpack(dv[r][i], df);
 #pragma unroll
-                    for (int e = 0; e < V; ++e) acc[i][e] = fmaf(h, df[e], acc[i][e]);
-                }
+                for (int e = 0; e < V; ++e) acc[i][e] = fmaf(h, df[e], acc[i][e]);
             }
         }
+    };
+
+    // The first batch's slot ids are fetched together with the token's offsets, from the
+    // range this work-group gets when the B tokens hold nnz / B rows each from index 0 (a
+    // top-k output, or one token with offsets {0, nnz}): the row loads then wait for one
+    // memory round trip instead of two (offsets, then ids). The guess is checked before the
+    // ids are used; a wrong guess fetches them again and costs only that round trip.
+    const int64_t per = split(nnz, 1, (int)gridDim.y);
+    const int64_t g0 = (int64_t)b * per + split(per, p, P);
+    fetch_ids(g0, R, sl);
+
+    int64_t lo = offsets[b], hi = offsets[b + 1];
+    lo = lo < 0 ? 0 : (lo > nnz ? nnz : lo);
+    hi = hi < lo ? lo : (hi > nnz ? nnz : hi);
+    const int64_t n = hi - lo;
+    int64_t rb = lo + split(n, p, P);
+    const int64_t r1 = lo + split(n, p + 1, P);
+    int nr = (int)((r1 - rb) < R ? (r1 - rb) : R);
+    if (rb == g0) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) sl[r] = r < nr ? sl[r] : -1;
+    } else {
+        fetch_ids(rb, nr, sl);
+    }
+
+    while (nr > 0) {
+        with_rows<1, R>(nr, batch);
         buf ^= 1;
         rb += R;
         if (rb >= r1) break;
         nr = (int)((r1 - rb) < R ? (r1 - rb) : R);
         fetch_ids(rb, nr, sl);
-        issue(sl);
     }
 
     const int64_t nch = part_chunks(d);
@@ -356,7 +374,7 @@ __global__ __launch_bounds__(kThreads) void sffn_rows(
                 o.w[1] = __float_as_uint(acc[i][e + 1]);
                 o.w[2] = __float_as_uint(acc[i][e + 2]);
                 o.w[3] = __float_as_uint(acc[i][e + 3]);
-                st16(out + e, o);
+                st16_nt(out + e, o);
             }
         }
     }

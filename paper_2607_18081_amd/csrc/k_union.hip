@@ -43,6 +43,7 @@ namespace {
 constexpr int kG2Cols = 256;               // GEMM2 columns per work-group
 constexpr int kG2Pitch = kG2Cols + 16;     // LDS row pitch (bf16): rows 32 bytes apart in bank
 constexpr int kGemm1Waves = 8;
+constexpr int kWordRegs = 4;               // GEMM2 chunks span at most 64 kWordRegs words
 
 struct Plan {
     int64_t W;      // 32-bit words per token bitmap (slot s is bit s % 32 of word s / 32)
@@ -66,6 +67,9 @@ Plan make_plan(int64_t B, int64_t L, int64_t d, int num_cu) {
     int64_t ks = ((int64_t)num_cu + ntn * ntm - 1) / (ntn * ntm);
     if (ks > p.W) ks = p.W;
     if (ks > 64) ks = 64;
+    // no chunk longer than GEMM2 holds in registers (W <= 16384 keeps this at most 64)
+    const int64_t ks_min = (p.W + 64 * kWordRegs - 1) / (64 * kWordRegs);
+    if (ks < ks_min) ks = ks_min;
     if (ks < 1) ks = 1;
     p.KS = (int)ks;
     size_t o = 0;
@@ -263,15 +267,16 @@ __global__ __launch_bounds__(64 * kGemm1Waves) void union_gemm1(
 }
 
 // GEMM2 (see the file comment). Grid: (ceil(d/256), ceil(B/(16*MT)), KS); 4 waves.
-template <typename ET, int MT>
+// FAST: H enters the MFMA as its bf16 (or half) rounding alone, without the low part.
+template <typename ET, int MT, bool FAST>
 __global__ __launch_bounds__(256) void union_gemm2(const float* __restrict__ H, int64_t Lp,
                                                    int64_t B, const uint16_t* __restrict__ dc,
                                                    int64_t d, int64_t L,
                                                    const uint32_t* __restrict__ words, int64_t W,
-                                                   float* __restrict__ part, int KS, int fast) {
+                                                   float* __restrict__ part, int KS) {
     const int ks = blockIdx.z;
     const int64_t cw = (W + KS - 1) / KS;          // bitmap words per chunk
-    const int64_t w0 = (int64_t)ks * cw;
+    const int64_t w0 = (int64_t)ks * cw < W ? (int64_t)ks * cw : W;  // chunk ks may be empty
     const int64_t w1 = (w0 + cw < W) ? w0 + cw : W;
     const int64_t c0 = (int64_t)blockIdx.x * kG2Cols;
     const int64_t m0 = (int64_t)blockIdx.y * 16 * MT;
@@ -290,31 +295,34 @@ __global__ __launch_bounds__(256) void union_gemm2(const float* __restrict__ H, 
     const __amdgpu_buffer_rsrc_t rd = make_rsrc(dc, L * d * 2);
     const int sr = threadIdx.x >> 3;         // staging: tile row (slot 32 wd + sr)
     const int sc = (threadIdx.x & 7) * 32;   // staging: first of 32 columns
-    // kDepth words' down rows in flight in registers ahead of the LDS tile being consumed
-    // words of down rows in flight in registers: deeper for few tokens, where the kernel only
-    // streams rows and register room is plentiful
+    // words of down rows in flight in registers ahead of the LDS tile being consumed: deeper
+    // for few tokens, where the kernel only streams rows and register room is plentiful
     constexpr int kDepth = MT == 1 ? 8 : (MT == 2 ? 6 : 3);
+    // The lane's chunk of a word's down rows and its H values (the A operand of its MT token
+    // tiles) travel kDepth words ahead: consuming a word then waits for no memory access.
     V16 nxt[kDepth][4];
-    // The union word, the lane's chunk of the word's down rows and the lane's H values (the A
-    // operand of its MT token tiles) all travel kDepth words ahead: consuming a word then waits
-    // for no memory access.
-    // The union words themselves run a further kDepth words ahead, as vector loads through a
-    // descriptor over this chunk (0 past its end): a row fetch never waits for its word, and
-    // vector loads complete in order, so no scalar-load wait serialises the pipeline.
     float nh[kDepth][MT][8];
-    uint32_t nw[kDepth], wv[kDepth];
     const __amdgpu_buffer_rsrc_t rh = make_rsrc(H, B * Lp * 4);
-    const __amdgpu_buffer_rsrc_t rw = make_rsrc(words + w0, (w1 - w0) * 4);
-    auto load_word = [&](int64_t wd) {
-        return (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(rw, (int)((wd - w0) * 4), 0, 0);
-    };
+    // The chunk's union words (at most 64 kWordRegs) are read once, spread over the lanes:
+    // word w0 + 64 i + l sits in register i of lane l (0 past the chunk), and each step takes
+    // its word from there with a lane read, so the row fetches never wait for a word load.
+    uint32_t wl[kWordRegs];
+    {
+        const __amdgpu_buffer_rsrc_t rw = make_rsrc(words + w0, (w1 - w0) * 4);
 #pragma unroll
-    for (int q = 0; q < kDepth; ++q) wv[q] = load_word(w0 + q);
-    auto fetch = [&](int64_t wd, V16 (&v)[4], float (&hv)[MT][8], uint32_t& word,
-                     uint32_t& wnext) {
-        const uint32_t u = wnext;  // words[wd], loaded kDepth words ago (0 past the chunk)
-        wnext = load_word(wd + kDepth);
-        word = u;
+        for (int i = 0; i < kWordRegs; ++i)
+            wl[i] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(rw, (i * 64 + lane) * 4, 0, 0);
+    }
+    auto word_at = [&](int64_t wd) -> uint32_t {
+        const int r = (int)(wd - w0);            // uniform; 0 <= r
+        uint32_t u = 0u;
+#pragma unroll
+        for (int i = 0; i < kWordRegs; ++i)
+            u = (r >> 6) == i ? (uint32_t)__builtin_amdgcn_readlane((int)wl[i], r & 63) : u;
+        return u;
+    };
+    auto fetch = [&](int64_t wd, V16 (&v)[4], float (&hv)[MT][8]) {
+        const uint32_t u = word_at(wd);
         const bool rok = (u >> sr) & 1u;
         const int64_t slot = wd * 32 + sr;
 #pragma unroll
@@ -336,8 +344,30 @@ __global__ __launch_bounds__(256) void union_gemm2(const float* __restrict__ H, 
             }
         }
     };
-    // consume the LDS tile `bsel` holding slots 32 wd .. 32 wd + 31, with the word's H values
-    auto consume = [&](int bsel, const float (&hvs)[MT][8]) {
+    // the A operands of the MT token tiles from a word's H values: the hi and lo roundings
+    typedef typename Mfma<ET>::vec8 AV;
+    auto a_ops = [&](const float (&hvs)[MT][8], AV (&ahi)[MT], AV (&alo)[MT]) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            const float* hv = hvs[mt];
+            uint32_t hi[4], lo[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const uint32_t h0 = Mfma<ET>::rne(hv[2 * q]);
+                const uint32_t h1 = Mfma<ET>::rne(hv[2 * q + 1]);
+                hi[q] = h0 | (h1 << 16);
+                if (!FAST) {
+                    const uint32_t l0 = Mfma<ET>::rne(hv[2 * q] - Mfma<ET>::widen(h0));
+                    const uint32_t l1 = Mfma<ET>::rne(hv[2 * q + 1] - Mfma<ET>::widen(h1));
+                    lo[q] = l0 | (l1 << 16);
+                }
+            }
+            ahi[mt] = Mfma<ET>::vec(V16{{hi[0], hi[1], hi[2], hi[3]}});
+            if (!FAST) alo[mt] = Mfma<ET>::vec(V16{{lo[0], lo[1], lo[2], lo[3]}});
+        }
+    };
+    // consume the LDS tile `bsel` holding slots 32 wd .. 32 wd + 31, with the word's A operands
+    auto consume = [&](int bsel, const AV (&ahi)[MT], const AV (&alo)[MT]) {
         // B operand: lane (nn, g) needs rows 8g..8g+7 of column nn of each 16-column subtile;
         // ds_read_b64_tr_b16 hands lane i of a 16-lane group element i%4 of the 8-byte pieces
         // addressed by lanes i/4 + 4j, so lane nn addresses row 8g + nn/4 (+4), columns
@@ -358,46 +388,40 @@ __global__ __launch_bounds__(256) void union_gemm2(const float* __restrict__ H, 
             bop[j] = Mfma<ET>::vec(V16{{p0, p1, p2, p3}});
         }
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-            const float* hv = hvs[mt];
-            uint32_t hi[4], lo[4];
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const uint32_t h0 = Mfma<ET>::rne(hv[2 * q]);
-                const uint32_t h1 = Mfma<ET>::rne(hv[2 * q + 1]);
-                hi[q] = h0 | (h1 << 16);
-                const uint32_t l0 = Mfma<ET>::rne(hv[2 * q] - Mfma<ET>::widen(h0));
-                const uint32_t l1 = Mfma<ET>::rne(hv[2 * q + 1] - Mfma<ET>::widen(h1));
-                lo[q] = l0 | (l1 << 16);
-            }
-            const typename Mfma<ET>::vec8 ahi = Mfma<ET>::vec(V16{{hi[0], hi[1], hi[2], hi[3]}});
-            const typename Mfma<ET>::vec8 alo = Mfma<ET>::vec(V16{{lo[0], lo[1], lo[2], lo[3]}});
+        for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                acc[mt][j] = Mfma<ET>::mma(ahi, bop[j], acc[mt][j]);
-                if (!fast) acc[mt][j] = Mfma<ET>::mma(alo, bop[j], acc[mt][j]);
+                acc[mt][j] = Mfma<ET>::mma(ahi[mt], bop[j], acc[mt][j]);
+                if (!FAST) acc[mt][j] = Mfma<ET>::mma(alo[mt], bop[j], acc[mt][j]);
             }
-        }
     };
 #pragma unroll
-    for (int q = 0; q < kDepth; ++q) fetch(w0 + q, nxt[q], nh[q], nw[q], wv[q]);
+    for (int q = 0; q < kDepth; ++q) fetch(w0 + q, nxt[q], nh[q]);
+    // The chunk runs to a multiple of kDepth words; the words past its end are empty (their
+    // loads are out of range). The unrolled body then has no exit, and every register of the
+    // pipeline keeps its place, so no wait for a load in flight is forced before its turn.
+    const int64_t wend = w0 + (w1 - w0 + kDepth - 1) / kDepth * kDepth;
     int buf = 0;
-    for (int64_t wg = w0; wg < w1; wg += kDepth) {
+    for (int64_t wg = w0; wg < wend; wg += kDepth) {
 #pragma unroll
         for (int q = 0; q < kDepth; ++q) {
             const int64_t wd = wg + q;
-            if (wd >= w1) break;                      // uniform over the work-group
 #pragma unroll
             for (int e = 0; e < 4; ++e) st16(&tile[buf][sr][sc + e * 8], nxt[q][e]);
-            const uint32_t word = nw[q];
-            float hcur[MT][8];
+            const uint32_t word = word_at(wd);
+            AV ahi[MT], alo[MT];
+            a_ops(nh[q], ahi, alo);
+            // the A operands are made here, before nh[q] is refilled: computed where they are
+            // used, after the refill, they would keep the old and new H values alive together,
+            // and the pipeline's registers would rotate through copies that wait for loads
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-                for (int e = 0; e < 8; ++e) hcur[mt][e] = nh[q][mt][e];
+            for (int mt = 0; mt < MT; ++mt) {
+                asm volatile("" : "+v"(ahi[mt]));
+                if (!FAST) asm volatile("" : "+v"(alo[mt]));
+            }
             __syncthreads();
-            fetch(wd + kDepth, nxt[q], nh[q], nw[q], wv[q]);  // refill: kDepth words ahead
-            if (word != 0u) consume(buf, hcur);       // uniform: empty words add nothing
+            fetch(wd + kDepth, nxt[q], nh[q]);        // refill: kDepth words ahead
+            if (word != 0u) consume(buf, ahi, alo);   // uniform: empty words add nothing
             buf ^= 1;
         }
     }
@@ -453,6 +477,7 @@ hipError_t launch_union_t(const void* x, int64_t B, int64_t d, const int32_t* of
                           const void* down_c, int64_t L, float* y, void* ws, int flags,
                           int num_cu, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
     const Plan p = make_plan(B, L, d, num_cu);
+    if ((p.W + p.KS - 1) / p.KS > 64 * kWordRegs) return hipErrorInvalidValue;
     uint8_t* base = static_cast<uint8_t*>(ws);
     uint32_t* bits = reinterpret_cast<uint32_t*>(base + p.off_bits);
     uint32_t* words = reinterpret_cast<uint32_t*>(base + p.off_words);
@@ -474,12 +499,14 @@ hipError_t launch_union_t(const void* x, int64_t B, int64_t d, const int32_t* of
         default: SI_G1(1); break;
     }
 #undef SI_G1
-    const int fast = (flags & 4) ? 1 : 0;
+    const bool fast = (flags & 4) != 0;
     dim3 g2((unsigned)((d + kG2Cols - 1) / kG2Cols),
             (unsigned)((B + 16 * p.MT - 1) / (16 * p.MT)), (unsigned)p.KS);
-#define SI_G2(MTV)                                                                              \
-    hipExtLaunchKernelGGL((union_gemm2<ET, MTV>), g2, dim3(256), 0, s, nullptr, ev1, 0, H, p.Lp, \
-                          B, dc, d, L, words, p.W, part, p.KS, fast)
+#define SI_G2F(MTV, F)                                                                          \
+    hipExtLaunchKernelGGL((union_gemm2<ET, MTV, F>), g2, dim3(256), 0, s, nullptr, ev1, 0, H,     \
+                          p.Lp, B, dc, d, L, words, p.W, part, p.KS)
+#define SI_G2(MTV) \
+    if (fast) SI_G2F(MTV, true); else SI_G2F(MTV, false)
     switch (p.MT) {
         case 8: SI_G2(8); break;
         case 4: SI_G2(4); break;
@@ -487,6 +514,7 @@ hipError_t launch_union_t(const void* x, int64_t B, int64_t d, const int32_t* of
         default: SI_G2(1); break;
     }
 #undef SI_G2
+#undef SI_G2F
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     return launch_reduce_partials(part, p.KS, B, d, y, s);

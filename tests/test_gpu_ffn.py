@@ -114,10 +114,13 @@ def test_per_token_ragged_shapes(d, wdtype):
     assert max_rel_l2(got_b, want) <= TOL[wdtype]
 
 
-@pytest.mark.parametrize("B,d", [(2, 264), (5, 1000), (17, 264), (33, 512), (70, 1000)])
-def test_union_path_ragged(B, d):
-    N, L = 900, 613
-    say(f"union ragged B={B} d={d}")
+@pytest.mark.parametrize("B,d,L", [(2, 264, 613), (5, 1000, 613), (17, 264, 613),
+                                   (33, 512, 613), (70, 1000, 613), (3, 72, 16500)])
+def test_union_path_ragged(B, d, L):
+    """Row-word GEMM path; L = 16500 gives over 512 bitmap words, where a work-group takes
+    both 16-row tiles of a word, and the smaller ones one tile each."""
+    N = L + 287
+    say(f"union ragged B={B} d={d} L={L}")
     rng, draw, ref, gpu = _rand_problem(B * 1000 + d, N, d, L, "bf16")
     sets = []
     for b in range(B):
