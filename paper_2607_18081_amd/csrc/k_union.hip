@@ -145,17 +145,21 @@ __global__ __launch_bounds__(64 * kGemm1Waves) void union_gemm1(
     const int g = lane >> 4;
 
     // this word of the union (OR over the batch) and of each token of the tile
+    // (both first reads in one memory round trip: range-checked loads, no branches)
     __shared__ uint32_t wor[kGemm1Waves];
     __shared__ uint32_t tokw[MTOK];
-    uint32_t uw = 0u;
-    for (int64_t b = threadIdx.x; b < B; b += 64 * kGemm1Waves) uw |= bits[b * W + wd];
+    const __amdgpu_buffer_rsrc_t rbits = make_rsrc(bits, B * W * 4);
+    constexpr int kT1 = 64 * kGemm1Waves;
+    const int64_t tk = m0 + threadIdx.x;
+    const uint32_t tw = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(
+        rbits, (threadIdx.x < MTOK && tk < B) ? (int)((tk * W + wd) * 4) : kOOB, 0, 0);
+    uint32_t uw = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(
+        rbits, threadIdx.x < B ? (int)((threadIdx.x * W + wd) * 4) : kOOB, 0, 0);
+    for (int64_t b = threadIdx.x + kT1; b < B; b += kT1) uw |= bits[b * W + wd];
 #pragma unroll
     for (int m = 32; m >= 1; m >>= 1) uw |= (uint32_t)__shfl_xor((int)uw, m, kWave);
     if (lane == 0) wor[w] = uw;
-    if (threadIdx.x < MTOK) {
-        const int64_t tok = m0 + threadIdx.x;
-        tokw[threadIdx.x] = tok < B ? bits[tok * W + wd] : 0u;
-    }
+    if (threadIdx.x < MTOK) tokw[threadIdx.x] = tw;
     __syncthreads();
     uint32_t u = 0u;
 #pragma unroll
@@ -198,37 +202,67 @@ __global__ __launch_bounds__(64 * kGemm1Waves) void union_gemm1(
         }
     const int ntile = n > 16 ? 2 : 1;
     const int64_t nkb = (d + 127) / 128;
-    for (int64_t kb = w; kb < nkb; kb += kGemm1Waves) {
-        V16 gv[2][4], uv[2][4];
+    // The wave's K blocks are kb = w, w + 8, ...: the loads of the next block are in flight
+    // while the MFMAs of the current one run (two register sets, the loop unrolled by two).
+    // Blocks past the end load nothing (out-of-range offsets) and add zeros. The MFMAs of the
+    // second tile run even when it is empty: a load used only under a branch would be moved
+    // into it, behind the MFMAs of the first tile.
+    struct Blk {
+        V16 g[2][4], u[2][4], x[MT1][4];
+    };
+    auto load = [&](int64_t kb, Blk& bk) {
 #pragma unroll
         for (int st = 0; st < 2; ++st)
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 const int64_t pos = kb * 128 + e * 32 + g * 8;    // element index in the row
                 const bool in = pos < d && goff[st] != kOOB;
-                gv[st][e] = bload16(rg, in ? goff[st] + (int)(pos * 2) : kOOB);
-                uv[st][e] = bload16(rg, in ? goff[st] + (int)((d + pos) * 2) : kOOB);
+                bk.g[st][e] = bload16(rg, in ? goff[st] + (int)(pos * 2) : kOOB);
+                bk.u[st][e] = bload16(rg, in ? goff[st] + (int)((d + pos) * 2) : kOOB);
             }
 #pragma unroll
-        for (int mt = 0; mt < MT1; ++mt) {
-            V16 xv[4];
+        for (int mt = 0; mt < MT1; ++mt)
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 const int64_t pos = kb * 128 + e * 32 + g * 8;
-                xv[e] = bload16(rx, (pos < d && xoff[mt] != kOOB) ? xoff[mt] + (int)(pos * 2)
-                                                                 : kOOB);
+                bk.x[mt][e] = bload16(rx, (pos < d && xoff[mt] != kOOB) ? xoff[mt] + (int)(pos * 2)
+                                                                        : kOOB);
             }
+    };
+    auto mma = [&](const Blk& bk) {
+#pragma unroll
+        for (int mt = 0; mt < MT1; ++mt)
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                const typename Mfma<ET>::vec8 a = Mfma<ET>::vec(xv[e]);
+                const typename Mfma<ET>::vec8 a = Mfma<ET>::vec(bk.x[mt][e]);
 #pragma unroll
                 for (int st = 0; st < 2; ++st) {
-                    if (st < ntile) {
-                        accg[mt][st] = Mfma<ET>::mma(a, Mfma<ET>::vec(gv[st][e]), accg[mt][st]);
-                        accu[mt][st] = Mfma<ET>::mma(a, Mfma<ET>::vec(uv[st][e]), accu[mt][st]);
-                    }
+                    accg[mt][st] = Mfma<ET>::mma(a, Mfma<ET>::vec(bk.g[st][e]), accg[mt][st]);
+                    accu[mt][st] = Mfma<ET>::mma(a, Mfma<ET>::vec(bk.u[st][e]), accu[mt][st]);
                 }
             }
+    };
+    // (the scheduling barriers keep each block's loads ahead of the other block's MFMAs).
+    // With four token tiles two register sets do not fit: one block at a time.
+    if constexpr (MT1 <= 2) {
+        Blk b0, b1;
+        load(w, b0);
+        for (int64_t kb = w; kb < nkb; kb += 2 * kGemm1Waves) {
+            load(kb + kGemm1Waves, b1);
+            __builtin_amdgcn_sched_barrier(0);
+            mma(b0);
+            __builtin_amdgcn_sched_barrier(0);
+            load(kb + 2 * kGemm1Waves, b0);
+            __builtin_amdgcn_sched_barrier(0);
+            mma(b1);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    } else {
+        for (int64_t kb = w; kb < nkb; kb += kGemm1Waves) {
+            Blk b0;
+            load(kb, b0);
+            __builtin_amdgcn_sched_barrier(0);
+            mma(b0);
         }
     }
     // the 8 waves' partial tiles meet in LDS; wave 0 adds them in a fixed order
@@ -461,7 +495,7 @@ static bool use_tiled(int64_t B, int64_t L, int64_t d) {
 bool union_supported(int64_t B, int64_t L, int64_t d) {
     // buffer loads take 32-bit byte offsets
     return L * 2 * d * 2 < ((int64_t)1 << 31) && B * d * 2 < ((int64_t)1 << 31) &&
-           L <= 524288;
+           L <= 524288 && B * ((L + 31) / 32) * 4 < ((int64_t)1 << 31);
 }
 
 size_t union_workspace(int64_t B, int64_t L, int64_t d, int num_cu) {
