@@ -71,10 +71,80 @@ __device__ __forceinline__ void xstore(bf16_t* p, int64_t i, float v) {
     p[i] = (bf16_t)f32_to_bf16_rne(v);
 }
 
+// One work-group of 1024 threads per token. Thread t owns the groups of four elements
+// 4 t + 4096 j: the first pass reads them (up to 16384 elements stay in registers, all loads
+// issued together), the sum of squares goes through a fixed shuffle tree in each wave and a
+// fixed-order sum of the 16 wave totals, and the second pass scales and stores.
+constexpr int kRmsThreads = 1024;
+constexpr int kRmsChunk = 4 * kRmsThreads;  // elements per chunk
+constexpr int kRmsHold = 4;                 // chunks held in registers
+
 template <typename XT>
-__global__ __launch_bounds__(256) void residual_rmsnorm(const XT* x, const float* __restrict__ y,
-                                                        int64_t d, float eps, XT* xo) {
+__global__ __launch_bounds__(kRmsThreads) void residual_rmsnorm(const XT* x,
+                                                               const float* __restrict__ y,
+                                                               int64_t d, float eps, XT* xo) {
     // x and xo may alias: each element is read and then written by the same thread
+    const int64_t b = blockIdx.x;
+    const XT* xb = x + b * d;
+    const float* yb = y + b * d;
+    XT* ob = xo + b * d;
+    const int t = threadIdx.x;
+    const int64_t nch = (d + kRmsChunk - 1) / kRmsChunk;
+    // d is a multiple of 4 (residual_rmsnorm_any takes the others), so a group of four is
+    // all in or all out
+    auto load_r = [&](int64_t i, float (&r)[4]) {
+        if (i < d) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) r[e] = xval<XT>(xb, i + e) + yb[i + e];
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) r[e] = 0.0f;
+        }
+    };
+    float r[kRmsHold][4];
+    float ss = 0.0f;
+    for (int64_t c0 = 0; c0 < nch; c0 += kRmsHold) {
+#pragma unroll
+        for (int h = 0; h < kRmsHold; ++h) load_r((c0 + h) * kRmsChunk + 4 * t, r[h]);
+#pragma unroll
+        for (int h = 0; h < kRmsHold; ++h)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) ss = fmaf(r[h][e], r[h][e], ss);
+    }
+#pragma unroll
+    for (int m = 1; m < kWave; m <<= 1) ss += __shfl_xor(ss, m, kWave);
+    __shared__ float red[kRmsThreads / kWave];
+    if ((t & (kWave - 1)) == 0) red[t / kWave] = ss;
+    __syncthreads();
+    float tot = 0.0f;
+#pragma unroll
+    for (int q = 0; q < kRmsThreads / kWave; ++q) tot += red[q];
+    const float scale = 1.0f / sqrtf(tot / (float)d + eps);
+    if (nch <= kRmsHold) {
+#pragma unroll
+        for (int h = 0; h < kRmsHold; ++h) {
+            const int64_t i = h * kRmsChunk + 4 * t;
+            if (i < d) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) xstore(ob, i + e, r[h][e] * scale);
+            }
+        }
+    } else {
+        for (int64_t i = 4 * t; i < d; i += kRmsChunk) {
+            float q[4];
+            load_r(i, q);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) xstore(ob, i + e, q[e] * scale);
+        }
+    }
+}
+
+// Any d (d not a multiple of 4): 256 threads, strided loops, the same fixed-order reduction
+// shape per work-group.
+template <typename XT>
+__global__ __launch_bounds__(256) void residual_rmsnorm_any(const XT* x,
+                                                            const float* __restrict__ y,
+                                                            int64_t d, float eps, XT* xo) {
     const int64_t b = blockIdx.x;
     const XT* xb = x + b * d;
     const float* yb = y + b * d;
@@ -120,12 +190,26 @@ hipError_t launch_check_csr(const int32_t* offsets, const int32_t* idx, int64_t 
 hipError_t launch_residual_rmsnorm(const void* x, int xdt, const float* y, int64_t B, int64_t d,
                                    float eps, void* x_out, hipStream_t s) {
     if (B == 0) return hipSuccess;
-    if (xdt == 1)
-        hipLaunchKernelGGL(residual_rmsnorm<bf16_t>, dim3((unsigned)B), dim3(256), 0, s,
-                           static_cast<const bf16_t*>(x), y, d, eps, static_cast<bf16_t*>(x_out));
-    else
-        hipLaunchKernelGGL(residual_rmsnorm<float>, dim3((unsigned)B), dim3(256), 0, s,
-                           static_cast<const float*>(x), y, d, eps, static_cast<float*>(x_out));
+    const bool v4 = d % 4 == 0;
+    if (xdt == 1) {
+        const bf16_t* xi = static_cast<const bf16_t*>(x);
+        bf16_t* xo = static_cast<bf16_t*>(x_out);
+        if (v4)
+            hipLaunchKernelGGL(residual_rmsnorm<bf16_t>, dim3((unsigned)B), dim3(kRmsThreads), 0,
+                               s, xi, y, d, eps, xo);
+        else
+            hipLaunchKernelGGL(residual_rmsnorm_any<bf16_t>, dim3((unsigned)B), dim3(256), 0, s,
+                               xi, y, d, eps, xo);
+    } else {
+        const float* xi = static_cast<const float*>(x);
+        float* xo = static_cast<float*>(x_out);
+        if (v4)
+            hipLaunchKernelGGL(residual_rmsnorm<float>, dim3((unsigned)B), dim3(kRmsThreads), 0,
+                               s, xi, y, d, eps, xo);
+        else
+            hipLaunchKernelGGL(residual_rmsnorm_any<float>, dim3((unsigned)B), dim3(256), 0, s,
+                               xi, y, d, eps, xo);
+    }
     return hipGetLastError();
 }
 

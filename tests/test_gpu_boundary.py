@@ -144,11 +144,14 @@ def test_topk_ties_zeros_nan(L):
         si.select_topk(scores, L + 1)
 
 
-@pytest.mark.parametrize("xdt", ["bf16", "f32"])
-def test_residual_rmsnorm(xdt):
-    say(f"rmsnorm {xdt}")
-    rng = np.random.default_rng(9)
-    B, d = 5, 4096
+@pytest.mark.parametrize("xdt,d", [("bf16", 4096), ("f32", 4096), ("bf16", 20000),
+                                   ("f32", 100), ("bf16", 102), ("f32", 4098)])
+def test_residual_rmsnorm(xdt, d):
+    """d = 4096: one chunk held in registers; 20000: past the register-held size, the second
+    pass reads again; 102 and 4098 (not multiples of 4): the generic kernel."""
+    say(f"rmsnorm {xdt} d={d}")
+    rng = np.random.default_rng(9 + d)
+    B = 5
     x32 = rng.standard_normal((B, d)).astype(np.float32)
     x = (x32.view(np.uint32) >> 16).astype(np.uint16) if xdt == "bf16" else x32
     y = (rng.standard_normal((B, d)) * 0.3).astype(np.float32)
