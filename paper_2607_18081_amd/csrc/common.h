@@ -86,6 +86,20 @@ __device__ __forceinline__ V16 bload16(__amdgpu_buffer_rsrc_t r, int off) {
     return o;
 }
 
+// The same load with the non-temporal cache policy: for weight rows that a launch reads once
+// (a decode step's active rows). Measured on a 54 MB gather of 24 KB rows: 10.4 us against
+// 11.3 us with the default policy.
+constexpr int kNonTemporal = 2;  // cache-policy word of a gfx950 buffer access: nt
+__device__ __forceinline__ V16 bload16nt(__amdgpu_buffer_rsrc_t r, int off) {
+    const i32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kNonTemporal);
+    V16 o;
+    o.w[0] = (uint32_t)v[0];
+    o.w[1] = (uint32_t)v[1];
+    o.w[2] = (uint32_t)v[2];
+    o.w[3] = (uint32_t)v[3];
+    return o;
+}
+
 // Buffer load at a per-lane offset plus a wave-uniform (scalar-register) offset. The row base
 // of a gather goes in the scalar offset, so addressing a row costs no vector instructions.
 __device__ __forceinline__ V16 bload16s(__amdgpu_buffer_rsrc_t r, int voff, int soff) {

@@ -123,10 +123,10 @@ struct XSlice<f16_t, f16_t> {
 };
 
 // Row loads of the gather-GEMV; lane column group i of row j, for a wave-uniform slot id j and
-// validity flag ok. BUF: buffer loads with 32-bit offsets (the compacted tensors must be
-// smaller than 2 GiB); a row or column that must read nothing gets an offset past the end of
-// the buffer, so the access reads no memory and returns zeros, without a branch. Otherwise
-// guarded global loads.
+// validity flag ok. A step reads each of its rows once, so the loads are non-temporal.
+// BUF: buffer loads with 32-bit offsets (the compacted tensors must be smaller than 2 GiB); a
+// row or column that must read nothing gets an offset past the end of the buffer, so the access
+// reads no memory and returns zeros, without a branch. Otherwise guarded global loads.
 template <typename WT, bool BUF, int NI>
 struct RowLoader;
 
@@ -147,11 +147,11 @@ struct RowLoader<WT, true, NI> {
     // kOOB + a row offset (< 2^31) stays out of range without wrapping
     __device__ __forceinline__ void load_gu(bool ok, int32_t j, int i, V16& g, V16& u) const {
         const int og = ok ? vcol[i] + j * rowg : kOOB;
-        g = bload16(rg, og);
-        u = bload16(rg, og + rowd);
+        g = bload16nt(rg, og);
+        u = bload16nt(rg, og + rowd);
     }
     __device__ __forceinline__ void load_dn(bool ok, int32_t j, int i, V16& dn) const {
-        dn = bload16(rd, ok ? vcol[i] + j * rowd : kOOB);
+        dn = bload16nt(rd, ok ? vcol[i] + j * rowd : kOOB);
     }
 };
 
