@@ -162,19 +162,27 @@ class Workload:
             si.selective_ffn(self.x[t0:t0 + B], self.off[0][s], self._slots(0, s),
                              cp.gate_up_c, cp.down_c, y=self.y[t0:t0 + B], workspace=self.ws)
         else:
+            # layer l > 0 takes the previous pair (x_{l-1}, y_{l-1}) and normalises it in the
+            # prologue of its own gather-GEMV (si_selective_ffn_resnorm); the last layer's
+            # output goes through si_residual_rmsnorm, so every layer does the same work
             xin = self.x[t0:t0 + 1]
+            y = self.y[t0:t0 + 1]
             for lay in range(cfg.layers):
                 cp = self.layers[lay][0]
                 if timing:
                     si.set_timing_events(*timing[lay])
-                y = self.y[t0:t0 + 1]
-                si.selective_ffn(xin, self.off[lay][s], self._slots(lay, s), cp.gate_up_c,
-                                 cp.down_c, y=y, workspace=self.ws)
+                if lay == 0:
+                    si.selective_ffn(xin, self.off[lay][s], self._slots(lay, s), cp.gate_up_c,
+                                     cp.down_c, y=y, workspace=self.ws)
+                else:
+                    xout = self.xbuf[lay % 2]
+                    si.selective_ffn_resnorm(xin, y, self.off[lay][s], self._slots(lay, s),
+                                             cp.gate_up_c, cp.down_c, x_out=xout, y=y,
+                                             workspace=self.ws)
+                    xin = xout
                 if timing:
                     si.set_timing_events(None, None)
-                xout = self.xbuf[lay % 2]
-                si.residual_rmsnorm(xin, y, out=xout)
-                xin = xout
+            si.residual_rmsnorm(xin, y, out=self.xbuf[cfg.layers % 2])
         if timing:
             si.set_timing_events(None, None)
 

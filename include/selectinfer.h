@@ -188,6 +188,35 @@ int si_residual_rmsnorm(const void* x, si_dtype xdt, const float* y, int64_t B, 
                         float eps, void* x_out, void* hip_stream);
 
 /*
+ * One layer of a stacked FFN whose input is the previous layer's pair (the per-layer step of
+ * an FFN stack fed sequentially; the paper's Selective Computation section for the FFN):
+ *
+ *   x_out[b] = RMSNorm(x_prev[b] + y_prev[b])   (as si_residual_rmsnorm, unit gain, eps)
+ *   y[b]     = the selective FFN of x_out[b]    (as si_selective_ffn, same arguments)
+ *
+ *   x_prev [B][d] xdt (SI_F32 or SI_BF16), y_prev [B][d] float32: the previous layer's input
+ *                 and output
+ *   x_out  [B][d] xdt out: this layer's input, kept for the next layer's residual
+ *
+ * On the per-token path the normalisation runs in the prologue of the gather-GEMV kernel:
+ * every work-group of a token computes it for its own columns (the sum of squares is reduced
+ * in a fixed order, the same in each work-group) and the token's first work-group stores
+ * x_out, so a layer takes one kernel launch less than si_residual_rmsnorm followed by
+ * si_selective_ffn. On the union path the two run one after the other. The result equals that
+ * pair of calls up to the summation order of the mean square (x_out may differ by one bf16
+ * unit where r / rms falls next to a rounding boundary).
+ * x_out must not overlap x_prev, y_prev or y; y may alias y_prev. Other requirements, errors
+ * and the workspace are those of si_selective_ffn; x_prev, y_prev and x_out 16-byte aligned,
+ * eps >= 0.
+ */
+int si_selective_ffn_resnorm(const void* x_prev, const float* y_prev, float eps, void* x_out,
+                             si_dtype xdt, int64_t B, int64_t d,
+                             const int32_t* offsets, const int32_t* idx, int64_t nnz,
+                             const void* gate_up_c, const void* down_c, int64_t L,
+                             si_dtype wdt, float* y, void* ws, size_t ws_bytes, int flags,
+                             void* hip_stream);
+
+/*
  * Dynamic-set construction (Selective Computation section) for one prompt of T tokens over a
  * compacted layer:
  *   1. a_t[j] = SiLU(gate_c[j] . x[t]) * (up_c[j] . x[t]) for every loaded slot j (float32);

@@ -175,6 +175,41 @@ def selective_ffn(x: torch.Tensor, offsets: torch.Tensor, idx: torch.Tensor,
     return y
 
 
+def selective_ffn_resnorm(x_prev: torch.Tensor, y_prev: torch.Tensor, offsets: torch.Tensor,
+                          idx: torch.Tensor, gate_up_c: torch.Tensor, down_c: torch.Tensor,
+                          eps: float = 1e-5, flags: int = 0, x_out: torch.Tensor | None = None,
+                          y: torch.Tensor | None = None,
+                          workspace: torch.Tensor | None = None):
+    """si_selective_ffn_resnorm: x = RMSNorm(x_prev + y_prev) -> x_out, then the selective FFN
+    of x -> y. Returns (x_out, y)."""
+    dev = _dev(x_prev)
+    if x_prev.dim() != 2 or y_prev.shape != x_prev.shape or y_prev.dtype != torch.float32:
+        raise ValueError("x_prev must be [B][d] and y_prev [B][d] float32")
+    B, d = x_prev.shape
+    L = gate_up_c.shape[0]
+    if gate_up_c.shape != (L, 2, d) or down_c.shape != (L, d):
+        raise ValueError("compacted weights must be [L][2][d] and [L][d]")
+    if offsets.dtype != torch.int32 or idx.dtype != torch.int32:
+        raise ValueError("offsets and idx must be int32")
+    if offsets.numel() < B + 1:
+        raise ValueError("offsets needs B + 1 entries")
+    nnz = idx.numel()
+    if x_out is None:
+        x_out = torch.empty_like(x_prev)
+    if y is None:
+        y = torch.empty((B, d), dtype=torch.float32, device=dev)
+    need = selective_ffn_workspace(B, nnz, L, d, _dt(x_prev), _dt(gate_up_c), flags)
+    if workspace is None:
+        workspace = _workspace(dev, need)
+    st = load().si_selective_ffn_resnorm(_ptr(x_prev), _ptr(y_prev), float(eps), _ptr(x_out),
+                                         _dt(x_prev), B, d, _ptr(offsets), _ptr(idx), nnz,
+                                         _ptr(gate_up_c), _ptr(down_c), L, _dt(gate_up_c),
+                                         _ptr(y), _ptr(workspace), workspace.numel(), flags,
+                                         _stream(dev))
+    _check(st, "si_selective_ffn_resnorm")
+    return x_out, y
+
+
 def set_timing_events(start: "torch.cuda.Event | None", stop: "torch.cuda.Event | None") -> None:
     """si_set_timing_events: bracket the main kernel of later selective_ffn calls on this thread.
 

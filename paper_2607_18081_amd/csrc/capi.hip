@@ -85,6 +85,56 @@ bool use_union(int64_t B, int64_t L, int64_t d, si_dtype xdt, si_dtype wdt, int 
            !(flags & SI_FLAG_PER_TOKEN) && si::union_supported(B, L, d);
 }
 
+// [a, a + na) and [b, b + nb) share a byte
+bool overlap(const void* a, int64_t na, const void* b, int64_t nb) {
+    const uintptr_t pa = reinterpret_cast<uintptr_t>(a), pb = reinterpret_cast<uintptr_t>(b);
+    return pa < pb + (uintptr_t)nb && pb < pa + (uintptr_t)na;
+}
+
+// si_selective_ffn, and with rn the same call whose x is first computed from the previous
+// layer's pair (si_selective_ffn_resnorm; x then points at rn->x_out)
+int selective_ffn(const void* x, si_dtype xdt, int64_t B, int64_t d, const int32_t* offsets,
+                  const int32_t* idx, int64_t nnz, const void* gate_up_c, const void* down_c,
+                  int64_t L, si_dtype wdt, float* y, void* ws, size_t ws_bytes, int flags,
+                  void* hip_stream, const si::ResNormIn* rn) {
+    if (B < 0 || d < 1 || L < 1 || nnz < 0) return SI_ERR_INVALID;
+    if (!valid_pair(xdt, wdt)) return SI_ERR_UNSUPPORTED;
+    if (B > 65535 || nnz > INT32_MAX || L > INT32_MAX) return SI_ERR_UNSUPPORTED;
+    if (si::decode_supported(xdt, wdt, d)) return SI_ERR_UNSUPPORTED;
+    if (B == 0) return SI_OK;
+    if (!x || !offsets || !gate_up_c || !down_c || !y) return SI_ERR_INVALID;
+    if (nnz > 0 && !idx) return SI_ERR_INVALID;
+    if (!aligned16(x) || !aligned16(gate_up_c) || !aligned16(down_c) || !aligned16(y))
+        return SI_ERR_INVALID;
+    const size_t need = si_selective_ffn_workspace(B, nnz, L, d, xdt, wdt, flags);
+    if (need > 0 && (!ws || ws_bytes < need || !aligned16(ws))) return SI_ERR_WORKSPACE;
+    const int dev = current_device();
+    if (dev < 0) return SI_ERR_HIP;
+    hipStream_t s = static_cast<hipStream_t>(hip_stream);
+    if (flags & SI_FLAG_CHECK) {
+        if (L > 524288) return SI_ERR_UNSUPPORTED;
+        const int st = checked(s, dev, [&](int* err) {
+            return si::launch_check_csr(offsets, idx, B, nnz, L, err, s);
+        });
+        if (st != SI_OK) return st;
+    }
+    const int ncu = num_cu(dev);
+    if (use_union(B, L, d, xdt, wdt, flags)) {
+        // the union kernels take x as is: the normalisation runs as its own kernel first
+        if (rn) {
+            const hipError_t e = si::launch_residual_rmsnorm(rn->x_prev, xdt, rn->y_prev, B, d,
+                                                             rn->eps, rn->x_out, s);
+            if (e != hipSuccess) return SI_ERR_HIP;
+        }
+        return from_hip(si::launch_union(x, B, d, offsets, idx, nnz, gate_up_c, down_c, L, wdt, y,
+                                         ws, flags, ncu, s, t_ev_start, t_ev_stop));
+    }
+    const int P = si::decode_chunks(B, nnz, ncu);
+    return from_hip(si::launch_decode(x, xdt, B, d, offsets, idx, nnz, gate_up_c, down_c, L, wdt,
+                                      static_cast<float*>(ws), P, y, s, t_ev_start, t_ev_stop,
+                                      rn));
+}
+
 }  // namespace
 
 extern "C" {
@@ -169,34 +219,29 @@ int si_selective_ffn(const void* x, si_dtype xdt, int64_t B, int64_t d, const in
                      const int32_t* idx, int64_t nnz, const void* gate_up_c, const void* down_c,
                      int64_t L, si_dtype wdt, float* y, void* ws, size_t ws_bytes, int flags,
                      void* hip_stream) {
-    if (B < 0 || d < 1 || L < 1 || nnz < 0) return SI_ERR_INVALID;
-    if (!valid_pair(xdt, wdt)) return SI_ERR_UNSUPPORTED;
-    if (B > 65535 || nnz > INT32_MAX || L > INT32_MAX) return SI_ERR_UNSUPPORTED;
-    if (si::decode_supported(xdt, wdt, d)) return SI_ERR_UNSUPPORTED;
-    if (B == 0) return SI_OK;
-    if (!x || !offsets || !gate_up_c || !down_c || !y) return SI_ERR_INVALID;
-    if (nnz > 0 && !idx) return SI_ERR_INVALID;
-    if (!aligned16(x) || !aligned16(gate_up_c) || !aligned16(down_c) || !aligned16(y))
-        return SI_ERR_INVALID;
-    const size_t need = si_selective_ffn_workspace(B, nnz, L, d, xdt, wdt, flags);
-    if (need > 0 && (!ws || ws_bytes < need || !aligned16(ws))) return SI_ERR_WORKSPACE;
-    const int dev = current_device();
-    if (dev < 0) return SI_ERR_HIP;
-    hipStream_t s = static_cast<hipStream_t>(hip_stream);
-    if (flags & SI_FLAG_CHECK) {
-        if (L > 524288) return SI_ERR_UNSUPPORTED;
-        const int st = checked(s, dev, [&](int* err) {
-            return si::launch_check_csr(offsets, idx, B, nnz, L, err, s);
-        });
-        if (st != SI_OK) return st;
+    return selective_ffn(x, xdt, B, d, offsets, idx, nnz, gate_up_c, down_c, L, wdt, y, ws,
+                         ws_bytes, flags, hip_stream, nullptr);
+}
+
+int si_selective_ffn_resnorm(const void* x_prev, const float* y_prev, float eps, void* x_out,
+                             si_dtype xdt, int64_t B, int64_t d, const int32_t* offsets,
+                             const int32_t* idx, int64_t nnz, const void* gate_up_c,
+                             const void* down_c, int64_t L, si_dtype wdt, float* y, void* ws,
+                             size_t ws_bytes, int flags, void* hip_stream) {
+    if (xdt != SI_F32 && xdt != SI_BF16) return SI_ERR_UNSUPPORTED;
+    if (!(eps >= 0.0f)) return SI_ERR_INVALID;
+    if (B > 0) {
+        if (!x_prev || !y_prev || !x_out) return SI_ERR_INVALID;
+        if (!aligned16(x_prev) || !aligned16(y_prev) || !aligned16(x_out)) return SI_ERR_INVALID;
+        // x_out is written while x_prev and y_prev are read, and before y is
+        const int64_t xb = B * d * (xdt == SI_F32 ? 4 : 2);
+        if (overlap(x_out, xb, x_prev, xb) || overlap(x_out, xb, y_prev, B * d * 4) ||
+            (y && overlap(x_out, xb, y, B * d * 4)))
+            return SI_ERR_INVALID;
     }
-    const int ncu = num_cu(dev);
-    if (use_union(B, L, d, xdt, wdt, flags))
-        return from_hip(si::launch_union(x, B, d, offsets, idx, nnz, gate_up_c, down_c, L, wdt, y,
-                                         ws, flags, ncu, s, t_ev_start, t_ev_stop));
-    const int P = si::decode_chunks(B, nnz, ncu);
-    return from_hip(si::launch_decode(x, xdt, B, d, offsets, idx, nnz, gate_up_c, down_c, L, wdt,
-                                      static_cast<float*>(ws), P, y, s, t_ev_start, t_ev_stop));
+    const si::ResNormIn rn{x_prev, y_prev, eps, x_out};
+    return selective_ffn(x_out, xdt, B, d, offsets, idx, nnz, gate_up_c, down_c, L, wdt, y, ws,
+                         ws_bytes, flags, hip_stream, &rn);
 }
 
 int si_set_timing_events(void* start, void* stop) {

@@ -77,6 +77,11 @@ struct XSlice {
     __device__ __forceinline__ static float xval(const uint32_t (&wd)[N], int e, const f16_t*) {
         return f16_to_f32((e & 1) ? (wd[e >> 1] >> 16) : (wd[e >> 1] & 0xffffu));
     }
+    // v = f: values already rounded to XT
+    __device__ __forceinline__ void set(const float (&f)[V]) {
+#pragma unroll
+        for (int e = 0; e < V; ++e) v[e] = f[e];
+    }
     __device__ __forceinline__ float dot(const V16& w, float acc) const {
         float f[V];
         Elem<WT>::unpack(w, f);
@@ -93,6 +98,12 @@ struct XSlice<bf16_t, bf16_t> {
         const V16 t = bload16(r, off);
 #pragma unroll
         for (int q = 0; q < 4; ++q) v[q] = t.w[q];
+    }
+    // f: 8 values already rounded to bf16, packed back into pairs
+    __device__ __forceinline__ void set(const float (&f)[8]) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            v[q] = (__float_as_uint(f[2 * q]) >> 16) | (__float_as_uint(f[2 * q + 1]) & 0xffff0000u);
     }
     __device__ __forceinline__ float dot(const V16& w, float acc) const {
 #pragma unroll
@@ -121,6 +132,55 @@ struct XSlice<f16_t, f16_t> {
         return acc;
     }
 };
+
+// Residual RMSNorm prologue: V consecutive elements of a row of type T (float or bf16) as
+// float32, through a buffer descriptor (kOOB: zeros, no access).
+template <typename T, int V>
+__device__ __forceinline__ void load_elems(__amdgpu_buffer_rsrc_t r, int off, float (&f)[V]) {
+    if constexpr (sizeof(T) == 4) {
+#pragma unroll
+        for (int q = 0; q < V / 4; ++q) {
+            const V16 t = bload16(r, off == kOOB ? kOOB : off + 16 * q);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) f[4 * q + e] = __uint_as_float(t.w[e]);
+        }
+    } else if constexpr (V == 8) {
+        const V16 t = bload16(r, off);
+        Elem<bf16_t>::unpack(t, f);
+    } else {
+        const i32x2_t t = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+            f[2 * e] = bf16lo((uint32_t)t[e]);
+            f[2 * e + 1] = bf16hi((uint32_t)t[e]);
+        }
+    }
+}
+// a float32 value rounded to the storage type T and widened back (bf16: round to nearest even)
+template <typename T>
+__device__ __forceinline__ float round_to(float f) {
+    if constexpr (sizeof(T) == 4) return f;
+    else return bf16_to_f32(f32_to_bf16_rne(f));
+}
+// V values (already rounded to T) stored as T at p
+template <typename T, int V>
+__device__ __forceinline__ void store_elems(T* p, const float (&f)[V]) {
+    if constexpr (sizeof(T) == 4) {
+#pragma unroll
+        for (int q = 0; q < V / 4; ++q)
+            st16(p + 4 * q, V16{{__float_as_uint(f[4 * q]), __float_as_uint(f[4 * q + 1]),
+                                 __float_as_uint(f[4 * q + 2]), __float_as_uint(f[4 * q + 3])}});
+    } else {
+        uint32_t wd[V / 2];
+#pragma unroll
+        for (int q = 0; q < V / 2; ++q)
+            wd[q] = (__float_as_uint(f[2 * q]) >> 16) | (__float_as_uint(f[2 * q + 1]) & 0xffff0000u);
+        if constexpr (V == 8)
+            st16(p, V16{{wd[0], wd[1], wd[2], wd[3]}});
+        else
+            *reinterpret_cast<uint2*>(p) = make_uint2(wd[0], wd[1]);
+    }
+}
 
 // Row loads of the gather-GEMV; lane column group i of row j, for a wave-uniform slot id j and
 // validity flag ok. A step reads each of its rows once, so the loads are non-temporal.
@@ -205,11 +265,15 @@ __device__ __forceinline__ int64_t split(int64_t n, int p, int P) {
     return (int64_t)((uint32_t)n * (uint32_t)p / (uint32_t)P);
 }
 
-template <typename WT, typename XT, int NI, bool BUF>
+// RN: x is not read; the token's input is RMSNorm(xprev + yprev) (unit gain, eps), computed by
+// every work-group of the token for its lanes' columns, and work-group 0 stores it to xout.
+template <typename WT, typename XT, int NI, bool BUF, bool RN>
 __global__ __launch_bounds__(kThreads) void sffn_rows(
     const XT* __restrict__ x, int64_t d, const int32_t* __restrict__ offsets,
     const int32_t* __restrict__ idx, int64_t nnz, const WT* __restrict__ gate_up_c,
-    const WT* __restrict__ down_c, int64_t L, float* __restrict__ partials, int P) {
+    const WT* __restrict__ down_c, int64_t L, float* __restrict__ partials, int P,
+    const XT* __restrict__ xprev, const float* __restrict__ yprev, float eps,
+    XT* __restrict__ xout) {
     constexpr int V = Elem<WT>::V;
     constexpr int R = RowsPerBatch<NI>::value;
     constexpr int NVAL = 2 * R;
@@ -235,9 +299,55 @@ __global__ __launch_bounds__(kThreads) void sffn_rows(
     // x first: vector loads complete in issue order, so the dot products of the first rows
     // wait only for x and their own rows
     XSlice<WT, XT> xs[NI];
-    const __amdgpu_buffer_rsrc_t rx = make_rsrc(x + (int64_t)b * d, d * (int64_t)sizeof(XT));
+    // RN: r = xprev + yprev for the lane's columns (zeros outside the row), then normalise()
+    float rr[NI][RN ? V : 1];
+    if constexpr (RN) {
+        const __amdgpu_buffer_rsrc_t rxp =
+            make_rsrc(xprev + (int64_t)b * d, d * (int64_t)sizeof(XT));
+        const __amdgpu_buffer_rsrc_t ryp = make_rsrc(yprev + (int64_t)b * d, d * 4);
 #pragma unroll
-    for (int i = 0; i < NI; ++i) xs[i].load(rx, cok[i] ? (int)(col[i] * (int64_t)sizeof(XT)) : kOOB);
+        for (int i = 0; i < NI; ++i) {
+            float xf[V], yf[V];
+            load_elems<XT, V>(rxp, cok[i] ? (int)(col[i] * (int64_t)sizeof(XT)) : kOOB, xf);
+            load_elems<float, V>(ryp, cok[i] ? (int)(col[i] * 4) : kOOB, yf);
+#pragma unroll
+            for (int e = 0; e < V; ++e) rr[i][e] = xf[e] + yf[e];
+        }
+    } else {
+        const __amdgpu_buffer_rsrc_t rx = make_rsrc(x + (int64_t)b * d, d * (int64_t)sizeof(XT));
+#pragma unroll
+        for (int i = 0; i < NI; ++i)
+            xs[i].load(rx, cok[i] ? (int)(col[i] * (int64_t)sizeof(XT)) : kOOB);
+    }
+    // RN: x = r / sqrt(mean(r^2) + eps), rounded to XT. The sum of squares is reduced over the
+    // work-group in a fixed order (lane tree, then the waves in order), the same in every
+    // work-group of the token. Called once, after the first batch's row loads are issued, so
+    // its wait for xprev / yprev and its barrier overlap the row loads.
+    bool pending = RN;
+    auto normalise = [&]() {
+        if constexpr (RN) {
+            float ss = 0.0f;
+#pragma unroll
+            for (int i = 0; i < NI; ++i)
+#pragma unroll
+                for (int e = 0; e < V; ++e) ss = fmaf(rr[i][e], rr[i][e], ss);
+            ss = wave_sum(ss);
+            __shared__ float nred[kWaves];
+            if (lane == 0) nred[w] = ss;
+            __syncthreads();
+            float tot = 0.0f;
+#pragma unroll
+            for (int q = 0; q < kWaves; ++q) tot += nred[q];
+            const float scale = 1.0f / sqrtf(tot / (float)d + eps);
+#pragma unroll
+            for (int i = 0; i < NI; ++i) {
+#pragma unroll
+                for (int e = 0; e < V; ++e) rr[i][e] = round_to<XT>(rr[i][e] * scale);
+                xs[i].set(rr[i]);
+            }
+            pending = false;
+        }
+    };
 
     // Slot ids of batch [rb, rb + nr): a batch that lies inside idx is read with unconditional
     // scalar loads, which the compiler merges into one wide load (separate conditional loads
@@ -283,6 +393,7 @@ __global__ __launch_bounds__(kThreads) void sffn_rows(
         for (int r = 0; r < N; ++r)
 #pragma unroll
             for (int i = 0; i < NI; ++i) ldr.load_dn(okr[r], sl[r], i, dv[r][i]);
+        if (pending) normalise();  // uniform; RN only
         // all N rows, without a branch (a load used only inside a branch is moved into it,
         // behind the other loads); a row with an invalid id gives a value nobody uses
         float vals[NVAL];
@@ -359,6 +470,15 @@ __global__ __launch_bounds__(kThreads) void sffn_rows(
         if (rb >= r1) break;
         nr = (int)((r1 - rb) < R ? (r1 - rb) : R);
         fetch_ids(rb, nr, sl);
+    }
+
+    if constexpr (RN) {
+        if (pending) normalise();  // a work-group without rows
+        if (p == 0) {
+#pragma unroll
+            for (int i = 0; i < NI; ++i)
+                if (cok[i]) store_elems<XT, V>(xout + (int64_t)b * d + col[i], rr[i]);
+        }
     }
 
     const int64_t nch = part_chunks(d);
@@ -472,7 +592,7 @@ template <typename WT, typename XT, bool BUF>
 hipError_t launch_rows_t(const void* x, int64_t B, int64_t d, const int32_t* offsets,
                          const int32_t* idx, int64_t nnz, const void* gu, const void* dc,
                          int64_t L, float* partials, int P, hipStream_t s, hipEvent_t ev0,
-                         hipEvent_t ev1) {
+                         hipEvent_t ev1, const ResNormIn* rn) {
     constexpr int V = Elem<WT>::V;
     const int64_t span = (int64_t)kThreads * V;
     const int ni = (int)((d + span - 1) / span);
@@ -481,10 +601,24 @@ hipError_t launch_rows_t(const void* x, int64_t B, int64_t d, const int32_t* off
     const XT* xx = static_cast<const XT*>(x);
     const WT* g = static_cast<const WT*>(gu);
     const WT* dn = static_cast<const WT*>(dc);
+    // the prologue stores x as float32 or bf16 only
+    constexpr bool kRN = !std::is_same<XT, f16_t>::value;
+    if (rn && !kRN) return hipErrorInvalidValue;
+    const XT* xp = rn ? static_cast<const XT*>(rn->x_prev) : nullptr;
+    const float* yp = rn ? rn->y_prev : nullptr;
+    const float eps = rn ? rn->eps : 0.0f;
+    XT* xo = rn ? static_cast<XT*>(rn->x_out) : nullptr;
 #define SI_ROWS_CASE(N)                                                                        \
     case N:                                                                                    \
-        hipExtLaunchKernelGGL((sffn_rows<WT, XT, N, BUF>), grid, block, 0, s, ev0, ev1, 0, xx, d, \
-                              offsets, idx, nnz, g, dn, L, partials, P);                       \
+        if (rn) {                                                                              \
+            if constexpr (kRN)                                                                 \
+                hipExtLaunchKernelGGL((sffn_rows<WT, XT, N, BUF, kRN>), grid, block, 0, s, ev0, \
+                                      ev1, 0, xx, d, offsets, idx, nnz, g, dn, L, partials, P, \
+                                      xp, yp, eps, xo);                                        \
+        } else                                                                                 \
+            hipExtLaunchKernelGGL((sffn_rows<WT, XT, N, BUF, false>), grid, block, 0, s, ev0,  \
+                                  ev1, 0, xx, d, offsets, idx, nnz, g, dn, L, partials, P, xp, \
+                                  yp, eps, xo);                                                \
         break;
     switch (ni) {
         SI_ROWS_CASE(1)
@@ -528,7 +662,8 @@ int decode_chunks(int64_t B, int64_t nnz, int num_cu) {
 hipError_t launch_decode(const void* x, int xdt, int64_t B, int64_t d, const int32_t* offsets,
                          const int32_t* idx, int64_t nnz, const void* gate_up_c,
                          const void* down_c, int64_t L, int wdt, float* partials, int P,
-                         float* y, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+                         float* y, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1,
+                         const ResNormIn* rn) {
     if (B == 0) return hipSuccess;
     hipError_t e;
     // buffer loads take 32-bit byte offsets: both compacted tensors must stay below 2 GiB
@@ -536,9 +671,9 @@ hipError_t launch_decode(const void* x, int xdt, int64_t B, int64_t d, const int
     const bool buf = L * 2 * d * es < ((int64_t)1 << 31);
 #define SI_DEC(WT, XT)                                                                        \
     (buf ? launch_rows_t<WT, XT, true>(x, B, d, offsets, idx, nnz, gate_up_c, down_c, L,      \
-                                       partials, P, s, ev0, ev1)                              \
+                                       partials, P, s, ev0, ev1, rn)                          \
          : launch_rows_t<WT, XT, false>(x, B, d, offsets, idx, nnz, gate_up_c, down_c, L,     \
-                                        partials, P, s, ev0, ev1))
+                                        partials, P, s, ev0, ev1, rn))
     if (wdt == 1 && xdt == 1)
         e = SI_DEC(bf16_t, bf16_t);
     else if (wdt == 1 && xdt == 0)

@@ -7,6 +7,15 @@
 namespace si {
 
 // ---- k_decode.hip: per-token path ------------------------------------------------------
+// Input of a stacked layer given as the previous layer's pair: x = RMSNorm(x_prev + y_prev),
+// unit gain, computed in the prologue of the per-token kernel and stored to x_out (float32 or
+// bf16, the type of x).
+struct ResNormIn {
+    const void* x_prev;
+    const float* y_prev;
+    float eps;
+    void* x_out;
+};
 // Number of row chunks (work-groups) per token for the per-token path.
 int decode_chunks(int64_t B, int64_t nnz, int num_cu);
 // 0 if the shape is supported, else nonzero.
@@ -20,7 +29,8 @@ hipError_t launch_reduce_partials(const float* partials, int P, int64_t B, int64
 hipError_t launch_decode(const void* x, int xdt, int64_t B, int64_t d, const int32_t* offsets,
                          const int32_t* idx, int64_t nnz, const void* gate_up_c,
                          const void* down_c, int64_t L, int wdt, float* partials, int P,
-                         float* y, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
+                         float* y, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1,
+                         const ResNormIn* rn = nullptr);
 
 // ---- k_union.hip: union (MFMA) path -----------------------------------------------------
 // sizes the union kernels handle (their buffer loads take 32-bit byte offsets)

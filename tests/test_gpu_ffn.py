@@ -5,6 +5,7 @@ weights. The per-token path only reassociates float32 sums, so it is also held t
 1e-4 alarm; the union path rounds h to a bf16 hi+lo pair for its MFMA GEMM.
 """
 import functools
+import math
 
 import numpy as np
 import pytest
@@ -259,6 +260,91 @@ def test_llama3_8b_stack_teacher_forced():
             ref_next = oracle.residual_rmsnorm_bf16(x[t], want[t])
             assert rel_l2(oracle.decode(xn[t]), oracle.decode(ref_next)) <= TOL["bf16"]
         x = xn                                      # the oracle's next layer takes the GPU's x
+
+
+def _resnorm_ref(xp, yp, xdtype):
+    """The oracle's next-layer input: bf16 bits, or the exact float64 value for f32."""
+    if xdtype == "bf16":
+        return oracle.decode(oracle.residual_rmsnorm_bf16(xp, yp))
+    r = np.asarray(xp, np.float64) + np.asarray(yp, np.float64)
+    return r / math.sqrt(np.mean(r * r) + 1e-5)
+
+
+def _check_resnorm(xp, yp, sets, ref, gpu, xdtype, wdtype, flags=0):
+    """si_selective_ffn_resnorm against the oracle (x_out, then y teacher-forced on the GPU's
+    x_out) and against the unfused pair si_residual_rmsnorm + si_selective_ffn."""
+    off, idx = csr_from_sets(sets)
+    xo, y = si.selective_ffn_resnorm(dev_tensor(xp), dev_tensor(yp), dev_tensor(off),
+                                     dev_tensor(idx), gpu.gate_up_c, gpu.down_c, flags=flags)
+    xo_h, y_h = host_array(xo), host_array(y)
+    x_got = oracle.decode(xo_h) if xdtype == "bf16" else xo_h.astype(np.float64)
+    for b in range(len(sets)):
+        assert rel_l2(x_got[b], _resnorm_ref(xp[b], yp[b], xdtype)) <= (
+            5e-3 if xdtype == "bf16" else 1e-6)
+    # the pair of calls it replaces
+    x_pair = host_array(si.residual_rmsnorm(dev_tensor(xp), dev_tensor(yp)))
+    assert np.mean(xo_h == x_pair) > 0.99
+    want = _oracle(xo_h, sets, ref)
+    tol = ALARM_PER_TOKEN if wdtype == "bf16" else TOL["f32"]
+    assert max_rel_l2(y_h, want) <= tol
+    for b in range(len(sets)):
+        if len(sets[b]) == 0:
+            assert not np.any(y_h[b])
+    return xo_h, y_h
+
+
+def test_llama3_8b_stack_resnorm_fused():
+    """Layer 1 of the 8B stack through the fused call, fed by layer 0's GPU output."""
+    name = "llama3_8b_stack"
+    cfg = CONFIGS[name]
+    toks = [3]
+    say(f"8B stack: fused residual RMSNorm into layer 1, token {toks}")
+    x0 = tokens_x(cfg, toks)
+    c, ref0, gpu0 = _layer(name, 0)
+    y0 = _run(x0, _slots(ref0, active_sets(cfg, toks, 0)), gpu0)
+    c, ref1, gpu1 = _layer(name, 1)
+    _check_resnorm(x0, y0.astype(np.float32), _slots(ref1, active_sets(cfg, toks, 1)), ref1,
+                   gpu1, "bf16", "bf16")
+
+
+@pytest.mark.parametrize("B,d,wdtype,xdtype", [(1, 4104, "bf16", "bf16"), (2, 1000, "bf16", "bf16"),
+                                               (3, 264, "f32", "f32"), (1, 8, "bf16", "bf16"),
+                                               (2, 2052, "f32", "f32"), (2, 1000, "f32", "bf16"),
+                                               (4, 512, "bf16", "bf16")])
+def test_selective_ffn_resnorm(B, d, wdtype, xdtype):
+    """Per-token path with the prologue (B = 1; f32 weights at any B; SI_FLAG_PER_TOKEN), a
+    token with an empty set (its x_out is still written), ragged d, and the union path (bf16,
+    B >= 2 without the flag), which runs the two steps as separate kernels."""
+    N, L = 700, 530
+    say(f"resnorm B={B} d={d} w={wdtype} x={xdtype}")
+    rng, draw, ref, gpu = _rand_problem(100 + d + B, N, d, L, wdtype)
+    xp = rng.standard_normal((B, d)).astype(np.float32)
+    if xdtype == "bf16":
+        xp = (xp.view(np.uint32) >> 16).astype(np.uint16)
+    yp = (rng.standard_normal((B, d)) * 0.3).astype(np.float32)
+    ks = [0, 1, 130, 529, 17, 8][:B] if B > 1 else [130]
+    sets = [rng.permutation(L)[:k].astype(np.int32) for k in ks]
+    _check_resnorm(xp, yp, sets, ref, gpu, xdtype, wdtype)
+    if B > 1 and wdtype == "bf16":
+        _check_resnorm(xp, yp, sets, ref, gpu, xdtype, wdtype, flags=si.FLAG_PER_TOKEN)
+
+
+def test_selective_ffn_resnorm_errors():
+    rng, draw, ref, gpu = _rand_problem(7, 300, 64, 200, "bf16")
+    xp = dev_tensor(draw(2, 64, scale=1.0))
+    yp = torch.zeros((2, 64), dtype=torch.float32, device="cuda:0")
+    off, idx = csr_from_sets([np.array([1, 2], np.int32), np.array([3], np.int32)])
+    off, idx = dev_tensor(off), dev_tensor(idx)
+    with pytest.raises(si.SelectInferError) as e:       # x_out aliases x_prev
+        si.selective_ffn_resnorm(xp, yp, off, idx, gpu.gate_up_c, gpu.down_c, x_out=xp)
+    assert e.value.status == 1
+    with pytest.raises(si.SelectInferError) as e:       # negative eps
+        si.selective_ffn_resnorm(xp, yp, off, idx, gpu.gate_up_c, gpu.down_c, eps=-1.0)
+    assert e.value.status == 1
+    xh = xp.view(torch.int16).to(torch.float16)         # half x: not a stack type here
+    with pytest.raises(si.SelectInferError) as e:
+        si.selective_ffn_resnorm(xh, yp, off, idx, gpu.gate_up_c, gpu.down_c)
+    assert e.value.status == 5
 
 
 def test_check_flag_and_errors():
