@@ -8,7 +8,9 @@
 // bound and are tiled for MFMA throughput instead of streamed:
 //  - or_blocks / union_scan: the OR of the token bitmaps per block of 64 tokens, then one
 //    work-group ORs the blocks and turns the union into the ascending list of its slots;
-//  - gemm1_tiled: a work-group computes 256 tokens x 80 union slots, K = d in steps of 64.
+//  - gemm1_tiled: a work-group computes 256 tokens x 80 union slots, K = d in steps of 64,
+//    with 8 waves of 32 tokens each: two waves per SIMD, so one wave's MFMAs run while the
+//    other waits on LDS or a barrier.
 //    The 160 weight rows of its tile are ordered per group of 16 slots as 16 gate rows then
 //    16 up rows, so gate and up of one (token, slot) land in the same lane and register of two
 //    neighbouring MFMA tiles and the SiLU*up*mask epilogue needs no data exchange. Both
@@ -36,11 +38,14 @@ typedef __attribute__((ext_vector_type(4))) short s16x4_t;
 
 constexpr int kBK = 64;          // K step (elements)
 constexpr int kKP = kBK + 8;     // LDS pitch (bf16) of K-contiguous tiles: 144 bytes
-constexpr int kT1M = 256;        // GEMM1 tokens per work-group (4 waves x 64)
+constexpr int kT1M = 256;        // GEMM1 tokens per work-group (8 waves x 32)
+constexpr int kT1W = 8;          // GEMM1 waves per work-group
+constexpr int kT1T = kT1W * 64;  // GEMM1 threads per work-group
 constexpr int kT1S = 80;         // GEMM1 union slots per work-group (5 groups of 16)
 constexpr int kT1N = 2 * kT1S;   // GEMM1 weight rows per work-group
-constexpr int kT2M = 256;        // GEMM2 tokens per work-group (2 waves x 128)
+constexpr int kT2M = 256;        // GEMM2 tokens per work-group (4 waves x 64)
 constexpr int kT2N = 128;        // GEMM2 columns per work-group (2 waves x 64)
+constexpr int kT2T = 512;        // GEMM2 threads per work-group (8 waves, two per SIMD)
 constexpr int kT2P = kT2N + 16;  // LDS pitch (bf16) of the down-row tile
 
 // part[c][w] = OR of bits[b][w] over the 64 tokens b of block c. Work-group (wx, c): 64 words
@@ -116,7 +121,7 @@ __global__ __launch_bounds__(1024) void union_scan(const uint32_t* __restrict__ 
 enum { kUnion = 0, kAct = 1, kScore = 2 };
 
 template <typename ET, int MODE>
-__global__ __launch_bounds__(256) void gemm1_tiled(
+__global__ __launch_bounds__(kT1T) void gemm1_tiled(
     const uint16_t* __restrict__ x, int64_t B, int64_t d, const uint16_t* __restrict__ gu, int64_t L,
     const int32_t* __restrict__ ulist, const int* __restrict__ ucount,
     const uint32_t* __restrict__ bits, int64_t W, uint16_t* __restrict__ Hhi,
@@ -137,40 +142,42 @@ __global__ __launch_bounds__(256) void gemm1_tiled(
     __shared__ __align__(16) uint16_t sA[kT1M][kKP];
     __shared__ __align__(16) uint16_t sB[kT1N][kKP];
 
-    // staging: thread t moves 16-byte chunk t % 8 of rows t / 8 + 32 j
+    // staging: thread t moves 16-byte chunk t % 8 of rows t / 8 + 64 j (weight rows: j < 3 and
+    // row < 160, i.e. the last j only in waves 0-3)
+    constexpr int kAJ = kT1M / 64, kBJ = (kT1N + 63) / 64;
     const int ch = t & 7;
     const int r0 = t >> 3;
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, B * d * 2);
     const __amdgpu_buffer_rsrc_t rg = make_rsrc(gu, L * 2 * d * 2);
-    int aoff[8], boff[5];  // byte offset of the row start, or kOOB
+    int aoff[kAJ], boff[kBJ];  // byte offset of the row start, or kOOB
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        const int64_t tok = m0 + r0 + 32 * j;
+    for (int j = 0; j < kAJ; ++j) {
+        const int64_t tok = m0 + r0 + 64 * j;
         aoff[j] = tok < B ? (int)(tok * d * 2) : kOOB;
     }
 #pragma unroll
-    for (int j = 0; j < 5; ++j) {
-        const int r = r0 + 32 * j;              // weight row of the tile
+    for (int j = 0; j < kBJ; ++j) {
+        const int r = r0 + 64 * j;              // weight row of the tile
         const int64_t u = u0 + 16 * (r / 32) + (r % 16);
         const int plane = (r % 32) / 16;        // 0 gate, 1 up
-        const int32_t slot = u < nU ? (MODE == kUnion ? ulist[u] : (int32_t)u) : -1;
+        const int32_t slot = (r < kT1N && u < nU) ? (MODE == kUnion ? ulist[u] : (int32_t)u) : -1;
         boff[j] = (slot >= 0 && slot < L) ? (int)(((int64_t)slot * 2 + plane) * d * 2) : kOOB;
     }
-    V16 pa[8], pb[5];
+    V16 pa[kAJ], pb[kBJ];
     auto fetch = [&](int64_t k0) {
         const int64_t k = k0 + 8 * ch;
         const bool kin = k < d;  // d % 8 == 0: a chunk is all in or all out
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
+        for (int j = 0; j < kAJ; ++j)
             pa[j] = bload16(rx, (kin && aoff[j] != kOOB) ? aoff[j] + (int)(k * 2) : kOOB);
 #pragma unroll
-        for (int j = 0; j < 5; ++j)
+        for (int j = 0; j < kBJ; ++j)
             pb[j] = bload16(rg, (kin && boff[j] != kOOB) ? boff[j] + (int)(k * 2) : kOOB);
     };
 
-    f32x4_t acc[4][10];
+    f32x4_t acc[2][10];
 #pragma unroll
-    for (int mi = 0; mi < 4; ++mi)
+    for (int mi = 0; mi < 2; ++mi)
 #pragma unroll
         for (int nj = 0; nj < 10; ++nj) acc[mi][nj] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
@@ -178,9 +185,10 @@ __global__ __launch_bounds__(256) void gemm1_tiled(
     for (int64_t k0 = 0; k0 < d; k0 += kBK) {
         __syncthreads();  // the previous tile has been read
 #pragma unroll
-        for (int j = 0; j < 8; ++j) st16(&sA[r0 + 32 * j][8 * ch], pa[j]);
+        for (int j = 0; j < kAJ; ++j) st16(&sA[r0 + 64 * j][8 * ch], pa[j]);
 #pragma unroll
-        for (int j = 0; j < 5; ++j) st16(&sB[r0 + 32 * j][8 * ch], pb[j]);
+        for (int j = 0; j < kBJ; ++j)
+            if (r0 + 64 * j < kT1N) st16(&sB[r0 + 64 * j][8 * ch], pb[j]);
         __syncthreads();
         fetch(k0 + kBK);  // in flight while this tile is used (past the end: reads nothing)
         // keep the prefetch ahead of the MFMAs (the scheduler would otherwise sink the loads
@@ -188,12 +196,12 @@ __global__ __launch_bounds__(256) void gemm1_tiled(
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
-            typename Mfma<ET>::vec8 a[4];
+            typename Mfma<ET>::vec8 a[2];
 #pragma unroll
-            for (int mi = 0; mi < 4; ++mi)
-                a[mi] = Mfma<ET>::vec(ld16(&sA[64 * w + 16 * mi + nn][32 * ks + 8 * g]));
+            for (int mi = 0; mi < 2; ++mi)
+                a[mi] = Mfma<ET>::vec(ld16(&sA[32 * w + 16 * mi + nn][32 * ks + 8 * g]));
             // B fragments one ahead: the next one's LDS read is in flight during this one's
-            // four MFMAs
+            // MFMAs
             typename Mfma<ET>::vec8 bq[2];
             bq[0] = Mfma<ET>::vec(ld16(&sB[nn][32 * ks + 8 * g]));
 #pragma unroll
@@ -202,25 +210,25 @@ __global__ __launch_bounds__(256) void gemm1_tiled(
                     bq[(nj + 1) & 1] = Mfma<ET>::vec(ld16(&sB[16 * (nj + 1) + nn][32 * ks + 8 * g]));
                 const typename Mfma<ET>::vec8 b = bq[nj & 1];
 #pragma unroll
-                for (int mi = 0; mi < 4; ++mi) acc[mi][nj] = Mfma<ET>::mma(a[mi], b, acc[mi][nj]);
+                for (int mi = 0; mi < 2; ++mi) acc[mi][nj] = Mfma<ET>::mma(a[mi], b, acc[mi][nj]);
             }
         }
     }
 
-    // epilogue: register i of lane l of tile (mi, nj) is token 64 w + 16 mi + 4 g + i and
+    // epilogue: register i of lane l of tile (mi, nj) is token 32 w + 16 mi + 4 g + i and
     // weight row 16 nj + nn; tiles 2q and 2q + 1 are gate and up of slots u0 + 16 q + nn
     if (MODE == kScore) {
-        // |a| summed over this lane's 16 tokens, then over the 4 lane groups (64 tokens of the
-        // wave), then over the 4 waves in LDS, each in a fixed order
-        __shared__ float ssum[4][kT1S];
+        // |a| summed over this lane's 8 tokens, then over the 4 lane groups (32 tokens of the
+        // wave), then over the 8 waves in LDS, each in a fixed order
+        __shared__ float ssum[kT1W][kT1S];
 #pragma unroll
         for (int q = 0; q < 5; ++q) {
             float v = 0.0f;
 #pragma unroll
-            for (int mi = 0; mi < 4; ++mi)
+            for (int mi = 0; mi < 2; ++mi)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const int64_t tok = m0 + 64 * w + 16 * mi + 4 * g + i;
+                    const int64_t tok = m0 + 32 * w + 16 * mi + 4 * g + i;
                     if (tok < B) v += fabsf(silu_f32(acc[mi][2 * q][i]) * acc[mi][2 * q + 1][i]);
                 }
             v += __shfl_xor(v, 16, kWave);
@@ -228,8 +236,12 @@ __global__ __launch_bounds__(256) void gemm1_tiled(
             if (g == 0) ssum[w][16 * q + nn] = v;
         }
         __syncthreads();
-        if (t < kT1S && u0 + t < nU)
-            out[(int64_t)tm * Up + u0 + t] = ((ssum[0][t] + ssum[1][t]) + ssum[2][t]) + ssum[3][t];
+        if (t < kT1S && u0 + t < nU) {
+            float a = ssum[0][t];
+#pragma unroll
+            for (int q = 1; q < kT1W; ++q) a += ssum[q][t];
+            out[(int64_t)tm * Up + u0 + t] = a;
+        }
         return;
     }
 #pragma unroll
@@ -237,10 +249,10 @@ __global__ __launch_bounds__(256) void gemm1_tiled(
         const int64_t u = u0 + 16 * q + nn;
         const int32_t slot = u < nU ? (MODE == kUnion ? ulist[u] : (int32_t)u) : -1;
 #pragma unroll
-        for (int mi = 0; mi < 4; ++mi)
+        for (int mi = 0; mi < 2; ++mi)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int64_t tok = m0 + 64 * w + 16 * mi + 4 * g + i;
+                const int64_t tok = m0 + 32 * w + 16 * mi + 4 * g + i;
                 if (tok < B && slot >= 0) {
                     if (MODE == kAct) {
                         out[tok * Up + u] = silu_f32(acc[mi][2 * q][i]) * acc[mi][2 * q + 1][i];
@@ -258,9 +270,10 @@ __global__ __launch_bounds__(256) void gemm1_tiled(
 }
 
 // ---- GEMM2 ---------------------------------------------------------------------------------
-// Grid: (ceil(d / 128), ceil(B / 256), KS), 256 threads. Partials in the chunked layout.
+// Grid: (ceil(d / 128), ceil(B / 256), KS), 512 threads: wave w computes tokens 64 (w / 2) ..
+// and columns 64 (w % 2) .. of the tile. Partials in the chunked layout.
 template <typename ET>
-__global__ __launch_bounds__(256) void gemm2_tiled(
+__global__ __launch_bounds__(kT2T) void gemm2_tiled(
     const uint16_t* __restrict__ Hhi, const uint16_t* __restrict__ Hlo, int64_t Up, int64_t B,
     const uint16_t* __restrict__ dc, int64_t d, int64_t L, const int32_t* __restrict__ ulist,
     const int* __restrict__ ucount, float* __restrict__ part, int KS, int fast) {
@@ -274,7 +287,7 @@ __global__ __launch_bounds__(256) void gemm2_tiled(
     const int t = threadIdx.x;
     const int lane = t & 63;
     const int w = t >> 6;
-    const int wm = w >> 1;
+    const int wm = w >> 1;  // 0..3
     const int wn = w & 1;
     const int nn = lane & 15;
     const int g = lane >> 4;
@@ -282,8 +295,8 @@ __global__ __launch_bounds__(256) void gemm2_tiled(
     __shared__ __align__(16) uint16_t sH[2][kT2M][kKP];
     __shared__ __align__(16) uint16_t sD[kBK][kT2P];
 
-    // staging of H: chunk t % 8 of rows t / 8 + 32 j; of the down rows: 16-byte chunk t % 16
-    // of union positions t / 16 + 16 j
+    // staging of H: chunk t % 8 of rows t / 8 + 64 j; of the down rows: 16-byte chunk t % 16
+    // of union positions t / 16 + 32 j
     const int ch = t & 7;
     const int r0 = t >> 3;
     const int dch = t & 15;
@@ -291,23 +304,24 @@ __global__ __launch_bounds__(256) void gemm2_tiled(
     const __amdgpu_buffer_rsrc_t rh = make_rsrc(Hhi, B * Up * 2);
     const __amdgpu_buffer_rsrc_t rl = make_rsrc(Hlo, B * Up * 2);
     const __amdgpu_buffer_rsrc_t rd = make_rsrc(dc, L * d * 2);
-    int hoff[8];
+    constexpr int kHJ = kT2M / 64, kDJ = kBK / 32;
+    int hoff[kHJ];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        const int64_t tok = m0 + r0 + 32 * j;
+    for (int j = 0; j < kHJ; ++j) {
+        const int64_t tok = m0 + r0 + 64 * j;
         hoff[j] = tok < B ? (int)(tok * Up * 2) : kOOB;
     }
     const int64_t dcol = n0 + 8 * dch;
     const bool dcol_in = dcol < d;  // d % 8 == 0
-    V16 ph[8], pl[8], pd[4];
+    V16 ph[kHJ], pl[kHJ], pd[kDJ];
     // slot ids of the down rows of the next fetch, loaded one K step ahead of their use so
     // the row loads do not wait on them (union positions past the chunk read as -1)
     const __amdgpu_buffer_rsrc_t ru = make_rsrc(ulist, ke * 4);
-    int32_t sl[4];
+    int32_t sl[kDJ];
     auto load_slots = [&](int64_t k0) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int64_t u = k0 + dr0 + 16 * j;
+        for (int j = 0; j < kDJ; ++j) {
+            const int64_t u = k0 + dr0 + 32 * j;
             sl[j] = u < ke ? (int32_t)__builtin_amdgcn_raw_buffer_load_b32(ru, (int)(u * 4), 0, 0)
                            : -1;
         }
@@ -321,7 +335,7 @@ __global__ __launch_bounds__(256) void gemm2_tiled(
         for (int e = 0; e < 4; ++e)
             keep[e] = (2 * e + 1 < nv) ? 0xffffffffu : (2 * e < nv ? 0x0000ffffu : 0u);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
+        for (int j = 0; j < kHJ; ++j) {
             const int off = (nv > 0 && hoff[j] != kOOB) ? hoff[j] + (int)(k * 2) : kOOB;
             ph[j] = bload16(rh, off);
             pl[j] = bload16(rl, fast ? kOOB : off);
@@ -332,16 +346,16 @@ __global__ __launch_bounds__(256) void gemm2_tiled(
             }
         }
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < kDJ; ++j)
             pd[j] = bload16(rd, (sl[j] >= 0 && sl[j] < L && dcol_in)
                                     ? (int)(((int64_t)sl[j] * d + dcol) * 2)
                                     : kOOB);
         load_slots(k0 + kBK);
     };
 
-    f32x4_t acc[8][4];
+    f32x4_t acc[4][4];
 #pragma unroll
-    for (int mi = 0; mi < 8; ++mi)
+    for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
         for (int nj = 0; nj < 4; ++nj) acc[mi][nj] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
@@ -352,12 +366,12 @@ __global__ __launch_bounds__(256) void gemm2_tiled(
     for (int64_t k0 = kb; k0 < ke; k0 += kBK) {
         __syncthreads();
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            st16(&sH[0][r0 + 32 * j][8 * ch], ph[j]);
-            st16(&sH[1][r0 + 32 * j][8 * ch], pl[j]);
+        for (int j = 0; j < kHJ; ++j) {
+            st16(&sH[0][r0 + 64 * j][8 * ch], ph[j]);
+            st16(&sH[1][r0 + 64 * j][8 * ch], pl[j]);
         }
 #pragma unroll
-        for (int j = 0; j < 4; ++j) st16(&sD[dr0 + 16 * j][8 * dch], pd[j]);
+        for (int j = 0; j < kDJ; ++j) st16(&sD[dr0 + 32 * j][8 * dch], pd[j]);
         __syncthreads();
         fetch(k0 + kBK);  // past the end of the chunk: reads nothing
         __builtin_amdgcn_sched_barrier(0);  // the prefetch stays ahead of the MFMAs
@@ -384,12 +398,12 @@ __global__ __launch_bounds__(256) void gemm2_tiled(
             }
             // A fragments (hi, lo) one row-tile ahead of their MFMAs
             typename Mfma<ET>::vec8 ah[2], al[2];
-            ah[0] = Mfma<ET>::vec(ld16(&sH[0][128 * wm + nn][32 * ks2 + 8 * g]));
-            al[0] = Mfma<ET>::vec(ld16(&sH[1][128 * wm + nn][32 * ks2 + 8 * g]));
+            ah[0] = Mfma<ET>::vec(ld16(&sH[0][64 * wm + nn][32 * ks2 + 8 * g]));
+            al[0] = Mfma<ET>::vec(ld16(&sH[1][64 * wm + nn][32 * ks2 + 8 * g]));
 #pragma unroll
-            for (int mi = 0; mi < 8; ++mi) {
-                if (mi + 1 < 8) {
-                    const int row = 128 * wm + 16 * (mi + 1) + nn;
+            for (int mi = 0; mi < 4; ++mi) {
+                if (mi + 1 < 4) {
+                    const int row = 64 * wm + 16 * (mi + 1) + nn;
                     ah[(mi + 1) & 1] = Mfma<ET>::vec(ld16(&sH[0][row][32 * ks2 + 8 * g]));
                     al[(mi + 1) & 1] = Mfma<ET>::vec(ld16(&sH[1][row][32 * ks2 + 8 * g]));
                 }
@@ -405,16 +419,16 @@ __global__ __launch_bounds__(256) void gemm2_tiled(
         }
     }
 
-    // register i of lane l of tile (mi, nj): token 128 wm + 16 mi + 4 g + i, column
+    // register i of lane l of tile (mi, nj): token 64 wm + 16 mi + 4 g + i, column
     // 64 wn + 16 nj + nn; the 16 lanes of a row write 64 contiguous bytes
     const int64_t nch = part_chunks(d);
 #pragma unroll
-    for (int mi = 0; mi < 8; ++mi)
+    for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
         for (int nj = 0; nj < 4; ++nj)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int64_t tok = m0 + 128 * wm + 16 * mi + 4 * g + i;
+                const int64_t tok = m0 + 64 * wm + 16 * mi + 4 * g + i;
                 const int64_t col = n0 + 64 * wn + 16 * nj + nn;
                 if (tok < B && col < d) part[part_off(tok, ks, col, KS, nch)] = acc[mi][nj][i];
             }
@@ -512,12 +526,12 @@ hipError_t launch_union_tiled_t(const void* x, int64_t B, int64_t d, const int32
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int nst8 = (p.nst + 7) / 8 * 8;
-    hipExtLaunchKernelGGL((gemm1_tiled<ET, kUnion>), dim3((unsigned)(nst8 * p.ntm1)), dim3(256), 0, s,
+    hipExtLaunchKernelGGL((gemm1_tiled<ET, kUnion>), dim3((unsigned)(nst8 * p.ntm1)), dim3(kT1T), 0, s,
                           ev0, nullptr, 0, xx, B, d, gu, L, ulist, ucount, bits, p.W, hhi, hlo,
                           p.Up, p.ntm1, nullptr);
     const int fast = (flags & 4) ? 1 : 0;
     hipExtLaunchKernelGGL((gemm2_tiled<ET>), dim3((unsigned)p.ntn2, (unsigned)p.ntm2, (unsigned)p.KS),
-                          dim3(256), 0, s, nullptr, ev1, 0, hhi, hlo, p.Up, B, dc, d, L, ulist,
+                          dim3(kT2T), 0, s, nullptr, ev1, 0, hhi, hlo, p.Up, B, dc, d, L, ulist,
                           ucount, part, p.KS, fast);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -535,11 +549,11 @@ hipError_t launch_activations_mfma_t(const void* x, int64_t T, int64_t d, const 
     const uint16_t* xx = static_cast<const uint16_t*>(x);
     const uint16_t* gu = static_cast<const uint16_t*>(gate_up_c);
     if (score)
-        hipExtLaunchKernelGGL((gemm1_tiled<ET, kScore>), dim3((unsigned)(nst8 * ntm)), dim3(256), 0, s,
+        hipExtLaunchKernelGGL((gemm1_tiled<ET, kScore>), dim3((unsigned)(nst8 * ntm)), dim3(kT1T), 0, s,
                               ev0, ev1, 0, xx, T, d, gu, L, nullptr, nullptr, nullptr, (int64_t)0,
                               nullptr, nullptr, ldo, ntm, out);
     else
-        hipExtLaunchKernelGGL((gemm1_tiled<ET, kAct>), dim3((unsigned)(nst8 * ntm)), dim3(256), 0, s,
+        hipExtLaunchKernelGGL((gemm1_tiled<ET, kAct>), dim3((unsigned)(nst8 * ntm)), dim3(kT1T), 0, s,
                               ev0, ev1, 0, xx, T, d, gu, L, nullptr, nullptr, nullptr, (int64_t)0,
                               nullptr, nullptr, ldo, ntm, out);
     return hipGetLastError();
