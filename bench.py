@@ -637,7 +637,8 @@ def main():
         flops = np.mean([work.launch_flops(i) for i in launches])
         achieved = flops / (kern_ms.mean() * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": achieved, "peak": MFMA_BF16_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": None}
+                "unit": "TFLOP/s", "frac": achieved / MFMA_BF16_PEAK_TFLOPS,
+                "traffic": traffic_record(cfg.name)}
     else:
         byts = np.mean([work.launch_bytes(i) for i in launches])
         achieved = byts / (kern_ms.mean() * 1e-3) / 1e9
