@@ -343,7 +343,9 @@ __global__ __launch_bounds__(256) void union_gemm2(const float* __restrict__ H, 
 
     const __amdgpu_buffer_rsrc_t rd = make_rsrc(dc, L * d * 2);
     const int sr = threadIdx.x >> 3;         // staging: tile row (slot 32 wd + sr)
-    const int sc = (threadIdx.x & 7) * 32;   // staging: first of 32 columns
+    // staging: the 8 lanes of a tile row take 16 contiguous bytes each of one 128-byte line
+    // per load (columns 64 e + 8 (t % 8) .. + 7 in load e), so a load reads whole lines
+    const int sc = (threadIdx.x & 7) * 8;
     // words of down rows in flight in registers ahead of the LDS tile being consumed: deeper
     // for few tokens, where the kernel only streams rows and register room is plentiful
     constexpr int kDepth = MT == 1 ? 8 : (MT == 2 ? 6 : 3);
@@ -376,7 +378,7 @@ __global__ __launch_bounds__(256) void union_gemm2(const float* __restrict__ H, 
         const int64_t slot = wd * 32 + sr;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const int64_t col = c0 + sc + e * 8;
+            const int64_t col = c0 + e * 64 + sc;
             v[e] = bload16(rd, (rok && col < d) ? (int)((slot * d + col) * 2) : kOOB);
         }
         // H of token tok at slots 32 wd + 8 g .. +7 (contiguous, 32-byte aligned)
@@ -456,7 +458,7 @@ __global__ __launch_bounds__(256) void union_gemm2(const float* __restrict__ H, 
         for (int q = 0; q < kDepth; ++q) {
             const int64_t wd = wg + q;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) st16(&tile[buf][sr][sc + e * 8], nxt[q][e]);
+            for (int e = 0; e < 4; ++e) st16(&tile[buf][sr][e * 64 + sc], nxt[q][e]);
             const uint32_t word = word_at(wd);
             AV ahi[MT], alo[MT];
             a_ops(nh[q], ahi, alo);
