@@ -194,7 +194,7 @@ hipError_t launch_activations(const void* x, int xdt, int64_t T, int64_t d, cons
 
 size_t score_workspace(int64_t T, int64_t N, int64_t d, int xdt, int wdt) {
     const int64_t ldo = (N + 63) / 64 * 64;
-    if (mfma_ok(xdt, wdt, T, N, d)) return (size_t)activation_tiles(T) * ldo * 4;  // per tile
+    if (mfma_ok(xdt, wdt, T, N, d)) return (size_t)activation_tiles_max(T) * ldo * 4;  // per tile
     return (size_t)T * ldo * 4;                         // the activations themselves
 }
 
@@ -209,7 +209,7 @@ hipError_t launch_scores(const void* x, int xdt, int64_t T, int64_t d, const voi
         e = launch_activations_mfma(x, T, d, gate_up, N, wdt, buf, ldo, 1, s, ev0, ev1);
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL(add_rows, dim3(blocks(N)), dim3(256), 0, s, buf,
-                           (int64_t)activation_tiles(T), N, ldo, scores);
+                           (int64_t)activation_tiles(T, N), N, ldo, scores);
     } else {
         e = launch_activations(x, xdt, T, d, gate_up, N, wdt, buf, ldo, s);
         if (e != hipSuccess) return e;

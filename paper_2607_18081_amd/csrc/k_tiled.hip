@@ -8,9 +8,10 @@
 // bound and are tiled for MFMA throughput instead of streamed:
 //  - or_blocks / union_scan: the OR of the token bitmaps per block of 64 tokens, then one
 //    work-group ORs the blocks and turns the union into the ascending list of its slots;
-//  - gemm1_tiled: a work-group computes 256 tokens x 80 union slots, K = d in steps of 64,
-//    with 8 waves of 32 tokens each: two waves per SIMD, so one wave's MFMAs run while the
-//    other waits on LDS or a barrier.
+//  - gemm1_tiled: a work-group computes TM tokens x 80 union slots, K = d in steps of 64,
+//    with TM / 32 waves of 32 tokens each. TM = 256 (two waves per SIMD) when that grid fits
+//    in one round of work-groups on the CUs; otherwise TM = 128, whose work-groups (41 KB of
+//    LDS) run two or three to a CU, so the grid's last round is not a partial one.
 //    The 160 weight rows of its tile are ordered per group of 16 slots as 16 gate rows then
 //    16 up rows, so gate and up of one (token, slot) land in the same lane and register of two
 //    neighbouring MFMA tiles and the SiLU*up*mask epilogue needs no data exchange. Both
@@ -38,9 +39,6 @@ typedef __attribute__((ext_vector_type(4))) short s16x4_t;
 
 constexpr int kBK = 64;          // K step (elements)
 constexpr int kKP = kBK + 8;     // LDS pitch (bf16) of K-contiguous tiles: 144 bytes
-constexpr int kT1M = 256;        // GEMM1 tokens per work-group (8 waves x 32)
-constexpr int kT1W = 8;          // GEMM1 waves per work-group
-constexpr int kT1T = kT1W * 64;  // GEMM1 threads per work-group
 constexpr int kT1S = 80;         // GEMM1 union slots per work-group (5 groups of 16)
 constexpr int kT1N = 2 * kT1S;   // GEMM1 weight rows per work-group
 constexpr int kT2M = 256;        // GEMM2 tokens per work-group (4 waves x 64)
@@ -120,8 +118,8 @@ __global__ __launch_bounds__(1024) void union_scan(const uint32_t* __restrict__ 
 //            tile; the host-side reducer adds the rows in order).
 enum { kUnion = 0, kAct = 1, kScore = 2 };
 
-template <typename ET, int MODE>
-__global__ __launch_bounds__(kT1T) void gemm1_tiled(
+template <typename ET, int MODE, int TM>
+__global__ __launch_bounds__(2 * TM) void gemm1_tiled(
     const uint16_t* __restrict__ x, int64_t B, int64_t d, const uint16_t* __restrict__ gu, int64_t L,
     const int32_t* __restrict__ ulist, const int* __restrict__ ucount,
     const uint32_t* __restrict__ bits, int64_t W, uint16_t* __restrict__ Hhi,
@@ -132,6 +130,7 @@ __global__ __launch_bounds__(kT1T) void gemm1_tiled(
     const int nU = MODE == kUnion ? *ucount : (int)L;
     const int64_t u0 = (int64_t)st * kT1S;
     if (u0 >= nU) return;  // uniform
+    constexpr int kT1M = TM, kT1W = TM / 32, kT1T = 2 * TM;
     const int64_t m0 = (int64_t)tm * kT1M;
     const int t = threadIdx.x;
     const int lane = t & 63;
@@ -142,9 +141,10 @@ __global__ __launch_bounds__(kT1T) void gemm1_tiled(
     __shared__ __align__(16) uint16_t sA[kT1M][kKP];
     __shared__ __align__(16) uint16_t sB[kT1N][kKP];
 
-    // staging: thread t moves 16-byte chunk t % 8 of rows t / 8 + 64 j (weight rows: j < 3 and
-    // row < 160, i.e. the last j only in waves 0-3)
-    constexpr int kAJ = kT1M / 64, kBJ = (kT1N + 63) / 64;
+    // staging: thread t moves 16-byte chunk t % 8 of rows t / 8 + kRP j (weight rows below
+    // 160 only)
+    constexpr int kRP = kT1T / 8;  // rows per staging pass
+    constexpr int kAJ = kT1M / kRP, kBJ = (kT1N + kRP - 1) / kRP;
     const int ch = t & 7;
     const int r0 = t >> 3;
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, B * d * 2);
@@ -152,12 +152,12 @@ __global__ __launch_bounds__(kT1T) void gemm1_tiled(
     int aoff[kAJ], boff[kBJ];  // byte offset of the row start, or kOOB
 #pragma unroll
     for (int j = 0; j < kAJ; ++j) {
-        const int64_t tok = m0 + r0 + 64 * j;
+        const int64_t tok = m0 + r0 + kRP * j;
         aoff[j] = tok < B ? (int)(tok * d * 2) : kOOB;
     }
 #pragma unroll
     for (int j = 0; j < kBJ; ++j) {
-        const int r = r0 + 64 * j;              // weight row of the tile
+        const int r = r0 + kRP * j;             // weight row of the tile
         const int64_t u = u0 + 16 * (r / 32) + (r % 16);
         const int plane = (r % 32) / 16;        // 0 gate, 1 up
         const int32_t slot = (r < kT1N && u < nU) ? (MODE == kUnion ? ulist[u] : (int32_t)u) : -1;
@@ -185,10 +185,10 @@ __global__ __launch_bounds__(kT1T) void gemm1_tiled(
     for (int64_t k0 = 0; k0 < d; k0 += kBK) {
         __syncthreads();  // the previous tile has been read
 #pragma unroll
-        for (int j = 0; j < kAJ; ++j) st16(&sA[r0 + 64 * j][8 * ch], pa[j]);
+        for (int j = 0; j < kAJ; ++j) st16(&sA[r0 + kRP * j][8 * ch], pa[j]);
 #pragma unroll
         for (int j = 0; j < kBJ; ++j)
-            if (r0 + 64 * j < kT1N) st16(&sB[r0 + 64 * j][8 * ch], pb[j]);
+            if (r0 + kRP * j < kT1N) st16(&sB[r0 + kRP * j][8 * ch], pb[j]);
         __syncthreads();
         fetch(k0 + kBK);  // in flight while this tile is used (past the end: reads nothing)
         // keep the prefetch ahead of the MFMAs (the scheduler would otherwise sink the loads
@@ -436,7 +436,7 @@ __global__ __launch_bounds__(kT2T) void gemm2_tiled(
 
 struct TPlan {
     int64_t W, Lp, Up;
-    int ntm1, nst, ntm2, ntn2, KS;
+    int tm1, ntm1, nst, ntm2, ntn2, KS;  // tm1: GEMM1 token tile (gemm1_tm)
     int64_t nb;  // blocks of 64 tokens
     size_t off_bits, off_words, off_ulist, off_count, off_hhi, off_hlo, off_part, total;
 };
@@ -448,7 +448,8 @@ TPlan make_tplan(int64_t B, int64_t L, int64_t d, int num_cu) {
     p.W = (L + 31) / 32;
     p.Lp = p.W * 32;
     p.Up = (L + kBK - 1) / kBK * kBK;
-    p.ntm1 = (int)((B + kT1M - 1) / kT1M);
+    p.tm1 = gemm1_tm(B, L);
+    p.ntm1 = (int)((B + p.tm1 - 1) / p.tm1);
     p.nst = (int)((L + kT1S - 1) / kT1S);
     p.ntm2 = (int)((B + kT2M - 1) / kT2M);
     p.ntn2 = (int)((d + kT2N - 1) / kT2N);
@@ -487,7 +488,20 @@ hipError_t launch_bits_to_list(const uint32_t* bits, int64_t W, int32_t* list, i
     return hipGetLastError();
 }
 
-int activation_tiles(int64_t T) { return (int)((T + kT1M - 1) / kT1M); }
+// GEMM1 token tile: 256 when the 256-token grid fits in one round on the CUs, else 128
+int gemm1_tm(int64_t T, int64_t L) {
+    int dev = 0, ncu = 256;
+    if (hipGetDevice(&dev) == hipSuccess)
+        (void)hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
+    const int64_t nst8 = ((L + kT1S - 1) / kT1S + 7) / 8 * 8;
+    return nst8 * ((T + 255) / 256) <= ncu ? 256 : 128;
+}
+
+int activation_tiles(int64_t T, int64_t L) {
+    const int tm = gemm1_tm(T, L);
+    return (int)((T + tm - 1) / tm);
+}
+int activation_tiles_max(int64_t T) { return (int)((T + 127) / 128); }
 
 bool tiled_supported(int64_t B, int64_t L, int64_t d) {
     const int64_t Up = (L + kBK - 1) / kBK * kBK;
@@ -526,9 +540,14 @@ hipError_t launch_union_tiled_t(const void* x, int64_t B, int64_t d, const int32
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int nst8 = (p.nst + 7) / 8 * 8;
-    hipExtLaunchKernelGGL((gemm1_tiled<ET, kUnion>), dim3((unsigned)(nst8 * p.ntm1)), dim3(kT1T), 0, s,
-                          ev0, nullptr, 0, xx, B, d, gu, L, ulist, ucount, bits, p.W, hhi, hlo,
-                          p.Up, p.ntm1, nullptr);
+    if (p.tm1 == 256)
+        hipExtLaunchKernelGGL((gemm1_tiled<ET, kUnion, 256>), dim3((unsigned)(nst8 * p.ntm1)),
+                              dim3(512), 0, s, ev0, nullptr, 0, xx, B, d, gu, L, ulist, ucount,
+                              bits, p.W, hhi, hlo, p.Up, p.ntm1, nullptr);
+    else
+        hipExtLaunchKernelGGL((gemm1_tiled<ET, kUnion, 128>), dim3((unsigned)(nst8 * p.ntm1)),
+                              dim3(256), 0, s, ev0, nullptr, 0, xx, B, d, gu, L, ulist, ucount,
+                              bits, p.W, hhi, hlo, p.Up, p.ntm1, nullptr);
     const int fast = (flags & 4) ? 1 : 0;
     hipExtLaunchKernelGGL((gemm2_tiled<ET>), dim3((unsigned)p.ntn2, (unsigned)p.ntm2, (unsigned)p.KS),
                           dim3(kT2T), 0, s, nullptr, ev1, 0, hhi, hlo, p.Up, B, dc, d, L, ulist,
@@ -543,19 +562,28 @@ hipError_t launch_activations_mfma_t(const void* x, int64_t T, int64_t d, const 
                                      int64_t L, float* out, int64_t ldo, int score, hipStream_t s,
                                      hipEvent_t ev0, hipEvent_t ev1) {
     if (T == 0 || L == 0) return hipSuccess;
-    const int ntm = (int)((T + kT1M - 1) / kT1M);
+    const int tm = gemm1_tm(T, L);
+    const int ntm = (int)((T + tm - 1) / tm);
     const int nst = (int)((L + kT1S - 1) / kT1S);
     const int nst8 = (nst + 7) / 8 * 8;
     const uint16_t* xx = static_cast<const uint16_t*>(x);
     const uint16_t* gu = static_cast<const uint16_t*>(gate_up_c);
-    if (score)
-        hipExtLaunchKernelGGL((gemm1_tiled<ET, kScore>), dim3((unsigned)(nst8 * ntm)), dim3(kT1T), 0, s,
-                              ev0, ev1, 0, xx, T, d, gu, L, nullptr, nullptr, nullptr, (int64_t)0,
-                              nullptr, nullptr, ldo, ntm, out);
-    else
-        hipExtLaunchKernelGGL((gemm1_tiled<ET, kAct>), dim3((unsigned)(nst8 * ntm)), dim3(kT1T), 0, s,
-                              ev0, ev1, 0, xx, T, d, gu, L, nullptr, nullptr, nullptr, (int64_t)0,
-                              nullptr, nullptr, ldo, ntm, out);
+#define SI_ACT_LAUNCH(MODE, TMV)                                                               \
+    hipExtLaunchKernelGGL((gemm1_tiled<ET, MODE, TMV>), dim3((unsigned)(nst8 * ntm)),          \
+                          dim3(2 * TMV), 0, s, ev0, ev1, 0, xx, T, d, gu, L, nullptr, nullptr,  \
+                          nullptr, (int64_t)0, nullptr, nullptr, ldo, ntm, out)
+    if (score) {
+        if (tm == 256)
+            SI_ACT_LAUNCH(kScore, 256);
+        else
+            SI_ACT_LAUNCH(kScore, 128);
+    } else {
+        if (tm == 256)
+            SI_ACT_LAUNCH(kAct, 256);
+        else
+            SI_ACT_LAUNCH(kAct, 128);
+    }
+#undef SI_ACT_LAUNCH
     return hipGetLastError();
 }
 
