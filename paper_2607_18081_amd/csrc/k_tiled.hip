@@ -27,6 +27,8 @@
 // while the previous tile is multiplied out of LDS.
 #include <hip/hip_ext.h>
 
+#include <atomic>
+
 #include "common.h"
 #include "launch.h"
 #include "mfma.h"
@@ -448,7 +450,7 @@ TPlan make_tplan(int64_t B, int64_t L, int64_t d, int num_cu) {
     p.W = (L + 31) / 32;
     p.Lp = p.W * 32;
     p.Up = (L + kBK - 1) / kBK * kBK;
-    p.tm1 = gemm1_tm(B, L);
+    p.tm1 = gemm1_tm(B, L, num_cu);
     p.ntm1 = (int)((B + p.tm1 - 1) / p.tm1);
     p.nst = (int)((L + kT1S - 1) / kT1S);
     p.ntm2 = (int)((B + kT2M - 1) / kT2M);
@@ -489,16 +491,28 @@ hipError_t launch_bits_to_list(const uint32_t* bits, int64_t W, int32_t* list, i
 }
 
 // GEMM1 token tile: 256 when the 256-token grid fits in one round on the CUs, else 128
-int gemm1_tm(int64_t T, int64_t L) {
-    int dev = 0, ncu = 256;
-    if (hipGetDevice(&dev) == hipSuccess)
-        (void)hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
+int gemm1_tm(int64_t T, int64_t L, int num_cu) {
     const int64_t nst8 = ((L + kT1S - 1) / kT1S + 7) / 8 * 8;
-    return nst8 * ((T + 255) / 256) <= ncu ? 256 : 128;
+    return nst8 * ((T + 255) / 256) <= num_cu ? 256 : 128;
+}
+
+// compute units of the current device, looked up once per device
+int current_cu_count() {
+    static std::atomic<int> cache[64] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    int n = cache[dev].load(std::memory_order_relaxed);
+    if (n == 0) {
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            n <= 0)
+            n = 256;
+        cache[dev].store(n, std::memory_order_relaxed);
+    }
+    return n;
 }
 
 int activation_tiles(int64_t T, int64_t L) {
-    const int tm = gemm1_tm(T, L);
+    const int tm = gemm1_tm(T, L, current_cu_count());
     return (int)((T + tm - 1) / tm);
 }
 int activation_tiles_max(int64_t T) { return (int)((T + 127) / 128); }
@@ -562,7 +576,7 @@ hipError_t launch_activations_mfma_t(const void* x, int64_t T, int64_t d, const 
                                      int64_t L, float* out, int64_t ldo, int score, hipStream_t s,
                                      hipEvent_t ev0, hipEvent_t ev1) {
     if (T == 0 || L == 0) return hipSuccess;
-    const int tm = gemm1_tm(T, L);
+    const int tm = gemm1_tm(T, L, current_cu_count());
     const int ntm = (int)((T + tm - 1) / tm);
     const int nst = (int)((L + kT1S - 1) / kT1S);
     const int nst8 = (nst + 7) / 8 * 8;

@@ -66,8 +66,8 @@ hipError_t launch_activations_mfma(const void* x, int64_t T, int64_t d, const vo
 // each), and an upper bound over L for sizing a workspace
 int activation_tiles(int64_t T, int64_t L);
 int activation_tiles_max(int64_t T);
-// GEMM1 token tile (256 or 128) for T tokens over L slots on the current device
-int gemm1_tm(int64_t T, int64_t L);
+// GEMM1 token tile (256 or 128) for T tokens over L slots on num_cu compute units
+int gemm1_tm(int64_t T, int64_t L, int num_cu);
 // ascending list of the set bits of bits[0..W) and their number
 hipError_t launch_bits_to_list(const uint32_t* bits, int64_t W, int32_t* list, int* count,
                                hipStream_t s);
