@@ -152,8 +152,9 @@ size_t si_selective_ffn_workspace(int64_t B, int64_t nnz, int64_t L, int64_t d,
  *     rows, with
  *     each token's h masked to its own set; below 128 tokens the union rows are streamed
  *     once (bandwidth bound), from 128 tokens on the products are LDS-tiled (compute bound).
- * Requirements: d % 8 == 0 for 16-bit data, d % 4 == 0 for f32; d <= 32768 (16-bit) or
- * 16384 (f32); 16-byte aligned x, gate_up_c, down_c, y and ws; B >= 0; nnz >= 0; L >= 1.
+ * Requirements: d % 8 == 0 for 16-bit data, d % 4 == 0 for f32; d <= 16384 (16-bit weights)
+ * or 8192 (f32 weights), else SI_ERR_UNSUPPORTED; 16-byte aligned x, gate_up_c, down_c, y and
+ * ws; B >= 0; nnz >= 0; L >= 1.
  * SI_FLAG_CHECK validates offsets (non-decreasing, within [0, nnz]), slot range and duplicates
  * on the device, synchronises and returns SI_ERR_RANGE / SI_ERR_DUPLICATE before computing.
  */

@@ -97,9 +97,13 @@ def _rand_problem(seed, N, d, L, wdtype):
 
 
 @pytest.mark.parametrize("d,wdtype", [(8, "bf16"), (264, "bf16"), (1000, "bf16"),
-                                      (4104, "bf16"), (5120, "bf16"), (12, "f32"),
-                                      (1000, "f32"), (2052, "f32")])
+                                      (4104, "bf16"), (5120, "bf16"), (12296, "bf16"),
+                                      (16384, "bf16"), (12, "f32"), (1000, "f32"),
+                                      (2052, "f32"), (6148, "f32"), (8192, "f32")])
 def test_per_token_ragged_shapes(d, wdtype):
+    """Each lane owns up to four 16-byte column groups of a row: d = 4104 / 2052 takes two,
+    12296 / 6148 three and four with a ragged last group, 16384 / 8192 the largest d the
+    per-token path supports (four full groups)."""
     N, L = 700, 530
     say(f"per-token ragged d={d} {wdtype}")
     rng, draw, ref, gpu = _rand_problem(d, N, d, L, wdtype)
@@ -345,6 +349,20 @@ def test_selective_ffn_resnorm_errors():
     with pytest.raises(si.SelectInferError) as e:
         si.selective_ffn_resnorm(xh, yp, off, idx, gpu.gate_up_c, gpu.down_c)
     assert e.value.status == 5
+
+
+def test_largest_d_and_refusal():
+    """d past the supported width is refused before anything is enqueued."""
+    say("d limits: 16392 (bf16) and 8196 (f32) are refused")
+    for d, dt in ((16392, torch.bfloat16), (8196, torch.float32)):
+        x = torch.zeros((1, d), dtype=dt, device="cuda:0")
+        gu = torch.zeros((2, 2, d), dtype=dt, device="cuda:0")
+        dn = torch.zeros((2, d), dtype=dt, device="cuda:0")
+        off = torch.tensor([0, 1], dtype=torch.int32, device="cuda:0")
+        idx = torch.tensor([1], dtype=torch.int32, device="cuda:0")
+        with pytest.raises(si.SelectInferError) as e:
+            si.selective_ffn(x, off, idx, gu, dn)
+        assert e.value.status == 5
 
 
 def test_check_flag_and_errors():
