@@ -59,8 +59,9 @@ enum { SI_TOPK_ABS = 0, SI_TOPK_RAW = 1 };
 enum {
     SI_FLAG_CHECK = 1,      /* validate index content on the device, synchronise, report     */
     SI_FLAG_PER_TOKEN = 2,  /* B > 1: use the per-token path even when the union path applies */
-    SI_FLAG_FAST_H = 4      /* union path: feed SiLU(g)*u to the second MFMA GEMM as one bf16
+    SI_FLAG_FAST_H = 4,     /* union path: feed SiLU(g)*u to the second MFMA GEMM as one bf16
                                value instead of a bf16 hi + lo pair (faster, ~1e-3 rel. err) */
+    SI_FLAG_UNION = 8       /* 2 <= B < 5: use the union path where the dtypes allow it */
 };
 
 /* Library version (major * 10000 + minor * 100 + patch). */
@@ -144,10 +145,11 @@ size_t si_selective_ffn_workspace(int64_t B, int64_t nnz, int64_t L, int64_t d,
  *   ws                 workspace of at least si_selective_ffn_workspace(...) bytes
  *
  * Accumulation is float32. An empty active set gives y[b] = 0 exactly. Paths:
- *   - per-token (B == 1, fp32 weights or x, or SI_FLAG_PER_TOKEN): a gather-GEMV streams only
+ *   - per-token (B < 5, fp32 weights or x, or SI_FLAG_PER_TOKEN): a gather-GEMV streams only
  *     the active rows with 16-byte loads and a fused SiLU*up epilogue, then accumulates the
  *     down rows into float32 partial sums that a second kernel adds in a fixed order;
- *   - union (B >= 2, x and weights both bf16 or both half): the union of the B active sets
+ *   - union (B >= 5, or B >= 2 with SI_FLAG_UNION; x and weights both bf16 or both half): the
+ *     union of the B active sets
  *     is built on the device and both projections run as MFMA gather-GEMMs over the union
  *     rows, with
  *     each token's h masked to its own set; below 128 tokens the union rows are streamed

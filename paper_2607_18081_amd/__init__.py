@@ -10,6 +10,7 @@ from .api import (  # noqa: F401
     FLAG_CHECK,
     FLAG_FAST_H,
     FLAG_PER_TOKEN,
+    FLAG_UNION,
     TOPK_ABS,
     TOPK_RAW,
     CompactLayer,

@@ -14,7 +14,7 @@ from ._lib import load
 
 F32, BF16, F16 = 0, 1, 2
 TOPK_ABS, TOPK_RAW = 0, 1
-FLAG_CHECK, FLAG_PER_TOKEN, FLAG_FAST_H = 1, 2, 4
+FLAG_CHECK, FLAG_PER_TOKEN, FLAG_FAST_H, FLAG_UNION = 1, 2, 4, 8
 
 _DT = {torch.float32: F32, torch.bfloat16: BF16, torch.float16: F16}
 

@@ -77,12 +77,17 @@ bool valid_pair(int xdt, int wdt) {
     return valid_dtype(xdt) && valid_dtype(wdt) && (xdt == SI_F32 || wdt == SI_F32 || xdt == wdt);
 }
 
+// Smallest batch that takes the union path by default. Reading the union once costs |U| rows
+// instead of nnz >= |U|, but the union path runs four kernels with a fixed cost of about
+// 11 000 row reads (measured on the 7B shape: a step is about 28.5 us + 3.6 ns per union row,
+// against 8 us + 2.5 ns per active row on the per-token path). With the workloads' overlap
+// the two meet between B = 4 (36.5 us per-token, 43.0 us union) and B = 6 (55.0 / 45.8 us).
+constexpr int64_t kUnionMinB = 5;
+
 bool use_union(int64_t B, int64_t L, int64_t d, si_dtype xdt, si_dtype wdt, int flags) {
-    // Reading the union once costs |U| rows instead of nnz >= |U|, and the dense-over-union
-    // MFMA work stays far below the HBM time of those rows for any overlap (see the design
-    // notes), so B >= 2 always takes it when the dtypes allow bf16 MFMA.
-    return B >= 2 && xdt == wdt && (wdt == SI_BF16 || wdt == SI_F16) &&
-           !(flags & SI_FLAG_PER_TOKEN) && si::union_supported(B, L, d);
+    return B >= 2 && (B >= kUnionMinB || (flags & SI_FLAG_UNION)) && xdt == wdt &&
+           (wdt == SI_BF16 || wdt == SI_F16) && !(flags & SI_FLAG_PER_TOKEN) &&
+           si::union_supported(B, L, d);
 }
 
 // [a, a + na) and [b, b + nb) share a byte

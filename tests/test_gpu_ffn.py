@@ -122,8 +122,9 @@ def test_per_token_ragged_shapes(d, wdtype):
 @pytest.mark.parametrize("B,d,L", [(2, 264, 613), (5, 1000, 613), (17, 264, 613),
                                    (33, 512, 613), (70, 1000, 613), (3, 72, 16500)])
 def test_union_path_ragged(B, d, L):
-    """Row-word GEMM path; L = 16500 gives over 512 bitmap words, where a work-group takes
-    both 16-row tiles of a word, and the smaller ones one tile each."""
+    """Row-word GEMM path (SI_FLAG_UNION below 5 tokens); L = 16500 gives over 512 bitmap
+    words, where a work-group takes both 16-row tiles of a word, and the smaller ones one tile
+    each. Without the flag, 2 and 3 tokens take the per-token path, to the same result."""
     N = L + 287
     say(f"union ragged B={B} d={d} L={L}")
     rng, draw, ref, gpu = _rand_problem(B * 1000 + d, N, d, L, "bf16")
@@ -133,13 +134,15 @@ def test_union_path_ragged(B, d, L):
         sets.append(rng.permutation(L)[:k].astype(np.int32))
     x = draw(B, d, scale=1.0)
     want = _oracle(x, sets, ref)
-    got = _run(x, sets, gpu)
+    got = _run(x, sets, gpu, flags=si.FLAG_UNION)
     for b in range(B):
         if len(sets[b]) == 0:
             assert not np.any(got[b])
     assert max_rel_l2(got, want) <= TOL["bf16"]
-    fast = _run(x, sets, gpu, flags=si.FLAG_FAST_H)
+    fast = _run(x, sets, gpu, flags=si.FLAG_FAST_H | si.FLAG_UNION)
     assert max_rel_l2(fast, want) <= TOL["bf16"]
+    default = _run(x, sets, gpu)
+    assert max_rel_l2(default, want) <= (ALARM_PER_TOKEN if B < 5 else TOL["bf16"])
 
 
 @pytest.mark.parametrize("B,d,L,sparse", [(128, 264, 613, False), (257, 1000, 300, False),

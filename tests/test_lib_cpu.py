@@ -73,6 +73,34 @@ def test_host_side_argument_errors(lib):
                                    None) == 1                             # eps < 0
 
 
+def test_path_choice_by_batch(lib):
+    """The workspace query follows the path the call takes: per-token below 5 tokens (unless
+    SI_FLAG_UNION), the union path from 5 (unless SI_FLAG_PER_TOKEN), per-token for f32."""
+    ws = lambda B, flags, dt=1: lib.si_selective_ffn_workspace(B, 2202 * B, 7706, 4096, dt, dt,
+                                                               flags)
+    PER, UNION = 2, 8
+    for B in (2, 3, 4):
+        assert ws(B, 0) == ws(B, PER)
+        assert ws(B, UNION) != ws(B, PER)
+    for B in (5, 16):
+        assert ws(B, 0) == ws(B, UNION)
+        assert ws(B, 0) != ws(B, PER)
+    assert ws(16, 0, dt=0) == ws(16, PER, dt=0)                          # f32: per-token
+
+
+def test_lib_exports_resnorm_entry(lib):
+    # x_out overlapping x_prev is refused before anything is enqueued
+    buf = ctypes.create_string_buffer(1024)
+    p = ctypes.addressof(buf)
+    p16 = (p + 15) & ~15
+    assert lib.si_selective_ffn_resnorm(p16, p16 + 256, ctypes.c_float(1e-5), p16 + 16, 1, 1, 64,
+                                        None, None, 0, None, None, 4, 1, None, None, 0, 0,
+                                        None) == 1
+    assert lib.si_selective_ffn_resnorm(None, None, ctypes.c_float(1e-5), None, 2, 1, 64, None,
+                                        None, 0, None, None, 4, 2, None, None, 0, 0,
+                                        None) == 5                        # half x
+
+
 def test_product_path_fails_without_library(monkeypatch, tmp_path):
     from paper_2607_18081_amd import _lib
     monkeypatch.setattr(_lib, "_lib", None)
