@@ -319,9 +319,9 @@ def test_llama3_8b_stack_resnorm_fused():
                                                (2, 2052, "f32", "f32"), (2, 1000, "f32", "bf16"),
                                                (4, 512, "bf16", "bf16")])
 def test_selective_ffn_resnorm(B, d, wdtype, xdtype):
-    """Per-token path with the prologue (B = 1; f32 weights at any B; SI_FLAG_PER_TOKEN), a
-    token with an empty set (its x_out is still written), ragged d, and the union path (bf16,
-    B >= 2 without the flag), which runs the two steps as separate kernels."""
+    """Per-token path with the prologue (B < 5; f32 weights at any B; SI_FLAG_PER_TOKEN), a
+    token with an empty set (its x_out is still written), ragged d, and the union path (bf16
+    with SI_FLAG_UNION), which runs the two steps as separate kernels."""
     N, L = 700, 530
     say(f"resnorm B={B} d={d} w={wdtype} x={xdtype}")
     rng, draw, ref, gpu = _rand_problem(100 + d + B, N, d, L, wdtype)
@@ -334,6 +334,7 @@ def test_selective_ffn_resnorm(B, d, wdtype, xdtype):
     _check_resnorm(xp, yp, sets, ref, gpu, xdtype, wdtype)
     if B > 1 and wdtype == "bf16":
         _check_resnorm(xp, yp, sets, ref, gpu, xdtype, wdtype, flags=si.FLAG_PER_TOKEN)
+        _check_resnorm(xp, yp, sets, ref, gpu, xdtype, wdtype, flags=si.FLAG_UNION)
 
 
 def test_selective_ffn_resnorm_errors():
