@@ -17,7 +17,7 @@ What the paper fixes, and what each function follows:
   ranked by activation, descending, and the top alpha kept.  -> ``select_topk``
 * Eq. 2 (Memory Footprint section): saving = N_ffn (1 - r_load) r_layer s.  -> ``memory_saving``
 
-Readings taken where the paper is silent (each is listed in the design notes):
+Readings taken where the paper is silent:
 
 * ranking key: |value| by default (the profiler scores absolute activations, Eq. 1); raw value
   on request. Ties go to the lower index, -0 equals +0, NaN ranks below every number.

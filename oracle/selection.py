@@ -22,7 +22,7 @@ path; it shares no code with the GPU library or its binding.
 * ``selective_layers`` (Table 1): selective loading applies to the FFN layers from the fifth
   to the second-to-last, 0-based [5, n - 2).
 
-Readings taken where the paper is silent (each is listed in the design notes):
+Readings taken where the paper is silent:
 
 * ranking key of the per-token selection: |a| (the profiler scores absolute activations);
   ties go to the lower index, -0 equals +0, NaN ranks below every number (as ``select_topk``);
