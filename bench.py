@@ -55,6 +55,15 @@ def parse_args():
     return ap.parse_args()
 
 
+def _settle():
+    """In the kernel-timing pass only: a marker on the stream before the timed launch. The
+    start time of a dispatch is stamped when the command processor takes up its packet, which
+    otherwise happens while the previous kernel (the step before's reducer) still drains; behind
+    a marker it is taken when that kernel has finished, as rocprofv3 counts it."""
+    import torch
+    torch.cuda.current_stream().record_event()
+
+
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
@@ -158,6 +167,7 @@ class Workload:
         if cfg.layers == 1:
             cp = self.layers[0][step % len(self.layers[0])]
             if timing:
+                _settle()
                 si.set_timing_events(*timing[0])
             si.selective_ffn(self.x[t0:t0 + B], self.off[0][s], self._slots(0, s),
                              cp.gate_up_c, cp.down_c, y=self.y[t0:t0 + B], workspace=self.ws)
@@ -170,6 +180,7 @@ class Workload:
             for lay in range(cfg.layers):
                 cp = self.layers[lay][0]
                 if timing:
+                    _settle()
                     si.set_timing_events(*timing[lay])
                 if lay == 0:
                     si.selective_ffn(xin, self.off[lay][s], self._slots(lay, s), cp.gate_up_c,
@@ -406,6 +417,7 @@ class SelectWork:
         si = self.si
         gu = self.gu[step % len(self.gu)]
         if timing:
+            _settle()
             si.set_timing_events(*timing[0])
         if self.kind == "dynset":
             si.dynamic_set(self.x, gu, self.static, self.alpha, self.n_total, workspace=self.ws,
