@@ -124,8 +124,10 @@ def test_topk_matches_oracle_on_sampling_keys(name):
         assert np.array_equal(got_abs[t], oracle.select_topk(keys[t], cfg.k, "abs"))
 
 
-@pytest.mark.parametrize("L", [1, 7, 1000, 1024, 1025, 5000])
+@pytest.mark.parametrize("L", [1, 7, 1000, 1024, 1025, 5000, 16384, 16385, 40000])
 def test_topk_ties_zeros_nan(L):
+    """Rows held in registers (up to 16384 keys, 1 to 16 per thread) and longer rows, which the
+    kernel reads again in each radix pass."""
     say(f"topk adversarial L={L}")
     rng = np.random.default_rng(L)
     pool = np.array([0.0, -0.0, 1.0, -1.0, 2.5, -2.5, np.inf, -np.inf, np.nan, 0.125,
