@@ -6,10 +6,13 @@
 //    k_tiled.hip instead;
 //  - col_abs_sum / add_rows: Eq. 1 sums |a| over tokens, and partial rows over token tiles,
 //    in ascending order;
-//  - count_slots: how many of the tokens' top-alpha lists hold each slot (integer atomics:
-//    the result does not depend on their order);
-//  - freq_keys, mask_static: the frequency of each slot as a float key (exact below 2^24),
-//    static slots below every frequency;
+//  - count_bits: how many tokens select each slot, from the tokens' top-alpha bitmaps (up to
+//    16384 slots): one work-group per 32-slot word, wave ballots and a fixed-order sum, so the
+//    count is exact and free of atomics; it also writes the counts as the keys of the pick;
+//  - count_slots: the same from the tokens' top-alpha lists (more slots), one integer atomic
+//    per id, so the result does not depend on their order;
+//  - freq_keys: the frequency of each slot as a float key (exact below 2^24), static slots
+//    (set in the bitmap) below every frequency;
 //  - set_bits: a slot list as a bitmap (then listed in ascending order by the union scan);
 //  - merge_file: out += s / tokens for one score file, file by file;
 //  - rank_scores: the position of each neuron in decreasing score (ties to the lower index,
@@ -72,11 +75,6 @@ __global__ __launch_bounds__(256) void add_rows(const float* __restrict__ P, int
     s[n] += v;
 }
 
-__global__ __launch_bounds__(256) void fill_u32(uint32_t* __restrict__ p, int64_t n, uint32_t v) {
-    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (i < n) p[i] = v;
-}
-
 __global__ __launch_bounds__(256) void count_slots(const int32_t* __restrict__ ids, int64_t n,
                                                    int64_t L, int* __restrict__ counts) {
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -85,18 +83,56 @@ __global__ __launch_bounds__(256) void count_slots(const int32_t* __restrict__ i
     if (v >= 0 && v < L) atomicAdd(&counts[v], 1);
 }
 
-__global__ __launch_bounds__(256) void freq_keys(const int* __restrict__ counts, int64_t L,
-                                                 float* __restrict__ keys) {
-    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (i < L) keys[i] = (float)counts[i];
+// Grid W, 256 threads. tb: T token bitmaps of W words each (row stride W). Work-group w sets,
+// for slot i = 32 w + j < L, counts[i] = how many tokens have bit j of word w set, and keys[i]
+// the same count as an unsigned key. Each wave counts a bit over its 64 tokens with a ballot;
+// the four wave counts are added in wave order.
+__global__ __launch_bounds__(256) void count_bits(const uint32_t* __restrict__ tb, int64_t T,
+                                                  int64_t W, int64_t L, int* __restrict__ counts,
+                                                  uint32_t* __restrict__ keys) {
+    __shared__ int part[4][32];
+    const int64_t w = blockIdx.x;
+    const int lane = threadIdx.x & 63;
+    const int wv = threadIdx.x >> 6;
+    int mine = 0;  // lane j < 32: this wave's count of bit j
+    for (int64_t t0 = 0; t0 < T; t0 += 256) {
+        const int64_t t = t0 + threadIdx.x;
+        const uint32_t v = t < T ? tb[t * W + w] : 0u;
+#pragma unroll
+        for (int j = 0; j < 32; ++j) {
+            const int c = __popcll(__ballot((v >> j) & 1u));
+            mine += lane == j ? c : 0;
+        }
+    }
+    if (lane < 32) part[wv][lane] = mine;
+    __syncthreads();
+    if (threadIdx.x < 32) {
+        const int64_t i = w * 32 + threadIdx.x;
+        const int c = part[0][threadIdx.x] + part[1][threadIdx.x] + part[2][threadIdx.x] +
+                      part[3][threadIdx.x];
+        if (i < L) {
+            counts[i] = c;
+            keys[i] = (uint32_t)c;
+        }
+    }
 }
 
-__global__ __launch_bounds__(256) void mask_static(const int32_t* __restrict__ st, int64_t n,
-                                                   int64_t L, float* __restrict__ keys) {
+// keys[i] = counts[i], or -1 for a static slot (bit i of the bitmap set): below every
+// frequency, so the dynamic pick never takes it
+__global__ __launch_bounds__(256) void freq_keys(const int* __restrict__ counts,
+                                                 const uint32_t* __restrict__ static_bits,
+                                                 int64_t L, float* __restrict__ keys) {
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (i >= n) return;
-    const int32_t v = st[i];
-    if (v >= 0 && v < L) keys[v] = -1.0f;
+    if (i < L) keys[i] = ((static_bits[i / 32] >> (i % 32)) & 1u) ? -1.0f : (float)counts[i];
+}
+
+// p[0 .. n) = v and q[0 .. m) = v
+__global__ __launch_bounds__(256) void fill2_u32(uint32_t* __restrict__ p, int64_t n,
+                                                 uint32_t* __restrict__ q, int64_t m,
+                                                 uint32_t v) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i < n) p[i] = v;
+    if (i < m) q[i] = v;
 }
 
 __global__ __launch_bounds__(256) void set_bits(const int32_t* __restrict__ ids, int64_t n,
@@ -226,8 +262,10 @@ DynPlan dyn_plan(int64_t T, int64_t L, int64_t alpha, int64_t n_total) {
     size_t o = 0;
     p.off_act = o;
     o = al(o + (size_t)T * p.lda * 4);
+    // the tokens' top-alpha choices: bitmaps of W words up to 16384 slots, else lists
+    p.token_bits = L <= kTokenBitsMaxL;
     p.off_lists = o;
-    o = al(o + (size_t)T * alpha * 4);
+    o = al(o + (size_t)T * (p.token_bits ? p.W : alpha) * 4);
     p.off_counts = o;
     o = al(o + (size_t)L * 4);
     p.off_keys = o;
@@ -256,36 +294,46 @@ hipError_t launch_dynamic_set(const void* x, int xdt, int64_t T, int64_t d, cons
     uint32_t* bits = reinterpret_cast<uint32_t*>(base + p.off_bits);
     int* cnt = reinterpret_cast<int*>(base + p.off_count);
     hipError_t e;
+    const int64_t kd = n_total - n_static;  // dynamic slots to add to the static ones
     // 1. activations of every loaded slot, per token
-    e = launch_activations(x, xdt, T, d, gate_up_c, L, wdt, act, p.lda, s, ev0, ev1);
-    if (e != hipSuccess) return e;
-    // 2. each token's top alpha by |a|
-    hipLaunchKernelGGL(fill_u32, dim3(blocks(L)), dim3(256), 0, s,
-                       reinterpret_cast<uint32_t*>(counts), L, 0u);
-    if (T > 0 && alpha > 0) {
-        e = launch_topk_strided(act, T, L, p.lda, alpha, 0, lists, s);
-        if (e != hipSuccess) return e;
-        // 3. frequency of each slot over the T lists
-        hipLaunchKernelGGL(count_slots, dim3(blocks(T * alpha)), dim3(256), 0, s, lists,
-                           T * alpha, L, counts);
-    }
-    // 4. the most frequent non-static slots, n_total - n_static of them
-    hipLaunchKernelGGL(freq_keys, dim3(blocks(L)), dim3(256), 0, s, counts, L, keys);
-    if (n_static > 0)
-        hipLaunchKernelGGL(mask_static, dim3(blocks(n_static)), dim3(256), 0, s, static_slots,
-                           n_static, L, keys);
-    const int64_t kd = n_total - n_static;
-    if (kd > 0) {
-        e = launch_topk(keys, 1, L, kd, 1, dyn, s);
+    if (alpha > 0) {
+        e = launch_activations(x, xdt, T, d, gate_up_c, L, wdt, act, p.lda, s, ev0, ev1);
         if (e != hipSuccess) return e;
     }
-    // 5. static u dynamic, ascending
-    hipLaunchKernelGGL(fill_u32, dim3(blocks(p.W)), dim3(256), 0, s, bits, p.W, 0u);
+    if (p.token_bits) {
+        // 2. each token's top alpha by |a| as a bitmap; 3. counts (the keys of the pick) per
+        //    32-slot word; 4. the static slots joined with the dynamic pick among the others,
+        //    ascending
+        uint32_t* tbits = reinterpret_cast<uint32_t*>(lists);
+        const int64_t Tr = alpha > 0 ? T : 0;
+        e = launch_topk_bitmap(act, Tr, L, p.lda, alpha, 0, tbits, p.W, s);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(count_bits, dim3((unsigned)p.W), dim3(256), 0, s, tbits, Tr, p.W, L,
+                           counts, reinterpret_cast<uint32_t*>(keys));
+        // the static slots are not candidates of the pick (mode 2: the keys are counts)
+        return launch_topk_join(keys, L, kd, 2, static_slots, n_static, out, n_total, cnt, s);
+    }
+    // counts and the bitmap start at zero; the bitmap takes the static slots
+    hipLaunchKernelGGL(fill2_u32, dim3(blocks(L > p.W ? L : p.W)), dim3(256), 0, s,
+                       reinterpret_cast<uint32_t*>(counts), L, bits, p.W, 0u);
     if (n_static > 0)
         hipLaunchKernelGGL(set_bits, dim3(blocks(n_static)), dim3(256), 0, s, static_slots,
                            n_static, L, bits);
-    if (kd > 0)
+    // 2. each token's top alpha by |a|; 3. how often each slot is chosen (atomics on the ids)
+    if (T > 0 && alpha > 0) {
+        e = launch_topk_strided(act, T, L, p.lda, alpha, 0, lists, s);
+        if (e != hipSuccess) return e;
+        const int64_t n = T * alpha;
+        hipLaunchKernelGGL(count_slots, dim3(blocks(n)), dim3(256), 0, s, lists, n, L, counts);
+    }
+    hipLaunchKernelGGL(freq_keys, dim3(blocks(L)), dim3(256), 0, s, counts, bits, L, keys);
+    // 4. the most frequent non-static slots, n_total - n_static of them
+    if (kd > 0) {
+        e = launch_topk(keys, 1, L, kd, 1, dyn, s);
+        if (e != hipSuccess) return e;
         hipLaunchKernelGGL(set_bits, dim3(blocks(kd)), dim3(256), 0, s, dyn, kd, L, bits);
+    }
+    // 5. static u dynamic, ascending
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     return launch_bits_to_list(bits, p.W, out, cnt, s);

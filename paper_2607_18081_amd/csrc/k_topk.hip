@@ -12,9 +12,11 @@
 //      its output position, so the output is ascending without a sort.
 // Rows of up to 16384 keys (topk_rows_reg): thread t holds the C contiguous keys t*C .. in
 // registers, read once; each wave counts into its own LDS histogram (16 x 256 bins), the bins
-// are added in wave order and searched with a wave-wide suffix scan; the selection takes two
-// block-wide scans of per-thread counts. Longer rows (topk_rows) re-read the row from memory
-// in each pass.
+// are added in wave order and every wave searches them with a DPP scan (two barriers a pass);
+// the search stops early once the whole bucket of T's prefix is taken (then the lower bytes
+// cannot change the choice), and in that case the selection needs no scan of equal keys.
+// The choice can also be written as a bitmap per row. Longer rows (topk_rows) re-read the row
+// from memory in each pass.
 #include "common.h"
 #include "launch.h"
 
@@ -26,8 +28,10 @@ constexpr int kTopkThreads = 1024;
 constexpr int kTopkWaves = kTopkThreads / kWave;
 
 // Integer-only mapping, so no floating-point mode can change how -0 or NaN are treated.
+// mode 0: |v|, 1: v, 2: the 32 bits as an unsigned integer (counts).
 __device__ __forceinline__ uint32_t order_key(float v, int mode) {
     uint32_t u = __float_as_uint(v);
+    if (mode == 2) return u;
     if (mode == 0) u &= 0x7fffffffu;                 // |v|
     const uint32_t mag = u & 0x7fffffffu;
     if (mag > 0x7f800000u) return 0u;                // NaN: below every number
@@ -118,14 +122,15 @@ __global__ __launch_bounds__(kTopkThreads) void topk_rows(const float* __restric
     }
 }
 
-// Inclusive prefix sum over the lanes of a wave (lane order).
+// Inclusive prefix sum over the 64 lanes of a wave (lane order): DPP row shifts scan each row
+// of 16 lanes, then two row broadcasts carry the totals of rows 0 and 0-1 upward.
 __device__ __forceinline__ int wave_incl_scan(int v) {
-    const int lane = threadIdx.x & 63;
-#pragma unroll
-    for (int m = 1; m < kWave; m <<= 1) {
-        const int o = __shfl_up(v, m, kWave);
-        v += lane >= m ? o : 0;
-    }
+    v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, false);  // row_shr:1
+    v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, false);  // row_shr:2
+    v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, false);  // row_shr:4
+    v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, false);  // row_shr:8
+    v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xa, 0xf, false);  // row_bcast:15 -> rows 1, 3
+    v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xc, 0xf, false);  // row_bcast:31 -> rows 2, 3
     return v;
 }
 
@@ -148,99 +153,265 @@ __device__ __forceinline__ int block_excl_scan(int v, int* wave_tot, int* total)
     return before + incl - v;
 }
 
+// What a register-resident launch writes (exactly one of idx, bmp, ulist is set):
+struct TopkOut {
+    int32_t* idx;  // [B][k] the chosen indices, ascending
+    uint32_t* bmp;  // [B][bW] a bitmap per row: bit j of word w set iff slot 32 w + j is chosen
+    int64_t bW;
+    // one row: the set join_ids[0 .. n_join) (ids outside [0, L) ignored) joined with the k
+    // chosen among the other keys, ascending, at most ucap of them -> ulist, their number ->
+    // *ucount
+    const int32_t* join_ids;
+    int64_t n_join;
+    int32_t* ulist;
+    int64_t ucap;
+    int* ucount;
+};
+
+constexpr int kMaxRegKeys = 16 * kTopkThreads;  // the register-resident kernel's longest row
+
+// vec: the rows are 16-byte aligned, so a thread's C keys are read as float4s.
 template <int C>
 __global__ __launch_bounds__(kTopkThreads) void topk_rows_reg(const float* __restrict__ scores,
                                                              int64_t L, int64_t ld, int64_t k,
-                                                             int mode,
-                                                             int32_t* __restrict__ out) {
+                                                             int mode, int vec, TopkOut o) {
+    static_assert(32 % C == 0, "a thread's keys lie in one bitmap word");
+    constexpr int kStride = 257;  // one histogram per wave, a bank apart
     const int64_t b = blockIdx.x;
-    const float* row = scores + b * ld;
-    int32_t* orow = out + b * k;
     const int t = threadIdx.x;
     const int lane = t & 63;
     const int w = t >> 6;
-    __shared__ int hist[kTopkWaves][256];
+    __shared__ int hist[kTopkWaves * kStride];
     __shared__ int tot[256];
     __shared__ int wave_tot[kTopkWaves];
-    __shared__ uint32_t s_prefix;
-    __shared__ int s_take;
-
-    // keys t*C .. t*C + C - 1; past L: never a candidate (valid = false)
-    uint32_t key[C];
-#pragma unroll
-    for (int j = 0; j < C; ++j) {
-        const int64_t i = (int64_t)t * C + j;
-        key[j] = i < L ? order_key(row[i], mode) : 0u;
-    }
-    const int64_t rest = L - (int64_t)t * C;  // keys of the row from this thread's first on
-    const int nvalid = rest <= 0 ? 0 : (rest < C ? (int)rest : C);
-
-    uint32_t prefix = 0u, pmask = 0u;
-    int take = (int)k;  // how many still to take among the keys matching the prefix
-#pragma unroll 1
-    for (int shift = 24; shift >= 0; shift -= 8) {
-        for (int q = t; q < kTopkWaves * 256; q += kTopkThreads) (&hist[0][0])[q] = 0;
+    __shared__ uint32_t s_or[kTopkWaves], s_and[kTopkWaves];
+    __shared__ uint32_t jbits[kMaxRegKeys / 32];
+    if (o.ulist) {  // the joined set as a bitmap
+        for (int q = t; q < kMaxRegKeys / 32; q += kTopkThreads) jbits[q] = 0u;
         __syncthreads();
+        for (int64_t i = t; i < o.n_join; i += kTopkThreads) {
+            const int32_t v = o.join_ids[i];
+            if (v >= 0 && v < L) atomicOr(&jbits[v >> 5], 1u << (v & 31));
+        }
+        __syncthreads();
+    }
+    const float* row = scores + b * ld;
+    // keys t*C .. t*C + C - 1 (the first nvalid of them lie in the row)
+    uint32_t key[C];
+    const int64_t rest = L - (int64_t)t * C;
+    const int nvalid = rest <= 0 ? 0 : (rest < C ? (int)rest : C);
+    if (C % 4 == 0 && vec && nvalid == C) {
+        const float4* r4 = reinterpret_cast<const float4*>(row + (int64_t)t * C);
+#pragma unroll
+        for (int q = 0; q < C / 4; ++q) {
+            const float4 v = r4[q];
+            key[4 * q] = order_key(v.x, mode);
+            key[4 * q + 1] = order_key(v.y, mode);
+            key[4 * q + 2] = order_key(v.z, mode);
+            key[4 * q + 3] = order_key(v.w, mode);
+        }
+    } else {
 #pragma unroll
         for (int j = 0; j < C; ++j)
-            if (j < nvalid && (key[j] & pmask) == prefix)
-                atomicAdd(&hist[w][(key[j] >> shift) & 255u], 1);
+            key[j] = j < nvalid ? order_key(row[(int64_t)t * C + j], mode) : 0u;
+    }
+    // candidates: the keys in the row, less (join mode) the slots of the joined set
+    uint32_t cand = k > 0 ? (1u << nvalid) - 1u : 0u;
+    const uint32_t jw = (o.ulist && nvalid > 0) ? jbits[(t * C) / 32] >> ((t * C) & 31) : 0u;
+    cand &= ~jw;
+    // bits common to every candidate need no pass: the search starts at the highest bit in
+    // which two candidates differ
+    uint32_t kor = 0u, kand = ~0u;
+#pragma unroll
+    for (int j = 0; j < C; ++j)
+        if ((cand >> j) & 1u) {
+            kor |= key[j];
+            kand &= key[j];
+        }
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) {
+        kor |= (uint32_t)__shfl_xor((int)kor, m, kWave);
+        kand &= (uint32_t)__shfl_xor((int)kand, m, kWave);
+    }
+    if (lane == 0) {
+        s_or[w] = kor;
+        s_and[w] = kand;
+    }
+    for (int q = t; q < kTopkWaves * kStride; q += kTopkThreads) hist[q] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < kTopkWaves; ++q) {
+        kor |= s_or[q];
+        kand &= s_and[q];
+    }
+    const uint32_t diff = kor ^ kand;
+    const int top = diff ? 31 - __clz((int)diff) : -1;  // -1: all candidates equal (or none)
+    // the bits above `top`, decided before the first pass
+    uint32_t pmask = top < 0 ? ~0u : (top >= 31 ? 0u : ~((2u << top) - 1u));
+    uint32_t prefix = kand & pmask;
+    int* my_hist = hist + w * kStride;
+    int take = (int)k;   // how many still to take among the candidates matching the prefix
+    bool done = k == 0;  // every candidate matching the prefix is taken: no further pass
+#pragma unroll 1
+    for (int hi = top; hi >= 0 && !done; hi -= 8) {
+        // this pass decides bits lo .. hi (8 of them, fewer at the bottom)
+        const int lo = hi >= 7 ? hi - 7 : 0;
+        const uint32_t dmask = (1u << (hi - lo + 1)) - 1u;
+        // 1. count the candidates by digit into the wave's histogram; a run of equal digits
+        //    in a thread's keys is added at once (few distinct digits would serialise the
+        //    atomics on one bin)
+        int cur = -1, cnt = 0;
+#pragma unroll
+        for (int j = 0; j < C; ++j) {
+            if (((cand >> j) & 1u) && (key[j] & pmask) == prefix) {
+                const int dg = (int)((key[j] >> lo) & dmask);
+                if (dg != cur) {
+                    if (cnt) atomicAdd(&my_hist[cur], cnt);
+                    cur = dg;
+                    cnt = 0;
+                }
+                ++cnt;
+            }
+        }
+        if (cnt) atomicAdd(&my_hist[cur], cnt);
         __syncthreads();
+        // 2. bins added in wave order; the histograms are cleared for the next pass
         if (t < 256) {
             int c = 0;
 #pragma unroll
-            for (int q = 0; q < kTopkWaves; ++q) c += hist[q][t];
+            for (int q = 0; q < kTopkWaves; ++q) {
+                c += hist[q * kStride + t];
+                hist[q * kStride + t] = 0;
+            }
             tot[t] = c;
         }
         __syncthreads();
-        if (w == 0) {
-            // lane l owns digits 255 - 4l .. 252 - 4l (descending); `above` = keys with a
-            // larger digit
-            int c4[4], sum = 0;
+        // 3. every wave finds the digit of the k-th key itself (the same result in each, so
+        //    no third barrier): lane l owns digits 255 - 4l .. 252 - 4l, `above` counts the
+        //    keys with a larger digit, exactly one digit qualifies. tot is rewritten only after
+        //    the next pass's first barrier, which every wave reaches after reading it.
+        int c4[4], sum = 0;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                c4[e] = tot[255 - 4 * lane - e];
-                sum += c4[e];
-            }
-            int above = wave_incl_scan(sum) - sum;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                if (above < take && above + c4[e] >= take) {  // exactly one digit qualifies
-                    s_prefix = prefix | ((uint32_t)(255 - 4 * lane - e) << shift);
-                    s_take = take - above;
-                }
-                above += c4[e];
-            }
+        for (int e = 0; e < 4; ++e) {
+            c4[e] = tot[255 - 4 * lane - e];
+            sum += c4[e];
         }
-        __syncthreads();
-        prefix = s_prefix;
-        take = s_take;
-        pmask |= 255u << shift;
-    }
-    const uint32_t T = prefix;
-
-    int n_eq = 0;
+        int above = wave_incl_scan(sum) - sum;
+        int found = 0, dsel = 0, tsel = 0, dn = 0;
 #pragma unroll
-    for (int j = 0; j < C; ++j) n_eq += (j < nvalid && key[j] == T) ? 1 : 0;
-    int eq_all;
-    int eq_before = block_excl_scan(n_eq, wave_tot, &eq_all);
+        for (int e = 0; e < 4; ++e) {
+            if (above < take && above + c4[e] >= take) {
+                found = 1;
+                dsel = 255 - 4 * lane - e;
+                tsel = take - above;
+                dn = tsel == c4[e];
+            }
+            above += c4[e];
+        }
+        const unsigned long long fm = __ballot(found);
+        if (fm == 0ull) {  // k above the number of candidates: every candidate is taken
+            done = true;
+            break;
+        }
+        const int src = __ffsll((long long)fm) - 1;
+        prefix |= (uint32_t)__builtin_amdgcn_readlane(dsel, src) << lo;
+        take = __builtin_amdgcn_readlane(tsel, src);
+        done = __builtin_amdgcn_readlane(dn, src) != 0;
+        pmask |= dmask << lo;
+    }
+    // keys compare on the bits decided
+    const uint32_t T = prefix;
+#pragma unroll
+    for (int j = 0; j < C; ++j) key[j] &= pmask;
     bool sel[C];
     int n_sel = 0;
+    if (done) {  // every candidate equal to T is taken
 #pragma unroll
-    for (int j = 0; j < C; ++j) {
-        const bool ok = j < nvalid;
-        const bool eq = ok && key[j] == T;
-        sel[j] = ok && (key[j] > T || (eq && eq_before < take));
-        eq_before += eq ? 1 : 0;
-        n_sel += sel[j] ? 1 : 0;
+        for (int j = 0; j < C; ++j) {
+            sel[j] = ((cand >> j) & 1u) && key[j] >= T;
+            n_sel += sel[j] ? 1 : 0;
+        }
+    } else {  // the first `take` candidates equal to T in index order
+        int n_eq = 0;
+#pragma unroll
+        for (int j = 0; j < C; ++j) n_eq += (((cand >> j) & 1u) && key[j] == T) ? 1 : 0;
+        int eq_all;
+        int eq_before = block_excl_scan(n_eq, wave_tot, &eq_all);
+#pragma unroll
+        for (int j = 0; j < C; ++j) {
+            const bool ok = (cand >> j) & 1u;
+            const bool eq = ok && key[j] == T;
+            sel[j] = ok && (key[j] > T || (eq && eq_before < take));
+            eq_before += eq ? 1 : 0;
+            n_sel += sel[j] ? 1 : 0;
+        }
+    }
+    if (o.bmp) {
+        // the 32 / C threads of one word (consecutive lanes) OR their bits together
+        uint32_t m = 0u;
+#pragma unroll
+        for (int j = 0; j < C; ++j) m |= sel[j] ? (1u << ((t * C + j) & 31)) : 0u;
+#pragma unroll
+        for (int q = 1; q < 32 / C; q <<= 1) m |= (uint32_t)__shfl_xor((int)m, q, kWave);
+        const int64_t wd = ((int64_t)t * C) / 32;
+        if (((t * C) & 31) == 0 && wd < o.bW) o.bmp[b * o.bW + wd] = m;
+        return;
+    }
+    int64_t cap = k;
+    int32_t* orow = o.ulist;
+    if (!o.ulist) {
+        orow = o.idx + b * k;
+    } else {
+        // join the bits of o.join (jw: this thread's C bits, none of them a candidate)
+        n_sel = 0;
+#pragma unroll
+        for (int j = 0; j < C; ++j) {
+            sel[j] = sel[j] || (j < nvalid && ((jw >> j) & 1u));
+            n_sel += sel[j] ? 1 : 0;
+        }
+        cap = o.ucap;
     }
     int sel_all;
     int pos = block_excl_scan(n_sel, wave_tot, &sel_all);
 #pragma unroll
     for (int j = 0; j < C; ++j) {
-        if (sel[j] && pos < k) orow[pos] = (int32_t)((int64_t)t * C + j);
+        if (sel[j] && pos < cap) orow[pos] = (int32_t)((int64_t)t * C + j);
         pos += sel[j] ? 1 : 0;
     }
+    if (o.ulist && t == 0) *o.ucount = sel_all < cap ? sel_all : (int)cap;
+}
+
+}  // namespace
+
+namespace {
+
+// One register-resident launch: C keys per thread (L <= 1024 C), one work-group per row.
+template <int C>
+void launch_reg_c(const float* scores, int64_t B, int64_t L, int64_t ld, int64_t k, int mode,
+                  const TopkOut& o, hipStream_t s) {
+    const bool al = reinterpret_cast<uintptr_t>(scores) % 16 == 0;
+    const int vec = (al && (B <= 1 || ld % 4 == 0)) ? 1 : 0;
+    hipLaunchKernelGGL(topk_rows_reg<C>, dim3((unsigned)B), dim3(kTopkThreads), 0, s, scores, L,
+                       ld, k, mode, vec, o);
+}
+
+// false when a row has more than 16384 keys
+bool launch_reg(const float* scores, int64_t B, int64_t L, int64_t ld, int64_t k, int mode,
+                const TopkOut& o, hipStream_t s) {
+    const int64_t per = (L + kTopkThreads - 1) / kTopkThreads;  // keys per thread
+    if (per <= 1)
+        launch_reg_c<1>(scores, B, L, ld, k, mode, o, s);
+    else if (per <= 2)
+        launch_reg_c<2>(scores, B, L, ld, k, mode, o, s);
+    else if (per <= 4)
+        launch_reg_c<4>(scores, B, L, ld, k, mode, o, s);
+    else if (per <= 8)
+        launch_reg_c<8>(scores, B, L, ld, k, mode, o, s);
+    else if (per <= 16)
+        launch_reg_c<16>(scores, B, L, ld, k, mode, o, s);
+    else
+        return false;
+    return true;
 }
 
 }  // namespace
@@ -248,24 +419,36 @@ __global__ __launch_bounds__(kTopkThreads) void topk_rows_reg(const float* __res
 hipError_t launch_topk_strided(const float* scores, int64_t B, int64_t L, int64_t ld, int64_t k,
                                int mode, int32_t* out, hipStream_t s) {
     if (B == 0 || k == 0) return hipSuccess;
-    const int64_t per = (L + kTopkThreads - 1) / kTopkThreads;  // keys per thread
-#define SI_TOPK_REG(C)                                                                          \
-    hipLaunchKernelGGL(topk_rows_reg<C>, dim3((unsigned)B), dim3(kTopkThreads), 0, s, scores, L, \
-                       ld, k, mode, out)
-    if (per <= 1)
-        SI_TOPK_REG(1);
-    else if (per <= 2)
-        SI_TOPK_REG(2);
-    else if (per <= 4)
-        SI_TOPK_REG(4);
-    else if (per <= 8)
-        SI_TOPK_REG(8);
-    else if (per <= 16)
-        SI_TOPK_REG(16);
-    else
+    TopkOut o{};
+    o.idx = out;
+    if (!launch_reg(scores, B, L, ld, k, mode, o, s))
         hipLaunchKernelGGL(topk_rows, dim3((unsigned)B), dim3(kTopkThreads), 0, s, scores, L, ld,
                            k, mode, out);
-#undef SI_TOPK_REG
+    return hipGetLastError();
+}
+
+hipError_t launch_topk_bitmap(const float* scores, int64_t B, int64_t L, int64_t ld, int64_t k,
+                              int mode, uint32_t* bits, int64_t W, hipStream_t s) {
+    if (B == 0) return hipSuccess;
+    TopkOut o{};
+    o.bmp = bits;
+    o.bW = W;
+    // every word of a row is written by the kernel: W must be exactly the row's word count
+    if (W != (L + 31) / 32 || !launch_reg(scores, B, L, ld, k, mode, o, s))
+        return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+hipError_t launch_topk_join(const float* scores, int64_t L, int64_t k, int mode,
+                            const int32_t* join_ids, int64_t n_join, int32_t* list, int64_t cap,
+                            int* count, hipStream_t s) {
+    TopkOut o{};
+    o.join_ids = join_ids;
+    o.n_join = n_join;
+    o.ulist = list;
+    o.ucap = cap;
+    o.ucount = count;
+    if (!launch_reg(scores, 1, L, L, k, mode, o, s)) return hipErrorInvalidValue;
     return hipGetLastError();
 }
 

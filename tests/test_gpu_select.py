@@ -80,6 +80,26 @@ def test_dynamic_set_exact(wdtype, T):
     assert np.array_equal(host_array(g3), oracle.select_dynamic(A, static, 0, n_total)[0])
     g4, _ = si.dynamic_set(dev_tensor(x), gpu.gate_up_c, dev_tensor(static), alpha, len(static))
     assert np.array_equal(host_array(g4), static)
+    # every slot: the pick takes all non-static slots
+    g5, _ = si.dynamic_set(dev_tensor(x), gpu.gate_up_c, dev_tensor(static), alpha, L)
+    assert np.array_equal(host_array(g5), np.arange(L, dtype=np.int32))
+
+
+@pytest.mark.parametrize("L", [16384, 16385])
+def test_dynamic_set_row_length_paths(L):
+    """Up to 16384 loaded slots the tokens' choices travel as bitmaps and are counted per word;
+    past it, as index lists counted with atomics. Both must give the oracle's result."""
+    N, d, T = L + 300, 64, 40
+    say(f"dynamic set L={L}")
+    rng, x, ref, gpu = _int_problem(L, N, d, L, T, "bf16")
+    static = rng.permutation(L)[:3000].astype(np.int32)   # unsorted on purpose
+    alpha, n_total = 2500, 6000
+    A = oracle.activations(x, ref["gate_up_c"]).astype(np.float32).astype(np.float64)
+    assert _margins_ok(A, alpha)
+    want, want_counts = oracle.dynamic_set(x, ref["gate_up_c"], np.sort(static), alpha, n_total)
+    got, counts = si.dynamic_set(dev_tensor(x), gpu.gate_up_c, dev_tensor(static), alpha, n_total)
+    assert np.array_equal(host_array(counts), want_counts)
+    assert np.array_equal(host_array(got), want)
 
 
 def test_dynamic_set_realistic_shape():
