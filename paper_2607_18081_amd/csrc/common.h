@@ -159,6 +159,18 @@ __host__ __device__ __forceinline__ int64_t part_off(int64_t b, int64_t p, int64
 }
 
 // SiLU(g) = g * sigmoid(g), float32
+// Inclusive prefix sum over the 64 lanes of a wave (lane order): DPP row shifts scan each row
+// of 16 lanes, then two row broadcasts carry the totals of rows 0 and 0-1 upward.
+__device__ __forceinline__ int wave_incl_scan(int v) {
+    v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, false);  // row_shr:1
+    v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, false);  // row_shr:2
+    v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, false);  // row_shr:4
+    v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, false);  // row_shr:8
+    v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xa, 0xf, false);  // row_bcast:15 -> rows 1, 3
+    v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xc, 0xf, false);  // row_bcast:31 -> rows 2, 3
+    return v;
+}
+
 __device__ __forceinline__ float silu_f32(float g) { return __fdividef(g, 1.0f + __expf(-g)); }
 
 // Sum over the 64 lanes of a wave; every lane receives the total.

@@ -71,12 +71,15 @@ __global__ __launch_bounds__(256) void or_blocks(const uint32_t* __restrict__ bi
 
 // One work-group: the union of the nb block bitmaps part[0..nb)[W], its set bits in ascending
 // order -> ulist, their number -> *ucount. Thread t owns a contiguous run of words; an
-// exclusive scan of the runs' counts in LDS gives each run its first position.
+// exclusive scan of the runs' counts (wave scans, then the 16 wave totals) gives each run its
+// first position.
 __global__ __launch_bounds__(1024) void union_scan(const uint32_t* __restrict__ part, int64_t nb,
                                                    int64_t W, int32_t* __restrict__ ulist,
                                                    int* __restrict__ ucount) {
-    __shared__ int cnt[1024];
+    __shared__ int wtot[16];
     const int t = threadIdx.x;
+    const int lane = t & 63;
+    const int wv = t >> 6;
     const int64_t per = (W + 1023) / 1024;
     const int64_t w0 = (int64_t)t * per;
     const int64_t w1 = (w0 + per < W) ? w0 + per : W;
@@ -87,16 +90,16 @@ __global__ __launch_bounds__(1024) void union_scan(const uint32_t* __restrict__ 
     };
     int c = 0;
     for (int64_t w = w0; w < w1; ++w) c += __popc(word(w));
-    cnt[t] = c;
+    const int incl = wave_incl_scan(c);
+    if (lane == kWave - 1) wtot[wv] = incl;
     __syncthreads();
-    // Hillis-Steele inclusive scan over 1024 counts
-    for (int off = 1; off < 1024; off <<= 1) {
-        const int v = t >= off ? cnt[t - off] : 0;
-        __syncthreads();
-        cnt[t] += v;
-        __syncthreads();
+    int before = 0, all = 0;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+        before += q < wv ? wtot[q] : 0;
+        all += wtot[q];
     }
-    int pos = cnt[t] - c;
+    int pos = before + incl - c;
     for (int64_t w = w0; w < w1; ++w) {
         uint32_t u = word(w);
         while (u) {
@@ -105,7 +108,7 @@ __global__ __launch_bounds__(1024) void union_scan(const uint32_t* __restrict__ 
             u &= u - 1u;
         }
     }
-    if (t == 1023) *ucount = cnt[1023];
+    if (t == 0) *ucount = all;
 }
 
 // ---- GEMM1 ---------------------------------------------------------------------------------

@@ -3,20 +3,21 @@
 //
 // Order: key = |s| (ABS) or s (RAW); larger key first; equal keys -> lower index first;
 // -0 == +0; NaN after every number. Each float key is mapped to a uint32 whose unsigned order
-// is that order (NaN -> 0). One 1024-thread work-group per row:
-//   1. radix select, 4 passes of 8 bits from the top: a histogram of the candidates that
-//      match the prefix found so far gives the next byte of the k-th largest key T and how
-//      many keys equal to T must still be taken (take_eq);
+// is that order (NaN -> 0); counts are taken as unsigned integers directly. One 1024-thread
+// work-group per row:
+//   1. radix select over 8-bit digits from the top: a histogram of the candidates that match
+//      the prefix found so far gives the next digit of the k-th largest key T and how many
+//      keys equal to T must still be taken (take_eq);
 //   2. selection in index order: an element is selected iff key > T, or key == T and fewer
 //      than take_eq equal keys precede it; block-wide prefix counts give each selected element
 //      its output position, so the output is ascending without a sort.
 // Rows of up to 16384 keys (topk_rows_reg): thread t holds the C contiguous keys t*C .. in
 // registers, read once; each wave counts into its own LDS histogram (16 x 256 bins), the bins
-// are added in wave order and every wave searches them with a DPP scan (two barriers a pass);
-// the search stops early once the whole bucket of T's prefix is taken (then the lower bytes
-// cannot change the choice), and in that case the selection needs no scan of equal keys.
-// The choice can also be written as a bitmap per row. Longer rows (topk_rows) re-read the row
-// from memory in each pass.
+// are added in wave order and every wave searches them with a DPP scan (two barriers a pass).
+// The digits start below the bits all candidates share, the search stops once the whole
+// bucket of T's prefix is taken (the lower bits cannot change the choice), and then the
+// selection needs no scan of equal keys. The choice can also be written as a bitmap per row,
+// or joined with a given set. Longer rows (topk_rows) re-read the row in each of 4 passes.
 #include "common.h"
 #include "launch.h"
 
@@ -120,18 +121,6 @@ __global__ __launch_bounds__(kTopkThreads) void topk_rows(const float* __restric
         run_eq += eq_total;
         run_sel += sel_total;
     }
-}
-
-// Inclusive prefix sum over the 64 lanes of a wave (lane order): DPP row shifts scan each row
-// of 16 lanes, then two row broadcasts carry the totals of rows 0 and 0-1 upward.
-__device__ __forceinline__ int wave_incl_scan(int v) {
-    v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, false);  // row_shr:1
-    v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, false);  // row_shr:2
-    v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, false);  // row_shr:4
-    v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, false);  // row_shr:8
-    v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xa, 0xf, false);  // row_bcast:15 -> rows 1, 3
-    v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xc, 0xf, false);  // row_bcast:31 -> rows 2, 3
-    return v;
 }
 
 // Exclusive prefix sum of v over the block in thread order; *total = block sum. Two barriers.
