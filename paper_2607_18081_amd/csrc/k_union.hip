@@ -19,9 +19,10 @@
 //    as two 16-row MFMA tiles (slots outside the union load nothing: their loads are out of
 //    range), splits K over 8 waves that meet in LDS in a fixed order, and writes H by slot,
 //    zero for slots outside the union. Within a K block of 128, the lanes of group g feed
-//    elements 32 e + 8 g .. +7 to MFMA e, so one load instruction covers 64 contiguous bytes
-//    of each row; the token operand uses the same K permutation, so the sum is unchanged.
-//    The y = 0 work-groups also publish the union word for GEMM2;
+//    elements 32 e + 8 g .. +7 to MFMA e; the token operand uses the same K permutation, so
+//    the sum is unchanged. The weight rows are loaded in whole 128-byte lines and reach that
+//    layout through the wave's own LDS area. The y = 0 work-groups also publish the union
+//    word for GEMM2;
 //  - GEMM2: a work-group takes 16 x MT tokens, 256 columns and one of KS chunks of bitmap
 //    words, with K = slot: each non-empty word is one K step of 32 slots whose down rows (zero
 //    rows outside the union, again without memory traffic) are staged in LDS, double buffered
@@ -60,8 +61,10 @@ Plan make_plan(int64_t B, int64_t L, int64_t d, int num_cu) {
     Plan p;
     p.W = (L + 31) / 32;
     p.Lp = (p.W * 32 + 63) / 64 * 64;
-    p.MT = B >= 128 ? 8 : (B >= 64 ? 4 : (B >= 32 ? 2 : 1));
-    p.MT1 = B >= 64 ? 4 : (B >= 32 ? 2 : 1);
+    // token tiles of 16 MT (GEMM2) and 16 MT1 (GEMM1) tokens: the smallest that holds the
+    // batch up to 64 tokens, since each tile streams the union rows again
+    p.MT = B >= 128 ? 8 : (B > 32 ? 4 : (B > 16 ? 2 : 1));
+    p.MT1 = B > 32 ? 4 : (B > 16 ? 2 : 1);
     const int64_t ntn = (d + kG2Cols - 1) / kG2Cols;
     const int64_t ntm = (B + 16 * p.MT - 1) / (16 * p.MT);
     int64_t ks = ((int64_t)num_cu + ntn * ntm - 1) / (ntn * ntm);
@@ -194,13 +197,21 @@ __global__ __launch_bounds__(64 * kGemm1Waves) void union_gemm1(
     const __amdgpu_buffer_rsrc_t rg = make_rsrc(gu, L * 2 * d * 2);
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, B * d * 2);
     int64_t slot[2];
-    int goff[2];
 #pragma unroll
     for (int st = 0; st < 2; ++st) {
         const int r = 16 * st + nn;
         slot[st] = r < n ? wd * 32 + nth_set_bit(u, r) : -1;
-        goff[st] = slot[st] >= 0 ? (int)(slot[st] * 4 * d) : kOOB;   // gate row, bytes
     }
+    // loads take whole 128-byte lines: load q of tile st gives lane l row 4 q + l / 16 of the
+    // tile, 16-byte chunk l % 16 of the K block (8 lanes per line, 8 lines per instruction)
+    int goff[2][4];
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int r = 16 * st + 4 * q + (lane >> 4);
+            goff[st][q] = r < n ? (int)((wd * 32 + nth_set_bit(u, r)) * 4 * d) : kOOB;  // gate row
+        }
     int xoff[MT1];
 #pragma unroll
     for (int mt = 0; mt < MT1; ++mt) {
@@ -217,6 +228,9 @@ __global__ __launch_bounds__(64 * kGemm1Waves) void union_gemm1(
         }
     const int ntile = n > 16 ? 2 : 1;
     const int64_t nkb = (d + 127) / 128;
+    constexpr int kStgPitch = 272;                      // bytes per staged row (256 + 16)
+    constexpr int kStgWave = 4 * 16 * kStgPitch;        // gate and up rows of both tiles
+    __shared__ __align__(16) uint8_t stg[kGemm1Waves * kStgWave];
     // The wave's K blocks are kb = w, w + 8, ...: the loads of the next block are in flight
     // while the MFMAs of the current one run (two register sets, the loop unrolled by two).
     // Blocks past the end load nothing (out-of-range offsets) and add zeros. The MFMAs of the
@@ -226,14 +240,14 @@ __global__ __launch_bounds__(64 * kGemm1Waves) void union_gemm1(
         V16 g[2][4], u[2][4], x[MT1][4];
     };
     auto load = [&](int64_t kb, Blk& bk) {
+        const int64_t wpos = kb * 128 + 8 * nn;  // this lane's element of the row (chunk nn)
 #pragma unroll
         for (int st = 0; st < 2; ++st)
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int64_t pos = kb * 128 + e * 32 + g * 8;    // element index in the row
-                const bool in = pos < d && goff[st] != kOOB;
-                bk.g[st][e] = bload16(rg, in ? goff[st] + (int)(pos * 2) : kOOB);
-                bk.u[st][e] = bload16(rg, in ? goff[st] + (int)((d + pos) * 2) : kOOB);
+            for (int q = 0; q < 4; ++q) {
+                const bool in = wpos < d && goff[st][q] != kOOB;
+                bk.g[st][q] = bload16(rg, in ? goff[st][q] + (int)(wpos * 2) : kOOB);
+                bk.u[st][q] = bload16(rg, in ? goff[st][q] + (int)((d + wpos) * 2) : kOOB);
             }
 #pragma unroll
         for (int mt = 0; mt < MT1; ++mt)
@@ -244,22 +258,43 @@ __global__ __launch_bounds__(64 * kGemm1Waves) void union_gemm1(
                                                                         : kOOB);
             }
     };
+    // The lines pass through this wave's own LDS area (no barrier: a wave's LDS accesses
+    // complete in order) and come back in the MFMA layout, lane (nn, g) holding row nn, chunk
+    // 4 e + g for MFMA e. Rows are 272 bytes apart, so the 16 rows one read touches fall in
+    // distinct banks.
+    uint8_t* my_stg = stg + w * kStgWave;
     auto mma = [&](const Blk& bk) {
 #pragma unroll
-        for (int mt = 0; mt < MT1; ++mt)
+        for (int st = 0; st < 2; ++st)
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
+            for (int q = 0; q < 4; ++q) {
+                const int off = (4 * q + (lane >> 4)) * kStgPitch + 16 * nn;
+                st16(my_stg + (2 * st) * 16 * kStgPitch + off, bk.g[st][q]);
+                st16(my_stg + (2 * st + 1) * 16 * kStgPitch + off, bk.u[st][q]);
+            }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            typename Mfma<ET>::vec8 wg_[2], wu_[2];
+#pragma unroll
+            for (int st = 0; st < 2; ++st) {
+                const int off = nn * kStgPitch + 16 * (4 * e + g);
+                wg_[st] = Mfma<ET>::vec(ld16(my_stg + (2 * st) * 16 * kStgPitch + off));
+                wu_[st] = Mfma<ET>::vec(ld16(my_stg + (2 * st + 1) * 16 * kStgPitch + off));
+            }
+#pragma unroll
+            for (int mt = 0; mt < MT1; ++mt) {
                 const typename Mfma<ET>::vec8 a = Mfma<ET>::vec(bk.x[mt][e]);
 #pragma unroll
                 for (int st = 0; st < 2; ++st) {
-                    accg[mt][st] = Mfma<ET>::mma(a, Mfma<ET>::vec(bk.g[st][e]), accg[mt][st]);
-                    accu[mt][st] = Mfma<ET>::mma(a, Mfma<ET>::vec(bk.u[st][e]), accu[mt][st]);
+                    accg[mt][st] = Mfma<ET>::mma(a, wg_[st], accg[mt][st]);
+                    accu[mt][st] = Mfma<ET>::mma(a, wu_[st], accu[mt][st]);
                 }
             }
+        }
     };
     // (the scheduling barriers keep each block's loads ahead of the other block's MFMAs).
-    // With four token tiles two register sets do not fit: one block at a time.
-    if constexpr (MT1 <= 2) {
+    // With two or four token tiles two register sets do not fit: one block at a time.
+    if constexpr (MT1 == 1) {
         Blk b0, b1;
         load(w, b0);
         for (int64_t kb = w; kb < nkb; kb += 2 * kGemm1Waves) {

@@ -120,7 +120,8 @@ def test_per_token_ragged_shapes(d, wdtype):
 
 
 @pytest.mark.parametrize("B,d,L", [(2, 264, 613), (5, 1000, 613), (17, 264, 613),
-                                   (33, 512, 613), (70, 1000, 613), (3, 72, 16500)])
+                                   (32, 264, 613), (33, 512, 613), (64, 264, 613),
+                                   (70, 1000, 613), (3, 72, 16500)])
 def test_union_path_ragged(B, d, L):
     """Row-word GEMM path (SI_FLAG_UNION below 5 tokens); L = 16500 gives over 512 bitmap
     words, where a work-group takes both 16-row tiles of a word, and the smaller ones one tile
