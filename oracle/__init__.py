@@ -19,7 +19,6 @@ from .ffn import (  # noqa: F401
     round_to_bf16_bits,
     select_topk,
     selective_ffn,
-    selective_ffn_batch,
     sigmoid,
     silu,
     stack_step,

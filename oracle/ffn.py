@@ -209,12 +209,6 @@ def selective_ffn(x: np.ndarray, slots, gate_up_c: np.ndarray, down_c: np.ndarra
     return y
 
 
-def selective_ffn_batch(X: np.ndarray, sets, gate_up_c, down_c) -> np.ndarray:
-    """One token at a time: row t of the result is selective_ffn(X[t], sets[t])."""
-    return np.stack([selective_ffn(X[t], sets[t], gate_up_c, down_c) for t in range(len(sets))]) \
-        if len(sets) else np.zeros((0, X.shape[-1]))
-
-
 def dense_swiglu(x: np.ndarray, w_gate: np.ndarray, w_up: np.ndarray, w_down: np.ndarray,
                  neuron_mask=None) -> np.ndarray:
     """Dense FFN with library matmuls and SciPy's logistic; optional 0/1 mask over neurons.
