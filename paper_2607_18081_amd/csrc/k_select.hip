@@ -7,7 +7,7 @@
 //  - col_abs_sum / add_rows: Eq. 1 sums |a| over tokens, and partial rows over token tiles,
 //    in ascending order;
 //  - count_bits: how many tokens select each slot, from the tokens' top-alpha bitmaps (up to
-//    16384 slots): one work-group per 32-slot word, wave ballots and a fixed-order sum, so the
+//    32768 slots): one work-group per 32-slot word, wave ballots and a fixed-order sum, so the
 //    count is exact and free of atomics; it also writes the counts as the keys of the pick;
 //  - count_slots: the same from the tokens' top-alpha lists (more slots), one integer atomic
 //    per id, so the result does not depend on their order;
@@ -262,7 +262,7 @@ DynPlan dyn_plan(int64_t T, int64_t L, int64_t alpha, int64_t n_total) {
     size_t o = 0;
     p.off_act = o;
     o = al(o + (size_t)T * p.lda * 4);
-    // the tokens' top-alpha choices: bitmaps of W words up to 16384 slots, else lists
+    // the tokens' top-alpha choices: bitmaps of W words up to 32768 slots, else lists
     p.token_bits = L <= kTokenBitsMaxL;
     p.off_lists = o;
     o = al(o + (size_t)T * (p.token_bits ? p.W : alpha) * 4);

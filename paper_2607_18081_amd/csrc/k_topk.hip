@@ -11,7 +11,7 @@
 //   2. selection in index order: an element is selected iff key > T, or key == T and fewer
 //      than take_eq equal keys precede it; block-wide prefix counts give each selected element
 //      its output position, so the output is ascending without a sort.
-// Rows of up to 16384 keys (topk_rows_reg): thread t holds the C contiguous keys t*C .. in
+// Rows of up to 32768 keys (topk_rows_reg): thread t holds the C contiguous keys t*C .. in
 // registers, read once; each wave counts into its own LDS histogram (16 x 256 bins), the bins
 // are added in wave order and every wave searches them with a DPP scan (two barriers a pass).
 // The digits start below the bits all candidates share, the search stops once the whole
@@ -157,7 +157,7 @@ struct TopkOut {
     int* ucount;
 };
 
-constexpr int kMaxRegKeys = 16 * kTopkThreads;  // the register-resident kernel's longest row
+constexpr int kMaxRegKeys = 32 * kTopkThreads;  // the register-resident kernel's longest row
 
 // vec: the rows are 16-byte aligned, so a thread's C keys are read as float4s.
 template <int C>
@@ -205,7 +205,8 @@ __global__ __launch_bounds__(kTopkThreads) void topk_rows_reg(const float* __res
             key[j] = j < nvalid ? order_key(row[(int64_t)t * C + j], mode) : 0u;
     }
     // candidates: the keys in the row, less (join mode) the slots of the joined set
-    uint32_t cand = k > 0 ? (1u << nvalid) - 1u : 0u;
+    const uint32_t vmask = nvalid >= 32 ? ~0u : (1u << nvalid) - 1u;  // keys in the row
+    uint32_t cand = k > 0 ? vmask : 0u;
     const uint32_t jw = (o.ulist && nvalid > 0) ? jbits[(t * C) / 32] >> ((t * C) & 31) : 0u;
     cand &= ~jw;
     // bits common to every candidate need no pass: the search starts at the highest bit in
@@ -312,14 +313,10 @@ __global__ __launch_bounds__(kTopkThreads) void topk_rows_reg(const float* __res
     const uint32_t T = prefix;
 #pragma unroll
     for (int j = 0; j < C; ++j) key[j] &= pmask;
-    bool sel[C];
-    int n_sel = 0;
+    uint32_t sel = 0u;  // bit j: key t*C + j is chosen
     if (done) {  // every candidate equal to T is taken
 #pragma unroll
-        for (int j = 0; j < C; ++j) {
-            sel[j] = ((cand >> j) & 1u) && key[j] >= T;
-            n_sel += sel[j] ? 1 : 0;
-        }
+        for (int j = 0; j < C; ++j) sel |= (((cand >> j) & 1u) && key[j] >= T) ? 1u << j : 0u;
     } else {  // the first `take` candidates equal to T in index order
         int n_eq = 0;
 #pragma unroll
@@ -330,16 +327,13 @@ __global__ __launch_bounds__(kTopkThreads) void topk_rows_reg(const float* __res
         for (int j = 0; j < C; ++j) {
             const bool ok = (cand >> j) & 1u;
             const bool eq = ok && key[j] == T;
-            sel[j] = ok && (key[j] > T || (eq && eq_before < take));
+            sel |= (ok && (key[j] > T || (eq && eq_before < take))) ? 1u << j : 0u;
             eq_before += eq ? 1 : 0;
-            n_sel += sel[j] ? 1 : 0;
         }
     }
     if (o.bmp) {
         // the 32 / C threads of one word (consecutive lanes) OR their bits together
-        uint32_t m = 0u;
-#pragma unroll
-        for (int j = 0; j < C; ++j) m |= sel[j] ? (1u << ((t * C + j) & 31)) : 0u;
+        uint32_t m = C == 32 ? sel : sel << ((t * C) & 31);
 #pragma unroll
         for (int q = 1; q < 32 / C; q <<= 1) m |= (uint32_t)__shfl_xor((int)m, q, kWave);
         const int64_t wd = ((int64_t)t * C) / 32;
@@ -351,21 +345,16 @@ __global__ __launch_bounds__(kTopkThreads) void topk_rows_reg(const float* __res
     if (!o.ulist) {
         orow = o.idx + b * k;
     } else {
-        // join the bits of o.join (jw: this thread's C bits, none of them a candidate)
-        n_sel = 0;
-#pragma unroll
-        for (int j = 0; j < C; ++j) {
-            sel[j] = sel[j] || (j < nvalid && ((jw >> j) & 1u));
-            n_sel += sel[j] ? 1 : 0;
-        }
+        sel |= jw & vmask;  // join the bits of o.join (none of them a candidate)
         cap = o.ucap;
     }
     int sel_all;
-    int pos = block_excl_scan(n_sel, wave_tot, &sel_all);
+    int pos = block_excl_scan(__popc(sel), wave_tot, &sel_all);
 #pragma unroll
     for (int j = 0; j < C; ++j) {
-        if (sel[j] && pos < cap) orow[pos] = (int32_t)((int64_t)t * C + j);
-        pos += sel[j] ? 1 : 0;
+        const bool on = (sel >> j) & 1u;
+        if (on && pos < cap) orow[pos] = (int32_t)((int64_t)t * C + j);
+        pos += on ? 1 : 0;
     }
     if (o.ulist && t == 0) *o.ucount = sel_all < cap ? sel_all : (int)cap;
 }
@@ -384,7 +373,7 @@ void launch_reg_c(const float* scores, int64_t B, int64_t L, int64_t ld, int64_t
                        ld, k, mode, vec, o);
 }
 
-// false when a row has more than 16384 keys
+// false when a row has more than 32768 keys
 bool launch_reg(const float* scores, int64_t B, int64_t L, int64_t ld, int64_t k, int mode,
                 const TopkOut& o, hipStream_t s) {
     const int64_t per = (L + kTopkThreads - 1) / kTopkThreads;  // keys per thread
@@ -398,6 +387,8 @@ bool launch_reg(const float* scores, int64_t B, int64_t L, int64_t ld, int64_t k
         launch_reg_c<8>(scores, B, L, ld, k, mode, o, s);
     else if (per <= 16)
         launch_reg_c<16>(scores, B, L, ld, k, mode, o, s);
+    else if (per <= 32)
+        launch_reg_c<32>(scores, B, L, ld, k, mode, o, s);
     else
         return false;
     return true;

@@ -78,10 +78,10 @@ hipError_t launch_topk(const float* scores, int64_t B, int64_t L, int64_t k, int
 hipError_t launch_topk_strided(const float* scores, int64_t B, int64_t L, int64_t ld, int64_t k,
                                int mode, int32_t* out, hipStream_t s);
 // the same choice as a bitmap per row: bits[b * W + w] bit j set iff slot 32 w + j is taken;
-// W = ceil(L / 32) exactly and L <= 16384, else hipErrorInvalidValue; k = 0 clears the rows
+// W = ceil(L / 32) exactly and L <= 32768, else hipErrorInvalidValue; k = 0 clears the rows
 hipError_t launch_topk_bitmap(const float* scores, int64_t B, int64_t L, int64_t ld, int64_t k,
                               int mode, uint32_t* bits, int64_t W, hipStream_t s);
-// one row of L <= 16384 keys: the ids join_ids[0..n_join) (those in [0, L)) joined with the k
+// one row of L <= 32768 keys: the ids join_ids[0..n_join) (those in [0, L)) joined with the k
 // largest keys among the other slots, in ascending order, at most cap of them -> list, their
 // number -> *count. mode 2 takes the keys as unsigned integers.
 hipError_t launch_topk_join(const float* scores, int64_t L, int64_t k, int mode,
@@ -98,7 +98,7 @@ hipError_t launch_scores(const void* x, int xdt, int64_t T, int64_t d, const voi
                          int64_t N, int wdt, float* scores, void* ws, hipStream_t s,
                          hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 // up to this many slots the tokens' top-alpha picks travel as bitmaps (the register top-k)
-constexpr int64_t kTokenBitsMaxL = 16384;
+constexpr int64_t kTokenBitsMaxL = 32768;
 struct DynPlan {
     int64_t lda, W;
     bool token_bits;

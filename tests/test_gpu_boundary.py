@@ -124,9 +124,9 @@ def test_topk_matches_oracle_on_sampling_keys(name):
         assert np.array_equal(got_abs[t], oracle.select_topk(keys[t], cfg.k, "abs"))
 
 
-@pytest.mark.parametrize("L", [1, 7, 1000, 1024, 1025, 5000, 16384, 16385, 40000])
+@pytest.mark.parametrize("L", [1, 7, 1000, 1024, 1025, 5000, 16384, 16385, 32768, 32769, 40000])
 def test_topk_ties_zeros_nan(L):
-    """Rows held in registers (up to 16384 keys, 1 to 16 per thread) and longer rows, which the
+    """Rows held in registers (up to 32768 keys, 1 to 32 per thread) and longer rows, which the
     kernel reads again in each radix pass."""
     say(f"topk adversarial L={L}")
     rng = np.random.default_rng(L)

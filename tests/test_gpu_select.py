@@ -85,9 +85,9 @@ def test_dynamic_set_exact(wdtype, T):
     assert np.array_equal(host_array(g5), np.arange(L, dtype=np.int32))
 
 
-@pytest.mark.parametrize("L", [16384, 16385])
+@pytest.mark.parametrize("L", [16384, 32768, 32769])
 def test_dynamic_set_row_length_paths(L):
-    """Up to 16384 loaded slots the tokens' choices travel as bitmaps and are counted per word;
+    """Up to 32768 loaded slots the tokens' choices travel as bitmaps and are counted per word;
     past it, as index lists counted with atomics. Both must give the oracle's result."""
     N, d, T = L + 300, 64, 40
     say(f"dynamic set L={L}")
