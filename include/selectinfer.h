@@ -309,10 +309,12 @@ int si_build_loaded_set(const int32_t* task_rank, const int32_t* model_rank, int
  *   gate_up_c    [L][2][d], down_c [L][d], slot_to_orig [L], orig_to_slot [N]  DEVICE out, as
  *                        for si_compact_ffn (slots in ascending original id)
  *
- * Host threads gather the rows and the transposed down columns into two pinned staging
- * buffers in turn while their copies to the device run on the stream. SYNCHRONOUS: returns
- * after the copies have finished. SI_ERR_RANGE / SI_ERR_DUPLICATE for bad ids (nothing is
- * moved). Calls are serialised within the process.
+ * Host threads cut each row of W_down to its loaded columns and gather the gate/up rows into
+ * two pinned staging buffers in turn while their copies to the device run on the stream; the
+ * cut rows pass through gate_up_c (overwritten afterwards) and a device transpose writes
+ * down_c. SYNCHRONOUS: returns after the copies have finished. SI_ERR_RANGE /
+ * SI_ERR_DUPLICATE for bad ids (nothing is moved); SI_ERR_UNSUPPORTED when 2 * d * s or
+ * L * s exceeds 64 MiB (one staging buffer). Calls are serialised within the process.
  */
 int si_load_selected(const void* w_gate, const void* w_up, const void* w_down, int64_t N,
                      int64_t d, si_dtype wdt, const int32_t* loaded, int64_t L,

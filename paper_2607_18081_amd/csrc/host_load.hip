@@ -4,22 +4,30 @@
 // compacted, neuron-major device layout. The full layer never sits on the device; the bytes
 // moved are the compacted size of Eq. 2, 3 * d * L * s.
 //
-// Host side: a pool of threads gathers the loaded rows of W_gate and W_up, and the loaded
-// columns of W_down (a blocked transpose), into two pinned staging buffers in turn; each
-// buffer's host-to-device copy runs on the caller's stream while the other is being filled.
+// Host side: a pool of threads gathers, into two pinned staging buffers in turn, first each
+// row of W_down cut down to its loaded columns ([d][L], a streaming pass), then the loaded rows
+// of W_gate and W_up; each buffer's host-to-device copy runs on the caller's stream while the
+// other is being filled. The cut W_down rows land in gate_up_c, not yet filled, and a device
+// transpose writes down_c from there before the gate/up rows overwrite it.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <condition_variable>
+#include <functional>
 #include <cstring>
 #include <mutex>
 #include <thread>
 #include <vector>
 
+#include "launch.h"
 #include "selectinfer.h"
 
 namespace {
 
 constexpr size_t kStage = (size_t)64 << 20;  // bytes per pinned staging buffer
+// bytes filled per copy: small enough that the first fill and the last copy, which do not
+// overlap anything, stay short; large enough for full-rate copies
+constexpr size_t kChunk = (size_t)16 << 20;
 
 struct Staging {
     void* buf[2] = {nullptr, nullptr};
@@ -35,16 +43,72 @@ int workers() {
     return n == 0 ? 4 : (int)std::min(n, 16u);
 }
 
+// Worker threads that live as long as the process: a loading call fills many staging chunks,
+// and starting threads for each would cost about as much as filling a small one.
+class Pool {
+public:
+    explicit Pool(int n) : n_(n) {
+        for (int i = 0; i < n_; ++i) th_.emplace_back([this, i] { loop(i); });
+    }
+    ~Pool() {
+        {
+            std::lock_guard<std::mutex> l(m_);
+            stop_ = true;
+        }
+        cv_.notify_all();
+        for (auto& t : th_) t.join();
+    }
+    int size() const { return n_; }
+    // job(i) on every worker i; returns when all have finished
+    void run(const std::function<void(int)>& job) {
+        std::unique_lock<std::mutex> l(m_);
+        job_ = &job;
+        left_ = n_;
+        ++gen_;
+        cv_.notify_all();
+        done_.wait(l, [this] { return left_ == 0; });
+        job_ = nullptr;
+    }
+
+private:
+    void loop(int i) {
+        int seen = 0;
+        for (;;) {
+            const std::function<void(int)>* job;
+            {
+                std::unique_lock<std::mutex> l(m_);
+                cv_.wait(l, [&] { return stop_ || gen_ != seen; });
+                if (stop_) return;
+                seen = gen_;
+                job = job_;
+            }
+            (*job)(i);
+            std::lock_guard<std::mutex> l(m_);
+            if (--left_ == 0) done_.notify_one();
+        }
+    }
+    int n_;
+    std::vector<std::thread> th_;
+    std::mutex m_;
+    std::condition_variable cv_, done_;
+    const std::function<void(int)>* job_ = nullptr;
+    int gen_ = 0, left_ = 0;
+    bool stop_ = false;
+};
+
+Pool& pool() {
+    static Pool p(workers());
+    return p;
+}
+
 // f(lo, hi) on contiguous pieces of [0, n), one per worker
 template <class F>
 void parallel_for(int64_t n, F f) {
-    int w = workers();
-    if (n < w) w = (int)std::max<int64_t>(n, 1);
-    std::vector<std::thread> th;
-    th.reserve(w);
-    for (int i = 0; i < w; ++i)
-        th.emplace_back([=] { f(n * i / w, n * (i + 1) / w); });
-    for (auto& t : th) t.join();
+    const int w = pool().size();
+    pool().run([&](int i) {
+        const int64_t lo = n * i / w, hi = n * (i + 1) / w;
+        if (lo < hi) f(lo, hi);
+    });
 }
 
 hipError_t ensure_staging() {
@@ -76,20 +140,15 @@ hipError_t ship(int b, void* dst, size_t bytes, hipStream_t s) {
     return e;
 }
 
-// down_c[s][i] = w_down[i][S[s]] for s in [s0, s1), into dst (slot-major, d per slot)
+// dst[i - i0][s] = w_down[i][S[s]] for rows i in [i0, i1): each row cut to its loaded columns
 template <typename T>
-void gather_down(const T* wd, int64_t N, int64_t d, const int32_t* S, int64_t s0, int64_t s1,
-                 T* dst) {
-    constexpr int64_t kRows = 16;  // rows of W_down per block: 16 elements per slot written
-    parallel_for((d + kRows - 1) / kRows, [&](int64_t b0, int64_t b1) {
-        for (int64_t blk = b0; blk < b1; ++blk) {
-            const int64_t i0 = blk * kRows;
-            const int64_t i1 = std::min(d, i0 + kRows);
-            for (int64_t s = s0; s < s1; ++s) {
-                const int64_t n = S[s];
-                T* o = dst + (s - s0) * d;
-                for (int64_t i = i0; i < i1; ++i) o[i] = wd[i * N + n];
-            }
+void cut_rows(const T* wd, int64_t N, const int32_t* S, int64_t L, int64_t i0, int64_t i1,
+              T* dst) {
+    parallel_for(i1 - i0, [&](int64_t a, int64_t z) {
+        for (int64_t r = a; r < z; ++r) {
+            const T* src = wd + (i0 + r) * N;
+            T* o = dst + r * L;
+            for (int64_t s = 0; s < L; ++s) o[s] = src[S[s]];
         }
     });
 }
@@ -138,7 +197,8 @@ int si_load_selected(const void* w_gate, const void* w_up, const void* w_down, i
         return SI_ERR_INVALID;
     const int64_t es = wdt == SI_F32 ? 4 : 2;
     const size_t row = (size_t)(d * es);
-    if (2 * row > kStage) return SI_ERR_UNSUPPORTED;
+    const size_t lrow = (size_t)(L * es);  // bytes of a W_down row cut to the loaded columns
+    if (2 * row > kStage || lrow > kStage) return SI_ERR_UNSUPPORTED;
     // slots in ascending original id; reject ids out of range or repeated
     std::vector<int32_t> S(loaded, loaded + L);
     std::sort(S.begin(), S.end());
@@ -165,10 +225,28 @@ int si_load_selected(const void* w_gate, const void* w_up, const void* w_down, i
         e = hipMemcpyAsync(orig_to_slot, o2s.data(), (size_t)N * 4, hipMemcpyHostToDevice, st);
     if (e != hipSuccess) return fail(e);
 
+    // down_c[s] = column S[s] of W_down: rows cut to the loaded columns, shipped into
+    // gate_up_c ([d][L], d * L * es bytes of its 2 * d * L * es), transposed on the device
+    char* cut = static_cast<char*>(gate_up_c);
+    const int64_t rows_per = (int64_t)(std::max(kChunk, lrow) / lrow);
+    for (int64_t i0 = 0; i0 < d; i0 += rows_per) {
+        const int64_t i1 = std::min(d, i0 + rows_per);
+        if ((e = claim(b)) != hipSuccess) return fail(e);
+        if (es == 2)
+            cut_rows(static_cast<const uint16_t*>(w_down), N, S.data(), L, i0, i1,
+                     static_cast<uint16_t*>(g_st.buf[b]));
+        else
+            cut_rows(static_cast<const uint32_t*>(w_down), N, S.data(), L, i0, i1,
+                     static_cast<uint32_t*>(g_st.buf[b]));
+        if ((e = ship(b, cut + i0 * lrow, (i1 - i0) * lrow, st)) != hipSuccess) return fail(e);
+        b ^= 1;
+    }
+    if ((e = si::launch_transpose_cols(cut, d, L, (int)es, down_c, st)) != hipSuccess)
+        return fail(e);
     // gate_up_c[s] = (W_gate[S[s]], W_up[S[s]])
     const char* wg = static_cast<const char*>(w_gate);
     const char* wu = static_cast<const char*>(w_up);
-    const int64_t cs_gu = (int64_t)(kStage / (2 * row));
+    const int64_t cs_gu = (int64_t)(std::max(kChunk, 2 * row) / (2 * row));
     for (int64_t s0 = 0; s0 < L; s0 += cs_gu) {
         const int64_t s1 = std::min(L, s0 + cs_gu);
         if ((e = claim(b)) != hipSuccess) return fail(e);
@@ -182,22 +260,6 @@ int si_load_selected(const void* w_gate, const void* w_up, const void* w_down, i
         });
         if ((e = ship(b, static_cast<char*>(gate_up_c) + s0 * 2 * row, (s1 - s0) * 2 * row,
                       st)) != hipSuccess)
-            return fail(e);
-        b ^= 1;
-    }
-    // down_c[s] = column S[s] of W_down
-    const int64_t cs_d = (int64_t)(kStage / row);
-    for (int64_t s0 = 0; s0 < L; s0 += cs_d) {
-        const int64_t s1 = std::min(L, s0 + cs_d);
-        if ((e = claim(b)) != hipSuccess) return fail(e);
-        if (es == 2)
-            gather_down(static_cast<const uint16_t*>(w_down), N, d, S.data(), s0, s1,
-                        static_cast<uint16_t*>(g_st.buf[b]));
-        else
-            gather_down(static_cast<const uint32_t*>(w_down), N, d, S.data(), s0, s1,
-                        static_cast<uint32_t*>(g_st.buf[b]));
-        if ((e = ship(b, static_cast<char*>(down_c) + s0 * row, (s1 - s0) * row, st)) !=
-            hipSuccess)
             return fail(e);
         b ^= 1;
     }

@@ -92,7 +92,8 @@ __global__ __launch_bounds__(256) void gather_cols(const T* __restrict__ wd, int
     const int64_t i0 = (int64_t)blockIdx.y * 64;
     const int tx = threadIdx.x & 63;
     const int ty = threadIdx.x >> 6;
-    if (threadIdx.x < 64) ids[tx] = (s0 + tx < L) ? s2o[s0 + tx] : 0;
+    // no s2o: the identity (a transpose of [d][L] into [L][d])
+    if (threadIdx.x < 64) ids[tx] = (s0 + tx < L) ? (s2o ? s2o[s0 + tx] : (int32_t)(s0 + tx)) : 0;
     __syncthreads();
     for (int r = ty; r < 64; r += 4) {
         const int64_t i = i0 + r;
@@ -136,6 +137,20 @@ hipError_t launch_compact_gather(const void* w_gate, const void* w_up, const voi
         hipLaunchKernelGGL(gather_cols<uint32_t>, grid, dim3(256), 0, s,
                            static_cast<const uint32_t*>(w_down), N, d, slot_to_orig, L,
                            static_cast<uint32_t*>(down_c));
+    return hipGetLastError();
+}
+
+hipError_t launch_transpose_cols(const void* src, int64_t d, int64_t L, int esize, void* dst,
+                                 hipStream_t s) {
+    dim3 grid((unsigned)((L + 63) / 64), (unsigned)((d + 63) / 64));
+    if (esize == 2)
+        hipLaunchKernelGGL(gather_cols<uint16_t>, grid, dim3(256), 0, s,
+                           static_cast<const uint16_t*>(src), L, d, (const int32_t*)nullptr, L,
+                           static_cast<uint16_t*>(dst));
+    else
+        hipLaunchKernelGGL(gather_cols<uint32_t>, grid, dim3(256), 0, s,
+                           static_cast<const uint32_t*>(src), L, d, (const int32_t*)nullptr, L,
+                           static_cast<uint32_t*>(dst));
     return hipGetLastError();
 }
 

@@ -121,6 +121,9 @@ hipError_t launch_compact_maps(const int32_t* loaded, int64_t L, int64_t N,
 hipError_t launch_compact_gather(const void* w_gate, const void* w_up, const void* w_down,
                                  int64_t N, int64_t d, int esize, const int32_t* slot_to_orig,
                                  int64_t L, void* gate_up_c, void* down_c, hipStream_t s);
+// dst[s][i] = src[i][s]: a [d][L] matrix of esize-byte elements into [L][d]
+hipError_t launch_transpose_cols(const void* src, int64_t d, int64_t L, int esize, void* dst,
+                                 hipStream_t s);
 
 // ---- k_misc.hip ---------------------------------------------------------------------------
 hipError_t launch_remap(const int32_t* orig_to_slot, int64_t N, const int32_t* ids, int64_t n,

@@ -23,8 +23,11 @@ def _same(layer, ref):
 
 
 @pytest.mark.parametrize("wdtype,N,d,L", [("bf16", 900, 264, 613), ("f32", 300, 100, 1),
-                                          ("f32", 257, 12, 257), ("f16", 500, 72, 333)])
+                                          ("f32", 257, 12, 257), ("f16", 500, 72, 333),
+                                          ("f32", 20001, 1000, 20000)])
 def test_load_selected_ragged(wdtype, N, d, L):
+    """Ragged d and L; the last case needs two staging buffers of W_down rows cut to the loaded
+    columns (20000 * 4 bytes a row, 838 rows a buffer) and three of gate/up rows."""
     say(f"load_selected {wdtype} N={N} d={d} L={L}")
     rng = np.random.default_rng(N + d)
     def draw(*s):
