@@ -1,7 +1,7 @@
-"""si_selective_ffn and si_selective_ffn_resnorm captured in a HIP graph (as the benchmark times
-them): each replay, with other eager work on the stream in between, must give the eager call's
-result bit for bit (every reduction has a fixed order). No entry point on these paths records a
-memset or an allocation, so a replay repeats exactly the eager kernels."""
+"""si_selective_ffn, si_selective_ffn_resnorm and si_dynamic_set captured in a HIP graph (as
+the benchmark times them): each replay, with other eager work on the stream in between, must
+give the eager call's result bit for bit (every reduction has a fixed order). No entry point on
+these paths records a memset or an allocation, so a replay repeats exactly the eager kernels."""
 import numpy as np
 import pytest
 import torch
@@ -97,4 +97,37 @@ def test_graph_replay_resnorm():
         torch.cuda.synchronize()
         assert np.array_equal(host_array(xo), xo_e) and np.array_equal(host_array(y), y_e), rep
         si.selective_ffn(xp, offd, idxd, gpu.gate_up_c, gpu.down_c, workspace=ws)
+        torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("L", [530, 33000])
+def test_graph_replay_dynamic_set(L):
+    """si_dynamic_set in a graph: the bitmap path (up to 32768 slots) and the list path past
+    it. No step records a memset, so each replay repeats the eager result bit for bit."""
+    say(f"graph replay of si_dynamic_set L={L}")
+    T, d = 40, 64
+    rng, ref, gpu, _, _ = _problem(L, L + 170, d, L, 1)
+    xb = (rng.standard_normal((T, d)).astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    x = dev_tensor(xb)
+    static = dev_tensor(rng.permutation(L)[:L // 8].astype(np.int32))
+    alpha, n_total = L // 5, L // 3
+    need = int(si._lib.load().si_dynamic_set_workspace(T, L, alpha, n_total))
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda:0")
+    out_e, cnt_e = si.dynamic_set(x, gpu.gate_up_c, static, alpha, n_total, workspace=ws)
+    out_e, cnt_e = host_array(out_e), host_array(cnt_e)
+    out = torch.empty(n_total, dtype=torch.int32, device="cuda:0")
+    cnt = torch.empty(L, dtype=torch.int32, device="cuda:0")
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        si.dynamic_set(x, gpu.gate_up_c, static, alpha, n_total, workspace=ws, out=out, counts=cnt)
+    x2 = dev_tensor(xb[::-1].copy())
+    for rep in range(3):
+        out.fill_(-7)
+        cnt.fill_(-7)
+        g.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(host_array(out), out_e), rep
+        assert np.array_equal(host_array(cnt), cnt_e), rep
+        si.dynamic_set(x2, gpu.gate_up_c, static, alpha, n_total, workspace=ws)
         torch.cuda.synchronize()
