@@ -149,7 +149,9 @@ __global__ __launch_bounds__(kBmThreads) void token_bitmaps(const int32_t* __res
 }
 
 // GEMM1 + SiLU*up*mask epilogue (see the file comment). Grid: (W, ceil(B/(16*MT1))).
-template <typename ET, int MT1>
+// NT: one token tile, so each weight row is read once: its loads carry the non-temporal
+// policy (with two tiles the second would miss the rows the first brought in)
+template <typename ET, int MT1, bool NT>
 __global__ __launch_bounds__(64 * kGemm1Waves) void union_gemm1(
     const uint16_t* __restrict__ x, int64_t B, int64_t d, const uint16_t* __restrict__ gu,
     int64_t L, const uint32_t* __restrict__ bits, int64_t W, uint32_t* __restrict__ words,
@@ -246,8 +248,10 @@ __global__ __launch_bounds__(64 * kGemm1Waves) void union_gemm1(
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
                 const bool in = wpos < d && goff[st][q] != kOOB;
-                bk.g[st][q] = bload16(rg, in ? goff[st][q] + (int)(wpos * 2) : kOOB);
-                bk.u[st][q] = bload16(rg, in ? goff[st][q] + (int)((d + wpos) * 2) : kOOB);
+                const int og = in ? goff[st][q] + (int)(wpos * 2) : kOOB;
+                const int ou = in ? goff[st][q] + (int)((d + wpos) * 2) : kOOB;
+                bk.g[st][q] = NT ? bload16nt(rg, og) : bload16(rg, og);
+                bk.u[st][q] = NT ? bload16nt(rg, ou) : bload16(rg, ou);
             }
 #pragma unroll
         for (int mt = 0; mt < MT1; ++mt)
@@ -576,13 +580,17 @@ hipError_t launch_union_t(const void* x, int64_t B, int64_t d, const int32_t* of
     hipError_t e = launch_token_bitmaps(offsets, idx, nnz, B, L, p.W, bits, s);
     if (e != hipSuccess) return e;
     const dim3 g1((unsigned)p.W, (unsigned)((B + 16 * p.MT1 - 1) / (16 * p.MT1)));
-#define SI_G1(M)                                                                               \
-    hipExtLaunchKernelGGL((union_gemm1<ET, M>), g1, dim3(64 * kGemm1Waves), 0, s, ev0, nullptr, \
-                          0, xx, B, d, gu, L, bits, p.W, words, H, p.Lp)
-    switch (p.MT1) {
-        case 4: SI_G1(4); break;
-        case 2: SI_G1(2); break;
-        default: SI_G1(1); break;
+#define SI_G1(M, N)                                                                            \
+    hipExtLaunchKernelGGL((union_gemm1<ET, M, N>), g1, dim3(64 * kGemm1Waves), 0, s, ev0,       \
+                          nullptr, 0, xx, B, d, gu, L, bits, p.W, words, H, p.Lp)
+    if (g1.y == 1) {
+        switch (p.MT1) {
+            case 4: SI_G1(4, true); break;
+            case 2: SI_G1(2, true); break;
+            default: SI_G1(1, true); break;
+        }
+    } else {  // more than 64 tokens: tiles of 64
+        SI_G1(4, false);
     }
 #undef SI_G1
     const bool fast = (flags & 4) != 0;
