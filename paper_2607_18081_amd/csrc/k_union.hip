@@ -27,8 +27,8 @@
 //    words, with K = slot: each non-empty word is one K step of 32 slots whose down rows (zero
 //    rows outside the union, again without memory traffic) are staged in LDS, double buffered
 //    with three tiles in flight, and read back transposed into the MFMA B-operand layout with
-//    ds_read_b64_tr_b16. The KS float32 partials are added in a fixed order by the shared
-//    partial reducer.
+//    ds_read_b64_tr_b16 (non-temporal row loads when one token tile reads each row once).
+//    The KS float32 partials are added in a fixed order by the shared partial reducer.
 #include <hip/hip_ext.h>
 
 #include "common.h"
@@ -356,7 +356,8 @@ __global__ __launch_bounds__(64 * kGemm1Waves) void union_gemm1(
 
 // GEMM2 (see the file comment). Grid: (ceil(d/256), ceil(B/(16*MT)), KS); 4 waves.
 // FAST: H enters the MFMA as its bf16 (or half) rounding alone, without the low part.
-template <typename ET, int MT, bool FAST>
+// NT: one token tile, so each down row is read once: non-temporal loads.
+template <typename ET, int MT, bool FAST, bool NT>
 __global__ __launch_bounds__(256) void union_gemm2(const float* __restrict__ H, int64_t Lp,
                                                    int64_t B, const uint16_t* __restrict__ dc,
                                                    int64_t d, int64_t L,
@@ -418,7 +419,8 @@ __global__ __launch_bounds__(256) void union_gemm2(const float* __restrict__ H, 
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const int64_t col = c0 + e * 64 + sc;
-            v[e] = bload16(rd, (rok && col < d) ? (int)((slot * d + col) * 2) : kOOB);
+            const int off = (rok && col < d) ? (int)((slot * d + col) * 2) : kOOB;
+            v[e] = NT ? bload16nt(rd, off) : bload16(rd, off);
         }
         // H of token tok at slots 32 wd + 8 g .. +7 (contiguous, 32-byte aligned)
 #pragma unroll
@@ -596,11 +598,15 @@ hipError_t launch_union_t(const void* x, int64_t B, int64_t d, const int32_t* of
     const bool fast = (flags & 4) != 0;
     dim3 g2((unsigned)((d + kG2Cols - 1) / kG2Cols),
             (unsigned)((B + 16 * p.MT - 1) / (16 * p.MT)), (unsigned)p.KS);
-#define SI_G2F(MTV, F)                                                                          \
-    hipExtLaunchKernelGGL((union_gemm2<ET, MTV, F>), g2, dim3(256), 0, s, nullptr, ev1, 0, H,     \
-                          p.Lp, B, dc, d, L, words, p.W, part, p.KS)
-#define SI_G2(MTV) \
-    if (fast) SI_G2F(MTV, true); else SI_G2F(MTV, false)
+#define SI_G2F(MTV, F, N)                                                                       \
+    hipExtLaunchKernelGGL((union_gemm2<ET, MTV, F, N>), g2, dim3(256), 0, s, nullptr, ev1, 0,     \
+                          H, p.Lp, B, dc, d, L, words, p.W, part, p.KS)
+#define SI_G2(MTV)                                                                              \
+    if (g2.y == 1) {                                                                            \
+        if (fast) SI_G2F(MTV, true, true); else SI_G2F(MTV, false, true);                       \
+    } else {                                                                                    \
+        if (fast) SI_G2F(MTV, true, false); else SI_G2F(MTV, false, false);                     \
+    }
     switch (p.MT) {
         case 8: SI_G2(8); break;
         case 4: SI_G2(4); break;
