@@ -4,11 +4,11 @@
 // compacted, neuron-major device layout. The full layer never sits on the device; the bytes
 // moved are the compacted size of Eq. 2, 3 * d * L * s.
 //
-// Host side: a pool of threads gathers, into two pinned staging buffers in turn, first each
-// row of W_down cut down to its loaded columns ([d][L], a streaming pass), then the loaded rows
-// of W_gate and W_up; each buffer's host-to-device copy runs on the caller's stream while the
-// other is being filled. The cut W_down rows land in gate_up_c, not yet filled, and a device
-// transpose writes down_c from there before the gate/up rows overwrite it.
+// Host side: a pool of threads gathers the loaded rows of W_gate and W_up and each row of
+// W_down cut down to its loaded columns ([d][L], a streaming pass) into two pinned staging
+// buffers in turn; each buffer's host-to-device copy runs on the caller's stream while the
+// other is being filled. The cut W_down rows pass through the first half of gate_up_c, and a
+// device transpose writes down_c from there before that half's gate/up rows overwrite it.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -225,8 +225,36 @@ int si_load_selected(const void* w_gate, const void* w_up, const void* w_down, i
         e = hipMemcpyAsync(orig_to_slot, o2s.data(), (size_t)N * 4, hipMemcpyHostToDevice, st);
     if (e != hipSuccess) return fail(e);
 
-    // down_c[s] = column S[s] of W_down: rows cut to the loaded columns, shipped into
-    // gate_up_c ([d][L], d * L * es bytes of its 2 * d * L * es), transposed on the device
+    // gate_up_c[s] = (W_gate[S[s]], W_up[S[s]]) for slots [s_lo, s_hi)
+    const char* wg = static_cast<const char*>(w_gate);
+    const char* wu = static_cast<const char*>(w_up);
+    const int64_t cs_gu = (int64_t)(std::max(kChunk, 2 * row) / (2 * row));
+    auto gate_up = [&](int64_t s_lo, int64_t s_hi) -> hipError_t {
+        for (int64_t s0 = s_lo; s0 < s_hi; s0 += cs_gu) {
+            const int64_t s1 = std::min(s_hi, s0 + cs_gu);
+            hipError_t err = claim(b);
+            if (err != hipSuccess) return err;
+            char* dst = static_cast<char*>(g_st.buf[b]);
+            parallel_for(s1 - s0, [&](int64_t a, int64_t z) {
+                for (int64_t s = a; s < z; ++s) {
+                    const int64_t n = S[s0 + s];
+                    std::memcpy(dst + s * 2 * row, wg + n * row, row);
+                    std::memcpy(dst + s * 2 * row + row, wu + n * row, row);
+                }
+            });
+            err = ship(b, static_cast<char*>(gate_up_c) + s0 * 2 * row, (s1 - s0) * 2 * row, st);
+            if (err != hipSuccess) return err;
+            b ^= 1;
+        }
+        return hipSuccess;
+    };
+    // The cut W_down rows ([d][L], d * L * es bytes) pass through the first half of gate_up_c;
+    // the slots from s_mid on lie past it. Those gate/up rows go first: a plain row copy is the
+    // quickest fill, so the first copy to the device starts sooner.
+    const int64_t s_mid = (L + 1) / 2;
+    if ((e = gate_up(s_mid, L)) != hipSuccess) return fail(e);
+    // down_c[s] = column S[s] of W_down: rows cut to the loaded columns, shipped into the
+    // first half of gate_up_c, transposed on the device
     char* cut = static_cast<char*>(gate_up_c);
     const int64_t rows_per = (int64_t)(std::max(kChunk, lrow) / lrow);
     for (int64_t i0 = 0; i0 < d; i0 += rows_per) {
@@ -243,26 +271,9 @@ int si_load_selected(const void* w_gate, const void* w_up, const void* w_down, i
     }
     if ((e = si::launch_transpose_cols(cut, d, L, (int)es, down_c, st)) != hipSuccess)
         return fail(e);
-    // gate_up_c[s] = (W_gate[S[s]], W_up[S[s]])
-    const char* wg = static_cast<const char*>(w_gate);
-    const char* wu = static_cast<const char*>(w_up);
-    const int64_t cs_gu = (int64_t)(std::max(kChunk, 2 * row) / (2 * row));
-    for (int64_t s0 = 0; s0 < L; s0 += cs_gu) {
-        const int64_t s1 = std::min(L, s0 + cs_gu);
-        if ((e = claim(b)) != hipSuccess) return fail(e);
-        char* dst = static_cast<char*>(g_st.buf[b]);
-        parallel_for(s1 - s0, [&](int64_t a, int64_t z) {
-            for (int64_t s = a; s < z; ++s) {
-                const int64_t n = S[s0 + s];
-                std::memcpy(dst + s * 2 * row, wg + n * row, row);
-                std::memcpy(dst + s * 2 * row + row, wu + n * row, row);
-            }
-        });
-        if ((e = ship(b, static_cast<char*>(gate_up_c) + s0 * 2 * row, (s1 - s0) * 2 * row,
-                      st)) != hipSuccess)
-            return fail(e);
-        b ^= 1;
-    }
+    // then the gate/up rows of the first half, over the cut rows (after the transpose, in
+    // stream order)
+    if ((e = gate_up(0, s_mid)) != hipSuccess) return fail(e);
     // the maps' host vectors and the staging buffers must outlive the copies
     e = hipStreamSynchronize(st);
     g_st.pending[0] = g_st.pending[1] = false;
