@@ -24,10 +24,10 @@ path; it shares no code with the GPU library or its binding.
 
 Readings taken where the paper is silent:
 
-* ranking key of the per-token selection: |a| (the profiler scores absolute activations);
-  ties go to the lower index, -0 equals +0, NaN ranks below every number (as ``select_topk``);
-  the decision is taken on a rounded to float32, the kernels' precision (the paper fixes none
-  for it);
+* ranking key of the per-token selection: |a| (the profiler scores absolute activations),
+  or a itself (``mode="raw"``, the section's literal "descending order"); ties go to the lower
+  index, -0 equals +0, NaN ranks below every number (as ``select_topk``); the activations are
+  the exact float64 values of the definition (the paper fixes no precision for them);
 * ties in frequency go to the lower slot;
 * "combine until phi is reached": the result holds every static slot plus the
   n_total - n_static most frequent non-static slots, so its size is exactly n_total; a slot
@@ -87,14 +87,9 @@ def select_dynamic(A: np.ndarray, static_slots, alpha: int, n_total: int, mode: 
 
 def dynamic_set(X: np.ndarray, gate_up_c: np.ndarray, static_slots, alpha: int, n_total: int,
                 mode: str = "abs"):
-    """Dynamic-set construction for a prompt X[T][d] over a compacted layer.
-
-    The ranking decision is taken on the activation rounded to float32, the precision in
-    which the kernels compute it: activations that float32 cannot tell apart (a saturated
-    gate, SiLU(g) = g) are equal keys, and the lower slot wins.
-    """
-    A = activations(X, gate_up_c).astype(np.float32).astype(np.float64)
-    return select_dynamic(A, static_slots, alpha, n_total, mode)
+    """Dynamic-set construction for a prompt X[T][d] over a compacted layer, on the float64
+    activations of every loaded slot."""
+    return select_dynamic(activations(X, gate_up_c), static_slots, alpha, n_total, mode)
 
 
 def profile_scores(X: np.ndarray, gate_up: np.ndarray):

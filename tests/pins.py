@@ -359,13 +359,24 @@ def pin_dynamic_set(impl):
         A[:, rng.integers(0, L, 3)] = 0.5                      # exact ties in |a|
         static = sorted(rng.permutation(L)[:ns].tolist())
         _dyn_properties(impl, A, static, alpha, n_total)
-    # from a prompt: the activations are the library's
+    # from a prompt: the activations are the library's, in float64
     wg, wu, _, _ = _problem(13, 18, 8, "bf16")
     X = (rng.standard_normal((6, 8))).astype(np.float32)
-    got, _ = impl.dynamic_set(X, _gu(wg, wu), [2, 9], 4, 7)
-    A32 = _lib_activations(X, wg, wu).astype(np.float32).astype(np.float64)
-    want, _ = impl.select_dynamic(A32, [2, 9], 4, 7)
-    assert np.array_equal(got, want)
+    for mode in ("abs", "raw"):
+        got, _ = impl.dynamic_set(X, _gu(wg, wu), [2, 9], 4, 7, mode=mode)
+        want, _ = impl.select_dynamic(_lib_activations(X, wg, wu), [2, 9], 4, 7, mode=mode)
+        assert np.array_equal(got, want)
+    # activations 2^-30 apart in relative terms: float64 tells them apart (the higher slot
+    # wins), float32 would round both to one value and give the tie to the lower slot
+    wg2 = np.array([[4.0, 0.0], [4.0, 0.0]], np.float32)
+    wu2 = np.array([[1.0, 0.0], [1.0, 1.0]], np.float32)
+    X2 = np.array([[1.0, 2.0 ** -30]], np.float32)
+    got, counts = impl.dynamic_set(X2, _gu(wg2, wu2), [], 1, 1)
+    assert [int(v) for v in got] == [1] and [int(v) for v in counts] == [0, 1]
+    # the literal "descending order": a large negative activation is not taken in raw mode
+    out, counts = impl.select_dynamic(_HAND_A, [], 2, 2, mode="raw")
+    assert [int(v) for v in counts] == [1, 1, 1, 1, 2, 0]    # {2, 4}, {0, 3}, {1, 4}
+    assert [int(v) for v in out] == [0, 4]
     for bad in (dict(static_slots=[1, 1], alpha=2, n_total=3),
                 dict(static_slots=[0, 1, 2], alpha=2, n_total=2),
                 dict(static_slots=[7], alpha=2, n_total=3)):

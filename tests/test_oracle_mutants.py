@@ -135,6 +135,16 @@ def _dyn_with(per_token_mode="abs", freq_high_ties=False, exclude_static=True, f
     return f
 
 
+def _dyn_float32(X, gate_up_c, static_slots, alpha, n_total, mode="abs"):
+    # mistake: the ranking decision taken on activations rounded to float32
+    A = S.activations(X, gate_up_c).astype(np.float32).astype(np.float64)
+    return S.select_dynamic(A, static_slots, alpha, n_total, mode)
+
+
+def _dyn_mode_ignored(X, gate_up_c, static_slots, alpha, n_total, mode="abs"):
+    return S.select_dynamic(S.activations(X, gate_up_c), static_slots, alpha, n_total)
+
+
 def _act_swapped(X, gate_up_c):
     sw = gate_up_c[:, ::-1].copy()
     return S.activations(X, sw)
@@ -178,6 +188,8 @@ MUTANTS = {
     "dyn_freq_high_index_ties": dict(select_dynamic=_dyn_with(freq_high_ties=True)),
     "dyn_static_not_excluded": dict(select_dynamic=_dyn_with(exclude_static=False)),
     "dyn_first_token_only": dict(select_dynamic=_dyn_with(first_token_only=True)),
+    "dyn_float32_activations": dict(dynamic_set=_dyn_float32),
+    "dyn_mode_ignored": dict(dynamic_set=_dyn_mode_ignored),
     "activations_gate_up_swapped": dict(activations=_act_swapped),
     "profile_signed": dict(profile_scores=_profile_signed),
     "merge_not_normalised": dict(merge_scores=_merge_no_norm),
