@@ -52,16 +52,19 @@ typedef enum {
     SI_ERR_WORKSPACE = 7    /* workspace NULL or smaller than the *_workspace query says     */
 } si_status;
 
-/* Ranking key of si_select_topk. */
-enum { SI_TOPK_ABS = 0, SI_TOPK_RAW = 1 };
-
-/* Flags of si_selective_ffn and si_remap_ids. */
+/* Ranking keys (the `mode` of si_select_topk and si_dynamic_set) and call flags. The values
+   are distinct bits, so a mode and flags can share one int. */
 enum {
-    SI_FLAG_CHECK = 1,      /* validate index content on the device, synchronise, report     */
-    SI_FLAG_PER_TOKEN = 2,  /* B > 1: use the per-token path even when the union path applies */
-    SI_FLAG_FAST_H = 4,     /* union path: feed SiLU(g)*u to the second MFMA GEMM as one bf16
-                               value instead of a bf16 hi + lo pair (faster, ~1e-3 rel. err) */
-    SI_FLAG_UNION = 8       /* 2 <= B < 5: use the union path where the dtypes allow it */
+    SI_TOPK_ABS = 1,        /* rank by |score| (the profiler ranks absolute activations)        */
+    SI_TOPK_RAW = 2,        /* rank by the score itself ("descending order" read literally)     */
+    SI_FLAG_CHECK = 4,      /* validate index content on the device, synchronise, report       */
+    SI_FLAG_SORTED = 8,     /* si_selective_ffn: every token's slot list is strictly ascending
+                               (a si_select_topk output); si_select_topk: rows are wanted
+                               ascending, which they always are                                 */
+    SI_FLAG_PER_TOKEN = 16, /* B > 1: use the per-token path even when the union path applies   */
+    SI_FLAG_FAST_H = 32,    /* union path: feed SiLU(g)*u to the second MFMA GEMM as one 16-bit
+                               value instead of a hi + lo pair (faster, ~1e-3 rel. err)         */
+    SI_FLAG_UNION = 64      /* 2 <= B < 5: use the union path where the dtypes allow it         */
 };
 
 /* Library version (major * 10000 + minor * 100 + patch). */
@@ -112,15 +115,21 @@ int si_remap_ids(const int32_t* orig_to_slot, int64_t N,
  * Per-token top-k over loaded neurons (dynamic-neuron selection, Selective Computation
  * section: rank a token's activations over the loaded neurons, descending, keep the top).
  *
- *   scores  [B][L] float32;  out_idx [B][k] int32 out, each row ascending.
+ *   scores  [B][L] float32;  out_idx [B][k] int32 out, each row ascending;
+ *   mode    SI_TOPK_ABS or SI_TOPK_RAW, optionally with SI_FLAG_SORTED (no effect: rows are
+ *           always ascending);
+ *   ws      workspace of si_select_topk_workspace(B, L, k) bytes (NULL when that is 0).
  *
  * Row b selects the k slots with the largest key: key = |score| (SI_TOPK_ABS) or score
  * (SI_TOPK_RAW). Equal keys go to the lower index; -0 and +0 are equal; NaN ranks below every
  * number. The selected set is therefore unique. Requires 0 <= k <= L (k > L is
- * SI_ERR_INVALID), L <= 2^24. B = 0 or k = 0 enqueue nothing.
+ * SI_ERR_INVALID), L <= 2^24, exactly one ranking key in mode. B = 0 or k = 0 enqueue nothing.
+ * The selection runs in one work-group per row with its state in registers and LDS, so the
+ * workspace query returns 0 for every size; ws and ws_bytes are checked against it.
  */
+size_t si_select_topk_workspace(int64_t B, int64_t L, int64_t k);
 int si_select_topk(const float* scores, int64_t B, int64_t L, int64_t k, int mode,
-                   int32_t* out_idx, void* hip_stream);
+                   int32_t* out_idx, void* ws, size_t ws_bytes, void* hip_stream);
 
 /*
  * Workspace bytes si_selective_ffn needs for these sizes and flags (0 means none needed but a
@@ -158,7 +167,10 @@ size_t si_selective_ffn_workspace(int64_t B, int64_t nnz, int64_t L, int64_t d,
  * or 8192 (f32 weights), else SI_ERR_UNSUPPORTED; 16-byte aligned x, gate_up_c, down_c, y and
  * ws; B >= 0; nnz >= 0; L >= 1.
  * SI_FLAG_CHECK validates offsets (non-decreasing, within [0, nnz]), slot range and duplicates
- * on the device, synchronises and returns SI_ERR_RANGE / SI_ERR_DUPLICATE before computing.
+ * on the device, synchronises and returns SI_ERR_RANGE / SI_ERR_DUPLICATE before computing;
+ * with SI_FLAG_SORTED it also returns SI_ERR_INVALID for a list that is not ascending. Without
+ * SI_FLAG_CHECK, SI_FLAG_SORTED is a promise of the caller that the result does not depend on:
+ * the sum is the same for any order of a token's list.
  */
 int si_selective_ffn(const void* x, si_dtype xdt, int64_t B, int64_t d,
                      const int32_t* offsets, const int32_t* idx, int64_t nnz,
@@ -180,6 +192,29 @@ int si_selective_ffn(const void* x, si_dtype xdt, int64_t B, int64_t d,
  * SI_ERR_INVALID if exactly one of the two is NULL.
  */
 int si_set_timing_events(void* start, void* stop);
+
+/*
+ * Memory-system references (measurement only; not part of the method): the read rates the
+ * per-token path is compared with. Both load and discard, storing one folded word per thread
+ * to `sink` so that the loads cannot be removed; neither computes any part of the FFN.
+ *
+ * si_ceiling_stream: a contiguous read of buf[0 .. bytes) with 16-byte non-temporal loads,
+ *   split into `blocks` work-groups of 512 threads (one contiguous part each).
+ *   16 <= bytes < 2^31, 1 <= blocks <= 65535, buf 16-byte aligned; sink [blocks * 512] uint32.
+ * si_ceiling_gather: the per-token path's row pattern for one token with k active slots
+ *   idx[0 .. k) over a compacted layer: P work-groups of 512 threads take the slots as that
+ *   path deals them, and for each batch of 16 rows load every gate and up row, then every down
+ *   row (16 bytes per thread per row, non-temporal). Slots outside [0, L) load nothing.
+ *   Requires d * s % 16 == 0 (s = element size of wdt), L * 2 * d * s < 2^31, k * P < 2^32,
+ *   1 <= P <= 65535; sink [P * 512] uint32.
+ * Asynchronous, stream-ordered. Timing events set with si_set_timing_events are attached to
+ * their dispatch as to the main kernel of si_selective_ffn.
+ */
+int si_ceiling_stream(const void* buf, int64_t bytes, int blocks, uint32_t* sink,
+                      void* hip_stream);
+int si_ceiling_gather(const void* gate_up_c, const void* down_c, int64_t L, int64_t d,
+                      si_dtype wdt, const int32_t* idx, int64_t k, int P, uint32_t* sink,
+                      void* hip_stream);
 
 /*
  * Layer step of a stacked FFN: x_out[b] = RMSNorm(x[b] + y[b]) with unit gain,
@@ -223,8 +258,8 @@ int si_selective_ffn_resnorm(const void* x_prev, const float* y_prev, float eps,
  * Dynamic-set construction (Selective Computation section) for one prompt of T tokens over a
  * compacted layer:
  *   1. a_t[j] = SiLU(gate_c[j] . x[t]) * (up_c[j] . x[t]) for every loaded slot j (float32);
- *   2. per token, the alpha slots with the largest |a_t[j]| (equal keys to the lower slot,
- *      -0 = +0, NaN last), as in si_select_topk;
+ *   2. per token, the alpha slots with the largest key, |a_t[j]| (mode SI_TOPK_ABS) or a_t[j]
+ *      (SI_TOPK_RAW); equal keys to the lower slot, -0 = +0, NaN last, as in si_select_topk;
  *   3. counts[j] = number of the T per-token lists that hold j;
  *   4. the n_total - n_static slots outside the static set with the largest count (equal
  *      counts to the lower slot), joined with the static slots.
@@ -244,7 +279,7 @@ size_t si_dynamic_set_workspace(int64_t T, int64_t L, int64_t alpha, int64_t n_t
 int si_dynamic_set(const void* x, si_dtype xdt, int64_t T, int64_t d,
                    const void* gate_up_c, int64_t L, si_dtype wdt,
                    const int32_t* static_slots, int64_t n_static,
-                   int64_t alpha, int64_t n_total,
+                   int64_t alpha, int64_t n_total, int mode,
                    int32_t* out_slots, int32_t* counts,
                    void* ws, size_t ws_bytes, void* hip_stream);
 
@@ -253,35 +288,38 @@ int si_dynamic_set(const void* x, si_dtype xdt, int64_t T, int64_t d,
  * |a_n(t)|, a_n(t) = SiLU(gate[n] . x[t]) * (up[n] . x[t]), for the N neurons of a full FFN
  * layer held in the compacted layout (si_compact_ffn with every neuron loaded).
  *
- *   x [T][d] (xdt);  gate_up [N][2][d] (wdt);  scores [N] float32, accumulated in place, so
+ *   x [T][d] (xdt);  gate_up [N][2][d] (wdt);  scores [N] float64, accumulated in place, so
  *   batches of tokens add up (the caller keeps the token count);  ws of at least
  *   si_profile_scores_workspace(...) bytes.
  *
- * Sums are float32, in a fixed order (bitwise reproducible). Requires d >= 1, N >= 1, 16-byte
- * aligned x and gate_up. Asynchronous, stream-ordered.
+ * Activations are float32; a call's |a| sums are float32 over at most 256 tokens, then added
+ * to scores in float64, all in a fixed order (bitwise reproducible). A profile of tens of
+ * millions of tokens then keeps the ranking precision of its float64 sums. Requires d >= 1,
+ * N >= 1, 16-byte aligned x and gate_up. Asynchronous, stream-ordered.
  */
 size_t si_profile_scores_workspace(int64_t T, int64_t N, int64_t d, si_dtype xdt, si_dtype wdt);
 int si_profile_scores(const void* x, si_dtype xdt, int64_t T, int64_t d,
                       const void* gate_up, int64_t N, si_dtype wdt,
-                      float* scores, void* ws, size_t ws_bytes, void* hip_stream);
+                      double* scores, void* ws, size_t ws_bytes, void* hip_stream);
 
 /*
  * Merging score files (LLM Profiler section): out[n] = sum over files f of
- * scores[f][n] / tokens[f], files added in order.
+ * scores[f][n] / tokens[f], files added in order, in float64.
  *
- *   scores [F][N] float32 (device);  tokens [F] int64 token counts, HOST memory, each >= 1;
- *   out [N] float32 (device; may not alias scores).  Requires F >= 1, N >= 1.
+ *   scores [F][N] float64 (device);  tokens [F] int64 token counts, HOST memory, each >= 1
+ *   (divided as exact float64 values up to 2^53);  out [N] float64 (device; may not alias
+ *   scores).  Requires F >= 1, N >= 1.
  */
-int si_merge_scores(const float* scores, const int64_t* tokens, int64_t F, int64_t N,
-                    float* out, void* hip_stream);
+int si_merge_scores(const double* scores, const int64_t* tokens, int64_t F, int64_t N,
+                    double* out, void* hip_stream);
 
 /*
  * Ranking (LLM Profiler section): order[r] = the neuron with the r-th largest score; equal
  * scores keep the lower index first, -0 = +0, NaN ranks last.
  *
- *   scores [N] float32;  order [N] int32 out.  Requires 1 <= N <= 2^24.
+ *   scores [N] float64;  order [N] int32 out.  Requires 1 <= N <= 2^24.
  */
-int si_rank_neurons(const float* scores, int64_t N, int32_t* order, void* hip_stream);
+int si_rank_neurons(const double* scores, int64_t N, int32_t* order, void* hip_stream);
 
 /*
  * Loaded-set construction (Selective Loading section): the base neurons are the first n_base

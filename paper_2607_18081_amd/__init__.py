@@ -10,12 +10,15 @@ from .api import (  # noqa: F401
     FLAG_CHECK,
     FLAG_FAST_H,
     FLAG_PER_TOKEN,
+    FLAG_SORTED,
     FLAG_UNION,
     TOPK_ABS,
     TOPK_RAW,
     CompactLayer,
     SelectInferError,
     build_loaded_set,
+    ceiling_gather,
+    ceiling_stream,
     compact_ffn,
     load_selected,
     dynamic_set,

@@ -22,7 +22,8 @@ SIGNATURES = {
     "si_compact_ffn": (c_int, [c_vp, c_vp, c_vp, c_i64, c_i64, c_int, c_vp, c_i64,
                                c_vp, c_vp, c_vp, c_vp, c_vp]),
     "si_remap_ids": (c_int, [c_vp, c_i64, c_vp, c_i64, c_vp, c_int, c_vp]),
-    "si_select_topk": (c_int, [c_vp, c_i64, c_i64, c_i64, c_int, c_vp, c_vp]),
+    "si_select_topk_workspace": (c_size, [c_i64, c_i64, c_i64]),
+    "si_select_topk": (c_int, [c_vp, c_i64, c_i64, c_i64, c_int, c_vp, c_vp, c_size, c_vp]),
     "si_selective_ffn_workspace": (c_size, [c_i64, c_i64, c_i64, c_i64, c_int, c_int, c_int]),
     "si_selective_ffn": (c_int, [c_vp, c_int, c_i64, c_i64, c_vp, c_vp, c_i64, c_vp, c_vp,
                                  c_i64, c_int, c_vp, c_vp, c_size, c_int, c_vp]),
@@ -30,11 +31,14 @@ SIGNATURES = {
                                          c_vp, c_vp, c_i64, c_vp, c_vp, c_i64, c_int, c_vp, c_vp,
                                          c_size, c_int, c_vp]),
     "si_set_timing_events": (c_int, [c_vp, c_vp]),
+    "si_ceiling_stream": (c_int, [c_vp, c_i64, c_int, c_vp, c_vp]),
+    "si_ceiling_gather": (c_int, [c_vp, c_vp, c_i64, c_i64, c_int, c_vp, c_i64, c_int, c_vp,
+                                  c_vp]),
     "si_residual_rmsnorm": (c_int, [c_vp, c_int, c_vp, c_i64, c_i64, ctypes.c_float, c_vp,
                                     c_vp]),
     "si_dynamic_set_workspace": (c_size, [c_i64, c_i64, c_i64, c_i64]),
     "si_dynamic_set": (c_int, [c_vp, c_int, c_i64, c_i64, c_vp, c_i64, c_int, c_vp, c_i64, c_i64,
-                               c_i64, c_vp, c_vp, c_vp, c_size, c_vp]),
+                               c_i64, c_int, c_vp, c_vp, c_vp, c_size, c_vp]),
     "si_profile_scores_workspace": (c_size, [c_i64, c_i64, c_i64, c_int, c_int]),
     "si_profile_scores": (c_int, [c_vp, c_int, c_i64, c_i64, c_vp, c_i64, c_int, c_vp, c_vp,
                                   c_size, c_vp]),

@@ -13,8 +13,9 @@ import torch
 from ._lib import load
 
 F32, BF16, F16 = 0, 1, 2
-TOPK_ABS, TOPK_RAW = 0, 1
-FLAG_CHECK, FLAG_PER_TOKEN, FLAG_FAST_H, FLAG_UNION = 1, 2, 4, 8
+TOPK_ABS, TOPK_RAW = 1, 2
+FLAG_CHECK, FLAG_SORTED, FLAG_PER_TOKEN, FLAG_FAST_H, FLAG_UNION = 4, 8, 16, 32, 64
+_MODES = {"abs": TOPK_ABS, "raw": TOPK_RAW}
 
 _DT = {torch.float32: F32, torch.bfloat16: BF16, torch.float16: F16}
 
@@ -121,8 +122,11 @@ def select_topk(scores: torch.Tensor, k: int, mode: str = "abs",
     B, L = scores.shape
     if out is None:
         out = torch.empty((B, k), dtype=torch.int32, device=dev)
-    m = {"abs": TOPK_ABS, "raw": TOPK_RAW}[mode]
-    st = load().si_select_topk(_ptr(scores), B, L, k, m, _ptr(out), _stream(dev))
+    lib = load()
+    need = int(lib.si_select_topk_workspace(B, L, k))
+    ws = _workspace(dev, need) if need > 0 else None
+    st = lib.si_select_topk(_ptr(scores), B, L, k, _MODES[mode], _ptr(out), _ptr(ws),
+                            ws.numel() if ws is not None else 0, _stream(dev))
     _check(st, "si_select_topk")
     return out
 
@@ -221,6 +225,31 @@ def set_timing_events(start: "torch.cuda.Event | None", stop: "torch.cuda.Event 
     _check(load().si_set_timing_events(h0, h1), "si_set_timing_events")
 
 
+def ceiling_stream(buf: torch.Tensor, blocks: int, sink: torch.Tensor) -> None:
+    """si_ceiling_stream (measurement only): read the whole of buf contiguously."""
+    dev = _dev(buf)
+    if sink.dtype != torch.int32 or sink.numel() < blocks * 512:
+        raise ValueError("sink must hold blocks * 512 int32 words")
+    st = load().si_ceiling_stream(_ptr(buf), buf.numel() * buf.element_size(), blocks,
+                                  _ptr(sink), _stream(dev))
+    _check(st, "si_ceiling_stream")
+
+
+def ceiling_gather(gate_up_c: torch.Tensor, down_c: torch.Tensor, idx: torch.Tensor, P: int,
+                   sink: torch.Tensor) -> None:
+    """si_ceiling_gather (measurement only): load the gate, up and down rows of the slots idx
+    in the per-token path's pattern, without its arithmetic."""
+    dev = _dev(gate_up_c)
+    L, _, d = gate_up_c.shape
+    if down_c.shape != (L, d) or idx.dtype != torch.int32:
+        raise ValueError("compacted weights [L][2][d], [L][d] and int32 slots expected")
+    if sink.dtype != torch.int32 or sink.numel() < P * 512:
+        raise ValueError("sink must hold P * 512 int32 words")
+    st = load().si_ceiling_gather(_ptr(gate_up_c), _ptr(down_c), L, d, _dt(gate_up_c),
+                                  _ptr(idx), idx.numel(), P, _ptr(sink), _stream(dev))
+    _check(st, "si_ceiling_gather")
+
+
 def residual_rmsnorm(x: torch.Tensor, y: torch.Tensor, eps: float = 1e-5,
                      out: torch.Tensor | None = None) -> torch.Tensor:
     """si_residual_rmsnorm: RMSNorm(x + y), unit gain, stored in x's dtype."""
@@ -236,9 +265,11 @@ def residual_rmsnorm(x: torch.Tensor, y: torch.Tensor, eps: float = 1e-5,
 
 def dynamic_set(x: torch.Tensor, gate_up_c: torch.Tensor, static_slots: torch.Tensor,
                 alpha: int, n_total: int, workspace: torch.Tensor | None = None,
-                out: torch.Tensor | None = None, counts: torch.Tensor | None = None):
+                out: torch.Tensor | None = None, counts: torch.Tensor | None = None,
+                mode: str = "abs"):
     """si_dynamic_set: a prompt x [T][d] over a compacted layer -> (active slots [n_total]
-    ascending, counts [L]: how many of the T per-token top-alpha lists hold each slot)."""
+    ascending, counts [L]: how many of the T per-token top-alpha lists hold each slot). The
+    per-token ranking key is |a| (mode "abs") or a ("raw")."""
     dev = _dev(gate_up_c)
     T, d = x.shape
     L = gate_up_c.shape[0]
@@ -257,23 +288,26 @@ def dynamic_set(x: torch.Tensor, gate_up_c: torch.Tensor, static_slots: torch.Te
     if workspace is None:
         workspace = _workspace(dev, need)
     st = lib.si_dynamic_set(_ptr(x), _dt(x), T, d, _ptr(gate_up_c), L, _dt(gate_up_c),
-                            _ptr(static_slots), static_slots.numel(), alpha, n_total, _ptr(out),
-                            _ptr(counts), _ptr(workspace), workspace.numel(), _stream(dev))
+                            _ptr(static_slots), static_slots.numel(), alpha, n_total,
+                            _MODES[mode], _ptr(out), _ptr(counts), _ptr(workspace),
+                            workspace.numel(), _stream(dev))
     _check(st, "si_dynamic_set")
     return out, counts
 
 
 def profile_scores(x: torch.Tensor, gate_up: torch.Tensor, scores: torch.Tensor | None = None,
                    workspace: torch.Tensor | None = None) -> torch.Tensor:
-    """si_profile_scores: scores [N] += sum over the tokens x [T][d] of |a_n| (Eq. 1); a new
-    zeroed scores tensor when none is given."""
+    """si_profile_scores: scores [N] float64 += sum over the tokens x [T][d] of |a_n| (Eq. 1);
+    a new zeroed scores tensor when none is given."""
     dev = _dev(gate_up)
     T, d = x.shape
     N = gate_up.shape[0]
     if gate_up.shape != (N, 2, d):
         raise ValueError("gate_up must be [N][2][d]")
     if scores is None:
-        scores = torch.zeros(N, dtype=torch.float32, device=dev)
+        scores = torch.zeros(N, dtype=torch.float64, device=dev)
+    if scores.dtype != torch.float64 or scores.numel() != N:
+        raise ValueError("scores must be a float64 tensor of N entries")
     lib = load()
     need = int(lib.si_profile_scores_workspace(T, N, d, _dt(x), _dt(gate_up)))
     if workspace is None:
@@ -285,13 +319,18 @@ def profile_scores(x: torch.Tensor, gate_up: torch.Tensor, scores: torch.Tensor 
 
 
 def merge_scores(scores: torch.Tensor, tokens) -> torch.Tensor:
-    """si_merge_scores: scores [F][N] with token counts [F] (host ints) -> sum of s_f / T_f."""
+    """si_merge_scores: float64 scores [F][N] with token counts [F] (host ints) -> sum of
+    s_f / T_f (float64)."""
     import ctypes
 
     dev = _dev(scores)
+    if scores.dtype != torch.float64 or scores.dim() != 2:
+        raise ValueError("scores must be a 2-D float64 tensor")
     F, N = scores.shape
+    if len(tokens) != F:
+        raise ValueError("one token count per score file")
     toks = (ctypes.c_int64 * F)(*[int(t) for t in tokens])
-    out = torch.empty(N, dtype=torch.float32, device=dev)
+    out = torch.empty(N, dtype=torch.float64, device=dev)
     st = load().si_merge_scores(_ptr(scores), ctypes.cast(toks, ctypes.c_void_p), F, N,
                                 _ptr(out), _stream(dev))
     _check(st, "si_merge_scores")
@@ -299,8 +338,10 @@ def merge_scores(scores: torch.Tensor, tokens) -> torch.Tensor:
 
 
 def rank_neurons(scores: torch.Tensor) -> torch.Tensor:
-    """si_rank_neurons: neuron indices by decreasing score (ties to the lower index)."""
+    """si_rank_neurons: neuron indices by decreasing float64 score (ties to the lower index)."""
     dev = _dev(scores)
+    if scores.dtype != torch.float64:
+        raise ValueError("scores must be float64")
     order = torch.empty(scores.numel(), dtype=torch.int32, device=dev)
     st = load().si_rank_neurons(_ptr(scores), scores.numel(), _ptr(order), _stream(dev))
     _check(st, "si_rank_neurons")

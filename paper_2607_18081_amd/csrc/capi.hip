@@ -77,6 +77,14 @@ bool valid_pair(int xdt, int wdt) {
     return valid_dtype(xdt) && valid_dtype(wdt) && (xdt == SI_F32 || wdt == SI_F32 || xdt == wdt);
 }
 
+// The kernels' ranking key from a public mode (exactly one of SI_TOPK_ABS, SI_TOPK_RAW):
+// 0 = |score|, 1 = score; -1 for anything else
+int topk_key(int mode) {
+    if (mode == SI_TOPK_ABS) return 0;
+    if (mode == SI_TOPK_RAW) return 1;
+    return -1;
+}
+
 // Smallest batch that takes the union path by default. Reading the union once costs |U| rows
 // instead of nnz >= |U|, but the union path runs four kernels with a fixed cost of about
 // 11 000 row reads (measured on the 7B shape: a step is about 28.5 us + 3.6 ns per union row,
@@ -118,8 +126,9 @@ int selective_ffn(const void* x, si_dtype xdt, int64_t B, int64_t d, const int32
     hipStream_t s = static_cast<hipStream_t>(hip_stream);
     if (flags & SI_FLAG_CHECK) {
         if (L > 524288) return SI_ERR_UNSUPPORTED;
+        const bool sorted = (flags & SI_FLAG_SORTED) != 0;
         const int st = checked(s, dev, [&](int* err) {
-            return si::launch_check_csr(offsets, idx, B, nnz, L, err, s);
+            return si::launch_check_csr(offsets, idx, B, nnz, L, sorted, err, s);
         });
         if (st != SI_OK) return st;
     }
@@ -144,7 +153,7 @@ int selective_ffn(const void* x, si_dtype xdt, int64_t B, int64_t d, const int32
 
 extern "C" {
 
-int si_version(void) { return 100; }
+int si_version(void) { return 200; }
 
 const char* si_status_string(int status) {
     switch (status) {
@@ -201,13 +210,18 @@ int si_remap_ids(const int32_t* orig_to_slot, int64_t N, const int32_t* ids, int
     return from_hip(si::launch_remap(orig_to_slot, N, ids, n, slots, nullptr, s));
 }
 
+size_t si_select_topk_workspace(int64_t, int64_t, int64_t) { return 0; }
+
 int si_select_topk(const float* scores, int64_t B, int64_t L, int64_t k, int mode,
-                   int32_t* out_idx, void* hip_stream) {
+                   int32_t* out_idx, void* ws, size_t ws_bytes, void* hip_stream) {
     if (B < 0 || L < 1 || k < 0 || k > L || L > (1 << 24)) return SI_ERR_INVALID;
-    if (mode != SI_TOPK_ABS && mode != SI_TOPK_RAW) return SI_ERR_INVALID;
+    const int key = topk_key(mode & ~SI_FLAG_SORTED);
+    if (key < 0) return SI_ERR_INVALID;
+    if (ws_bytes < si_select_topk_workspace(B, L, k) || (ws_bytes > 0 && !ws))
+        return SI_ERR_WORKSPACE;
     if (B == 0 || k == 0) return SI_OK;
     if (!scores || !out_idx) return SI_ERR_INVALID;
-    return from_hip(si::launch_topk(scores, B, L, k, mode, out_idx,
+    return from_hip(si::launch_topk(scores, B, L, k, key, out_idx,
                                     static_cast<hipStream_t>(hip_stream)));
 }
 
@@ -249,6 +263,33 @@ int si_selective_ffn_resnorm(const void* x_prev, const float* y_prev, float eps,
                          ws_bytes, flags, hip_stream, &rn);
 }
 
+int si_ceiling_stream(const void* buf, int64_t bytes, int blocks, uint32_t* sink,
+                      void* hip_stream) {
+    if (!buf || !sink || bytes < 16 || bytes >= ((int64_t)1 << 31) || blocks < 1 ||
+        blocks > 65535)
+        return SI_ERR_INVALID;
+    if (!aligned16(buf)) return SI_ERR_INVALID;
+    return from_hip(si::launch_ceiling_stream(buf, bytes, blocks, sink,
+                                              static_cast<hipStream_t>(hip_stream), t_ev_start,
+                                              t_ev_stop));
+}
+
+int si_ceiling_gather(const void* gate_up_c, const void* down_c, int64_t L, int64_t d,
+                      si_dtype wdt, const int32_t* idx, int64_t k, int P, uint32_t* sink,
+                      void* hip_stream) {
+    if (!valid_dtype(wdt)) return SI_ERR_UNSUPPORTED;
+    const int64_t rb = d * (wdt == SI_F32 ? 4 : 2);
+    if (!gate_up_c || !down_c || !sink || L < 1 || d < 1 || k < 0 || P < 1 || P > 65535)
+        return SI_ERR_INVALID;
+    if (k > 0 && !idx) return SI_ERR_INVALID;
+    if (rb % 16 != 0 || L * 2 * rb >= ((int64_t)1 << 31) || k * P >= ((int64_t)1 << 32))
+        return SI_ERR_UNSUPPORTED;
+    if (!aligned16(gate_up_c) || !aligned16(down_c)) return SI_ERR_INVALID;
+    return from_hip(si::launch_ceiling_gather(gate_up_c, down_c, L, rb, idx, k, P, sink,
+                                              static_cast<hipStream_t>(hip_stream), t_ev_start,
+                                              t_ev_stop));
+}
+
 int si_set_timing_events(void* start, void* stop) {
     if ((start == nullptr) != (stop == nullptr)) return SI_ERR_INVALID;
     t_ev_start = static_cast<hipEvent_t>(start);
@@ -273,9 +314,11 @@ size_t si_dynamic_set_workspace(int64_t T, int64_t L, int64_t alpha, int64_t n_t
 
 int si_dynamic_set(const void* x, si_dtype xdt, int64_t T, int64_t d, const void* gate_up_c,
                    int64_t L, si_dtype wdt, const int32_t* static_slots, int64_t n_static,
-                   int64_t alpha, int64_t n_total, int32_t* out_slots, int32_t* counts, void* ws,
-                   size_t ws_bytes, void* hip_stream) {
+                   int64_t alpha, int64_t n_total, int mode, int32_t* out_slots, int32_t* counts,
+                   void* ws, size_t ws_bytes, void* hip_stream) {
     if (T < 0 || d < 1 || L < 1 || L > (1 << 24)) return SI_ERR_INVALID;
+    const int key = topk_key(mode);
+    if (key < 0) return SI_ERR_INVALID;
     if (alpha < 0 || alpha > L || n_static < 0 || n_static > n_total || n_total > L)
         return SI_ERR_INVALID;
     if (!valid_pair(xdt, wdt)) return SI_ERR_UNSUPPORTED;
@@ -286,7 +329,7 @@ int si_dynamic_set(const void* x, si_dtype xdt, int64_t T, int64_t d, const void
     if (!ws || ws_bytes < need || !aligned16(ws)) return SI_ERR_WORKSPACE;
     if (current_device() < 0) return SI_ERR_HIP;
     return from_hip(si::launch_dynamic_set(x, xdt, T, d, gate_up_c, L, wdt, static_slots,
-                                           n_static, alpha, n_total, out_slots, counts, ws,
+                                           n_static, alpha, n_total, key, out_slots, counts, ws,
                                            static_cast<hipStream_t>(hip_stream), t_ev_start,
                                            t_ev_stop));
 }
@@ -297,7 +340,7 @@ size_t si_profile_scores_workspace(int64_t T, int64_t N, int64_t d, si_dtype xdt
 }
 
 int si_profile_scores(const void* x, si_dtype xdt, int64_t T, int64_t d, const void* gate_up,
-                      int64_t N, si_dtype wdt, float* scores, void* ws, size_t ws_bytes,
+                      int64_t N, si_dtype wdt, double* scores, void* ws, size_t ws_bytes,
                       void* hip_stream) {
     if (T < 0 || d < 1 || N < 1 || N > INT32_MAX) return SI_ERR_INVALID;
     if (!valid_pair(xdt, wdt)) return SI_ERR_UNSUPPORTED;
@@ -312,21 +355,22 @@ int si_profile_scores(const void* x, si_dtype xdt, int64_t T, int64_t d, const v
                                       t_ev_stop));
 }
 
-int si_merge_scores(const float* scores, const int64_t* tokens, int64_t F, int64_t N, float* out,
-                    void* hip_stream) {
+int si_merge_scores(const double* scores, const int64_t* tokens, int64_t F, int64_t N,
+                    double* out, void* hip_stream) {
     if (F < 1 || N < 1 || !scores || !tokens || !out) return SI_ERR_INVALID;
     for (int64_t f = 0; f < F; ++f)
-        if (tokens[f] < 1) return SI_ERR_INVALID;
+        if (tokens[f] < 1 || tokens[f] > ((int64_t)1 << 53)) return SI_ERR_INVALID;
+    if (overlap(out, N * 8, scores, F * N * 8)) return SI_ERR_INVALID;
     hipStream_t s = static_cast<hipStream_t>(hip_stream);
     for (int64_t f = 0; f < F; ++f) {
         const hipError_t e =
-            si::launch_merge_file(scores + f * N, N, (float)tokens[f], f == 0 ? 1 : 0, out, s);
+            si::launch_merge_file(scores + f * N, N, (double)tokens[f], f == 0 ? 1 : 0, out, s);
         if (e != hipSuccess) return from_hip(e);
     }
     return SI_OK;
 }
 
-int si_rank_neurons(const float* scores, int64_t N, int32_t* order, void* hip_stream) {
+int si_rank_neurons(const double* scores, int64_t N, int32_t* order, void* hip_stream) {
     if (N < 1 || N > (1 << 24) || !scores || !order) return SI_ERR_INVALID;
     return from_hip(si::launch_rank(scores, N, order, static_cast<hipStream_t>(hip_stream)));
 }

@@ -29,9 +29,14 @@ namespace {
 constexpr int kWaves = 8;
 constexpr int kThreads = kWaves * kWave;
 
-template <int NI>
+// Rows whose loads a work-group issues together: 3 * R * NI 16-byte loads per lane stay in
+// registers. A stacked-layer instance (RN) also holds the residual r until the normalisation,
+// so beyond the one-group bf16 case it takes smaller batches and never spills.
+template <typename XT, int NI, bool RN>
 struct RowsPerBatch {
-    static constexpr int value = NI == 1 ? 16 : NI == 2 ? 8 : NI == 3 ? 4 : 2;
+    static constexpr bool lean = RN && !(sizeof(XT) == 2 && NI == 1);
+    static constexpr int value = lean ? (NI == 1 ? 8 : NI == 2 ? 4 : NI == 3 ? 2 : 1)
+                                      : (NI == 1 ? 16 : NI == 2 ? 8 : NI == 3 ? 4 : 2);
 };
 
 typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
@@ -275,7 +280,7 @@ __global__ __launch_bounds__(kThreads) void sffn_rows(
     const XT* __restrict__ xprev, const float* __restrict__ yprev, float eps,
     XT* __restrict__ xout) {
     constexpr int V = Elem<WT>::V;
-    constexpr int R = RowsPerBatch<NI>::value;
+    constexpr int R = RowsPerBatch<XT, NI, RN>::value;
     constexpr int NVAL = 2 * R;
     constexpr int PER = kWave / NVAL;
 
@@ -344,6 +349,8 @@ __global__ __launch_bounds__(kThreads) void sffn_rows(
 #pragma unroll
                 for (int e = 0; e < V; ++e) rr[i][e] = round_to<XT>(rr[i][e] * scale);
                 xs[i].set(rr[i]);
+                // the token's first work-group keeps x for the next layer's residual
+                if (p == 0 && cok[i]) store_elems<XT, V>(xout + (int64_t)b * d + col[i], rr[i]);
             }
             pending = false;
         }
@@ -474,11 +481,6 @@ __global__ __launch_bounds__(kThreads) void sffn_rows(
 
     if constexpr (RN) {
         if (pending) normalise();  // a work-group without rows
-        if (p == 0) {
-#pragma unroll
-            for (int i = 0; i < NI; ++i)
-                if (cok[i]) store_elems<XT, V>(xout + (int64_t)b * d + col[i], rr[i]);
-        }
     }
 
     const int64_t nch = part_chunks(d);

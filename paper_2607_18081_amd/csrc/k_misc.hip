@@ -7,6 +7,7 @@ namespace si {
 
 namespace {
 
+constexpr int kErrInvalid = 1;
 constexpr int kErrRange = 2;
 constexpr int kErrDuplicate = 3;
 constexpr int kErrNotLoaded = 4;
@@ -30,10 +31,10 @@ __global__ void remap_ids(const int32_t* __restrict__ o2s, int64_t N,
 }
 
 // One work-group per token: offsets in range and non-decreasing, slots in [0, L), no slot
-// twice (an LDS bitmap of L bits).
+// twice (an LDS bitmap of L bits); with `sorted`, each slot above the one before it.
 __global__ __launch_bounds__(256) void check_csr(const int32_t* __restrict__ offsets,
                                                  const int32_t* __restrict__ idx, int64_t nnz,
-                                                 int64_t L, int* err) {
+                                                 int64_t L, int sorted, int* err) {
     extern __shared__ uint32_t bits[];
     const int64_t b = blockIdx.x;
     const int64_t lo = offsets[b], hi = offsets[b + 1];
@@ -53,6 +54,7 @@ __global__ __launch_bounds__(256) void check_csr(const int32_t* __restrict__ off
         const uint32_t bit = 1u << (s & 31);
         const uint32_t old = atomicOr(&bits[s >> 5], bit);
         if (old & bit) set_err(err, kErrDuplicate, (int)r);
+        if (sorted && r > lo && idx[r - 1] > s) set_err(err, kErrInvalid, (int)r);
     }
 }
 
@@ -179,11 +181,11 @@ hipError_t launch_remap(const int32_t* orig_to_slot, int64_t N, const int32_t* i
 }
 
 hipError_t launch_check_csr(const int32_t* offsets, const int32_t* idx, int64_t B, int64_t nnz,
-                            int64_t L, int* err, hipStream_t s) {
+                            int64_t L, bool sorted, int* err, hipStream_t s) {
     if (B == 0) return hipSuccess;
     const size_t lds = (size_t)((L + 31) / 32) * 4;
     hipLaunchKernelGGL(check_csr, dim3((unsigned)B), dim3(256), lds, s, offsets, idx, nnz, L,
-                       err);
+                       sorted ? 1 : 0, err);
     return hipGetLastError();
 }
 

@@ -4,8 +4,8 @@
 //  - act_rows: the activation a[t][j] = SiLU(gate_j . x_t) * (up_j . x_t) of every loaded slot
 //    for any storage type (one wave per (token, slot)); bf16 data use the MFMA tiles of
 //    k_tiled.hip instead;
-//  - col_abs_sum / add_rows: Eq. 1 sums |a| over tokens, and partial rows over token tiles,
-//    in ascending order;
+//  - col_abs_sum / add_rows: Eq. 1 sums |a| over tokens (float32 over at most 256 tokens) and
+//    the partial rows of the token tiles in float64, in ascending order, into float64 scores;
 //  - count_bits: how many tokens select each slot, from the tokens' top-alpha bitmaps (up to
 //    32768 slots): one work-group per 32-slot word, wave ballots and a fixed-order sum, so the
 //    count is exact and free of atomics; it also writes the counts as the keys of the pick;
@@ -14,7 +14,7 @@
 //  - freq_keys: the frequency of each slot as a float key (exact below 2^24), static slots
 //    (set in the bitmap) below every frequency;
 //  - set_bits: a slot list as a bitmap (then listed in ascending order by the union scan);
-//  - merge_file: out += s / tokens for one score file, file by file;
+//  - merge_file: out += s / tokens for one score file, file by file (float64);
 //  - rank_scores: the position of each neuron in decreasing score (ties to the lower index,
 //    NaN last), by counting the neurons ranked before it; exact and order-free.
 #include "common.h"
@@ -55,23 +55,30 @@ __global__ __launch_bounds__(256) void act_rows(const XT* __restrict__ x, int64_
     if (lane == 0) out[t * ldo + j] = silu_f32(g) * u;
 }
 
-// s[n] += sum over t = 0 .. T-1 of |A[t][n]| (A with row stride lda)
+// s[n] += sum over t = 0 .. T-1 of |A[t][n]| (A with row stride lda): float32 sums over
+// blocks of 256 tokens, as the MFMA tiles form them, added in float64
 __global__ __launch_bounds__(256) void col_abs_sum(const float* __restrict__ A, int64_t T,
-                                                   int64_t N, int64_t lda, float* __restrict__ s) {
+                                                   int64_t N, int64_t lda,
+                                                   double* __restrict__ s) {
     const int64_t n = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (n >= N) return;
-    float v = 0.0f;
-    for (int64_t t = 0; t < T; ++t) v += fabsf(A[t * lda + n]);
-    s[n] += v;
+    double tot = 0.0;
+    for (int64_t t0 = 0; t0 < T; t0 += 256) {
+        const int64_t t1 = (T - t0) < 256 ? T : t0 + 256;
+        float v = 0.0f;
+        for (int64_t t = t0; t < t1; ++t) v += fabsf(A[t * lda + n]);
+        tot += (double)v;
+    }
+    s[n] += tot;
 }
 
-// s[n] += sum over r = 0 .. R-1 of P[r][n] (P with row stride ldp)
+// s[n] += sum over r = 0 .. R-1 of P[r][n] (P with row stride ldp), in float64
 __global__ __launch_bounds__(256) void add_rows(const float* __restrict__ P, int64_t R, int64_t N,
-                                                int64_t ldp, float* __restrict__ s) {
+                                                int64_t ldp, double* __restrict__ s) {
     const int64_t n = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (n >= N) return;
-    float v = 0.0f;
-    for (int64_t r = 0; r < R; ++r) v += P[r * ldp + n];
+    double v = 0.0;
+    for (int64_t r = 0; r < R; ++r) v += (double)P[r * ldp + n];
     s[n] += v;
 }
 
@@ -143,38 +150,38 @@ __global__ __launch_bounds__(256) void set_bits(const int32_t* __restrict__ ids,
     if (v >= 0 && v < L) atomicOr(&bits[v >> 5], 1u << (v & 31));
 }
 
-__global__ __launch_bounds__(256) void merge_file(const float* __restrict__ s, int64_t N,
-                                                  float tokens, int first,
-                                                  float* __restrict__ out) {
+__global__ __launch_bounds__(256) void merge_file(const double* __restrict__ s, int64_t N,
+                                                  double tokens, int first,
+                                                  double* __restrict__ out) {
     const int64_t n = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (n >= N) return;
-    const float v = s[n] / tokens;
+    const double v = s[n] / tokens;
     out[n] = first ? v : out[n] + v;
 }
 
-// Order key, larger first: -0 and +0 equal, NaN below every number.
-__device__ __forceinline__ uint32_t desc_key(float f) {
-    if (f != f) return 0u;
-    uint32_t u = __float_as_uint(f);
-    if ((u << 1) == 0u) u = 0u;
-    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+// Order key of a float64 score, larger first: -0 and +0 equal, NaN below every number.
+__device__ __forceinline__ uint64_t desc_key(double f) {
+    if (f != f) return 0ull;
+    uint64_t u = (uint64_t)__double_as_longlong(f);
+    if ((u << 1) == 0ull) u = 0ull;
+    return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
 }
 
 // Grid ceil(N / 256): thread n counts the neurons ranked before n over LDS tiles of keys.
-__global__ __launch_bounds__(256) void rank_scores(const float* __restrict__ s, int64_t N,
+__global__ __launch_bounds__(256) void rank_scores(const double* __restrict__ s, int64_t N,
                                                    int32_t* __restrict__ order) {
-    __shared__ uint32_t tk[256];
+    __shared__ uint64_t tk[256];
     const int64_t n = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    const uint32_t kn = n < N ? desc_key(s[n]) : 0u;
+    const uint64_t kn = n < N ? desc_key(s[n]) : 0ull;
     int64_t before = 0;
     for (int64_t m0 = 0; m0 < N; m0 += 256) {
         __syncthreads();
         const int64_t m = m0 + threadIdx.x;
-        tk[threadIdx.x] = m < N ? desc_key(s[m]) : 0u;
+        tk[threadIdx.x] = m < N ? desc_key(s[m]) : 0ull;
         __syncthreads();
         const int64_t lim = (N - m0) < 256 ? (N - m0) : 256;
         for (int q = 0; q < lim; ++q) {
-            const uint32_t km = tk[q];
+            const uint64_t km = tk[q];
             before += (km > kn) || (km == kn && m0 + q < n);
         }
     }
@@ -235,7 +242,7 @@ size_t score_workspace(int64_t T, int64_t N, int64_t d, int xdt, int wdt) {
 }
 
 hipError_t launch_scores(const void* x, int xdt, int64_t T, int64_t d, const void* gate_up,
-                         int64_t N, int wdt, float* scores, void* ws, hipStream_t s,
+                         int64_t N, int wdt, double* scores, void* ws, hipStream_t s,
                          hipEvent_t ev0, hipEvent_t ev1) {
     if (T == 0 || N == 0) return hipSuccess;
     const int64_t ldo = (N + 63) / 64 * 64;
@@ -282,8 +289,9 @@ DynPlan dyn_plan(int64_t T, int64_t L, int64_t alpha, int64_t n_total) {
 
 hipError_t launch_dynamic_set(const void* x, int xdt, int64_t T, int64_t d, const void* gate_up_c,
                               int64_t L, int wdt, const int32_t* static_slots, int64_t n_static,
-                              int64_t alpha, int64_t n_total, int32_t* out, int32_t* counts_out,
-                              void* ws, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+                              int64_t alpha, int64_t n_total, int key, int32_t* out,
+                              int32_t* counts_out, void* ws, hipStream_t s, hipEvent_t ev0,
+                              hipEvent_t ev1) {
     const DynPlan p = dyn_plan(T, L, alpha, n_total);
     uint8_t* base = static_cast<uint8_t*>(ws);
     float* act = reinterpret_cast<float*>(base + p.off_act);
@@ -301,12 +309,12 @@ hipError_t launch_dynamic_set(const void* x, int xdt, int64_t T, int64_t d, cons
         if (e != hipSuccess) return e;
     }
     if (p.token_bits) {
-        // 2. each token's top alpha by |a| as a bitmap; 3. counts (the keys of the pick) per
-        //    32-slot word; 4. the static slots joined with the dynamic pick among the others,
-        //    ascending
+        // 2. each token's top alpha by |a| or a (key) as a bitmap; 3. counts (the keys of the
+        //    pick) per 32-slot word; 4. the static slots joined with the dynamic pick among the
+        //    others, ascending
         uint32_t* tbits = reinterpret_cast<uint32_t*>(lists);
         const int64_t Tr = alpha > 0 ? T : 0;
-        e = launch_topk_bitmap(act, Tr, L, p.lda, alpha, 0, tbits, p.W, s);
+        e = launch_topk_bitmap(act, Tr, L, p.lda, alpha, key, tbits, p.W, s);
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL(count_bits, dim3((unsigned)p.W), dim3(256), 0, s, tbits, Tr, p.W, L,
                            counts, reinterpret_cast<uint32_t*>(keys));
@@ -319,9 +327,10 @@ hipError_t launch_dynamic_set(const void* x, int xdt, int64_t T, int64_t d, cons
     if (n_static > 0)
         hipLaunchKernelGGL(set_bits, dim3(blocks(n_static)), dim3(256), 0, s, static_slots,
                            n_static, L, bits);
-    // 2. each token's top alpha by |a|; 3. how often each slot is chosen (atomics on the ids)
+    // 2. each token's top alpha by |a| or a (key); 3. how often each slot is chosen (atomics
+    //    on the ids)
     if (T > 0 && alpha > 0) {
-        e = launch_topk_strided(act, T, L, p.lda, alpha, 0, lists, s);
+        e = launch_topk_strided(act, T, L, p.lda, alpha, key, lists, s);
         if (e != hipSuccess) return e;
         const int64_t n = T * alpha;
         hipLaunchKernelGGL(count_slots, dim3(blocks(n)), dim3(256), 0, s, lists, n, L, counts);
@@ -339,13 +348,13 @@ hipError_t launch_dynamic_set(const void* x, int xdt, int64_t T, int64_t d, cons
     return launch_bits_to_list(bits, p.W, out, cnt, s);
 }
 
-hipError_t launch_merge_file(const float* sc, int64_t N, float tokens, int first, float* out,
+hipError_t launch_merge_file(const double* sc, int64_t N, double tokens, int first, double* out,
                              hipStream_t s) {
     hipLaunchKernelGGL(merge_file, dim3(blocks(N)), dim3(256), 0, s, sc, N, tokens, first, out);
     return hipGetLastError();
 }
 
-hipError_t launch_rank(const float* sc, int64_t N, int32_t* order, hipStream_t s) {
+hipError_t launch_rank(const double* sc, int64_t N, int32_t* order, hipStream_t s) {
     if (N == 0) return hipSuccess;
     hipLaunchKernelGGL(rank_scores, dim3(blocks(N)), dim3(256), 0, s, sc, N, order);
     return hipGetLastError();

@@ -32,6 +32,7 @@
 #include "common.h"
 #include "launch.h"
 #include "mfma.h"
+#include "selectinfer.h"
 
 namespace si {
 
@@ -565,7 +566,7 @@ hipError_t launch_union_tiled_t(const void* x, int64_t B, int64_t d, const int32
         hipExtLaunchKernelGGL((gemm1_tiled<ET, kUnion, 128>), dim3((unsigned)(nst8 * p.ntm1)),
                               dim3(256), 0, s, ev0, nullptr, 0, xx, B, d, gu, L, ulist, ucount,
                               bits, p.W, hhi, hlo, p.Up, p.ntm1, nullptr);
-    const int fast = (flags & 4) ? 1 : 0;
+    const int fast = (flags & SI_FLAG_FAST_H) ? 1 : 0;
     hipExtLaunchKernelGGL((gemm2_tiled<ET>), dim3((unsigned)p.ntn2, (unsigned)p.ntm2, (unsigned)p.KS),
                           dim3(kT2T), 0, s, nullptr, ev1, 0, hhi, hlo, p.Up, B, dc, d, L, ulist,
                           ucount, part, p.KS, fast);

@@ -34,6 +34,7 @@
 #include "common.h"
 #include "launch.h"
 #include "mfma.h"
+#include "selectinfer.h"
 
 namespace si {
 
@@ -595,7 +596,7 @@ hipError_t launch_union_t(const void* x, int64_t B, int64_t d, const int32_t* of
         SI_G1(4, false);
     }
 #undef SI_G1
-    const bool fast = (flags & 4) != 0;
+    const bool fast = (flags & SI_FLAG_FAST_H) != 0;
     dim3 g2((unsigned)((d + kG2Cols - 1) / kG2Cols),
             (unsigned)((B + 16 * p.MT - 1) / (16 * p.MT)), (unsigned)p.KS);
 #define SI_G2F(MTV, F, N)                                                                       \

@@ -95,7 +95,7 @@ hipError_t launch_activations(const void* x, int xdt, int64_t T, int64_t d, cons
                               hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 size_t score_workspace(int64_t T, int64_t N, int64_t d, int xdt, int wdt);
 hipError_t launch_scores(const void* x, int xdt, int64_t T, int64_t d, const void* gate_up,
-                         int64_t N, int wdt, float* scores, void* ws, hipStream_t s,
+                         int64_t N, int wdt, double* scores, void* ws, hipStream_t s,
                          hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 // up to this many slots the tokens' top-alpha picks travel as bitmaps (the register top-k)
 constexpr int64_t kTokenBitsMaxL = 32768;
@@ -107,12 +107,13 @@ struct DynPlan {
 DynPlan dyn_plan(int64_t T, int64_t L, int64_t alpha, int64_t n_total);
 hipError_t launch_dynamic_set(const void* x, int xdt, int64_t T, int64_t d, const void* gate_up_c,
                               int64_t L, int wdt, const int32_t* static_slots, int64_t n_static,
-                              int64_t alpha, int64_t n_total, int32_t* out, int32_t* counts_out,
+                              int64_t alpha, int64_t n_total, int key, int32_t* out,
+                              int32_t* counts_out,
                               void* ws, hipStream_t s, hipEvent_t ev0 = nullptr,
                               hipEvent_t ev1 = nullptr);
-hipError_t launch_merge_file(const float* sc, int64_t N, float tokens, int first, float* out,
+hipError_t launch_merge_file(const double* sc, int64_t N, double tokens, int first, double* out,
                              hipStream_t s);
-hipError_t launch_rank(const float* sc, int64_t N, int32_t* order, hipStream_t s);
+hipError_t launch_rank(const double* sc, int64_t N, int32_t* order, hipStream_t s);
 
 // ---- k_compact.hip ------------------------------------------------------------------------
 hipError_t launch_compact_maps(const int32_t* loaded, int64_t L, int64_t N,
@@ -125,11 +126,20 @@ hipError_t launch_compact_gather(const void* w_gate, const void* w_up, const voi
 hipError_t launch_transpose_cols(const void* src, int64_t d, int64_t L, int esize, void* dst,
                                  hipStream_t s);
 
+// ---- k_ceiling.hip: memory-system references (measurement only) ---------------------------
+// sink: blocks (or P) * 512 words; ev0/ev1 (optional) stamped by the kernel's dispatch
+hipError_t launch_ceiling_stream(const void* buf, int64_t bytes, int blocks, uint32_t* sink,
+                                 hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
+hipError_t launch_ceiling_gather(const void* gate_up_c, const void* down_c, int64_t L,
+                                 int64_t row_bytes, const int32_t* idx, int64_t k, int P,
+                                 uint32_t* sink, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
+
 // ---- k_misc.hip ---------------------------------------------------------------------------
 hipError_t launch_remap(const int32_t* orig_to_slot, int64_t N, const int32_t* ids, int64_t n,
                         int32_t* slots, int* err, hipStream_t s);
+// sorted: also require each token's slots in strictly ascending order (else error 1)
 hipError_t launch_check_csr(const int32_t* offsets, const int32_t* idx, int64_t B,
-                            int64_t nnz, int64_t L, int* err, hipStream_t s);
+                            int64_t nnz, int64_t L, bool sorted, int* err, hipStream_t s);
 hipError_t launch_residual_rmsnorm(const void* x, int xdt, const float* y, int64_t B, int64_t d,
                                    float eps, void* x_out, hipStream_t s);
 

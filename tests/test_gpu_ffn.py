@@ -1,8 +1,11 @@
 """GPU parity of si_selective_ffn against the fp64 oracle, per token.
 
 Tolerance (per token, relative L2, max over tokens): 1e-5 for f32 weights, 5e-3 for bf16
-weights. The per-token path only reassociates float32 sums, so it is also held to an internal
-1e-4 alarm; the union path rounds h to a bf16 hi+lo pair for its MFMA GEMM.
+weights. The paths are held tighter where their arithmetic allows: the per-token path only
+reassociates float32 sums, and the union path's default feeds h to its MFMA GEMM as a 16-bit
+hi + lo pair (about 16 significant bits), so both are held to 1e-4 per token and to an
+element-wise bound, max |y - y_ref| <= 1e-4 * max |y_ref| per token. SI_FLAG_FAST_H (h as one
+16-bit value, about 8 bits for bf16) is held to the 5e-3 bar.
 """
 import functools
 import math
@@ -20,6 +23,17 @@ pytestmark = pytest.mark.gpu
 
 TOL = {"f32": 1e-5, "bf16": 5e-3}
 ALARM_PER_TOKEN = 1e-4
+ELEM = 1e-4
+
+
+def max_elem_err(got2d, ref2d) -> float:
+    """max over tokens of max |got - ref| / max |ref| (0 / 0 counts as 0)."""
+    worst = 0.0
+    for g, r in zip(np.asarray(got2d, np.float64), np.asarray(ref2d, np.float64)):
+        m = np.max(np.abs(r)) if r.size else 0.0
+        e = np.max(np.abs(g - r)) if r.size else 0.0
+        worst = max(worst, e / m if m > 0 else (0.0 if e == 0 else np.inf))
+    return worst
 
 
 @functools.lru_cache(maxsize=2)
@@ -204,6 +218,22 @@ def test_fp16_weights(B, d, xdt):
         assert max_rel_l2(per, want) <= ALARM_PER_TOKEN
 
 
+@pytest.mark.parametrize("B,d", [(1, 4096), (1, 5120), (3, 1000), (1, 12296), (2, 16384)])
+def test_bf16_weights_f32_x(B, d):
+    """bf16 weights with float32 x (the per-token path takes the pair at every batch size)."""
+    N, L = 700, 530
+    say(f"bf16 weights, f32 x: B={B} d={d}")
+    rng, draw, ref, gpu = _rand_problem(B * 13 + d, N, d, L, "bf16")
+    ks = [300, 0, 17][:B]
+    sets = [rng.permutation(L)[:k].astype(np.int32) for k in ks]
+    x = rng.standard_normal((B, d)).astype(np.float32)
+    want = _oracle(x, sets, ref)
+    got = _run(x, sets, gpu)
+    assert max_rel_l2(got, want) <= ALARM_PER_TOKEN and max_elem_err(got, want) <= ELEM
+    if B > 1:
+        assert not np.any(got[1])
+
+
 def test_invalid_slots_add_nothing():
     """Without SI_FLAG_CHECK an invalid slot id (negative or >= L) in a set is skipped: the result
     is the FFN over the valid slots, on the per-token and the union path."""
@@ -227,28 +257,42 @@ def test_llama2_7b_batch16_union():
         slots = _slots(ref, active_sets(cfg, toks))
         want = _oracle(x, slots, ref)
         got = _run(x, slots, gpu)
-        err = max_rel_l2(got, want)
-        say(f"union step {step} max rel L2 {err:.3e}")
-        assert err <= TOL["bf16"]
+        err, elem = max_rel_l2(got, want), max_elem_err(got, want)
+        say(f"union step {step} max rel L2 {err:.3e}, element-wise {elem:.3e}")
+        assert err <= ALARM_PER_TOKEN and elem <= ELEM
         per_tok = _run(x, slots, gpu, flags=si.FLAG_PER_TOKEN)
         assert max_rel_l2(per_tok, want) <= ALARM_PER_TOKEN
-        assert max_rel_l2(got, per_tok) <= TOL["bf16"]
+        assert max_elem_err(per_tok, want) <= ELEM
+        fast = _run(x, slots, gpu, flags=si.FLAG_FAST_H)
+        errf = max_rel_l2(fast, want)
+        say(f"union step {step} fast-h max rel L2 {errf:.3e}")
+        assert errf <= TOL["bf16"]
 
 
-def test_llama2_13b_prefill_union_sampled():
+def test_llama2_13b_prefill_union_all_tokens():
+    """All 512 tokens of the union call against the per-token path, and 64 of them (every
+    eighth) against the oracle directly, which also pins the per-token path at this shape."""
     cfg, ref, gpu = _layer("llama2_13b_prefill")
-    say("13B prefill: 512 tokens in one union call, 12 tokens checked")
+    say("13B prefill: 512 tokens in one union call; all against the per-token path, 64 "
+        "against the oracle")
     toks = range(cfg.B)
     x = tokens_x(cfg, toks)
     slots = _slots(ref, active_sets(cfg, toks))
     got = _run(x, slots, gpu)
-    sample = [0, 1, 77, 128, 255, 256, 300, 383, 384, 500, 510, 511]
+    per_tok = _run(x, slots, gpu, flags=si.FLAG_PER_TOKEN)
+    sample = list(range(0, cfg.B, 8))
     want = _oracle(x[sample], [slots[t] for t in sample], ref)
-    err = max_rel_l2(got[sample], want)
-    say(f"13B prefill max rel L2 {err:.3e}")
-    assert err <= TOL["bf16"]
-    # every token's output is finite and nonzero
-    assert np.all(np.isfinite(got)) and np.all(np.abs(got).sum(axis=1) > 0)
+    e_per = max_rel_l2(per_tok[sample], want)
+    assert e_per <= ALARM_PER_TOKEN and max_elem_err(per_tok[sample], want) <= ELEM
+    err, elem = max_rel_l2(got[sample], want), max_elem_err(got[sample], want)
+    say(f"13B prefill vs oracle ({len(sample)} tokens): union {err:.3e} (element-wise "
+        f"{elem:.3e}), per-token {e_per:.3e}")
+    assert err <= ALARM_PER_TOKEN and elem <= ELEM
+    err_all, elem_all = max_rel_l2(got, per_tok), max_elem_err(got, per_tok)
+    say(f"13B prefill vs per-token (512 tokens): {err_all:.3e} (element-wise {elem_all:.3e})")
+    assert err_all <= ALARM_PER_TOKEN and elem_all <= ELEM
+    fast = _run(x, slots, gpu, flags=si.FLAG_FAST_H)
+    assert max_rel_l2(fast[sample], want) <= TOL["bf16"]
 
 
 def test_llama3_8b_stack_teacher_forced():
@@ -289,9 +333,13 @@ def _check_resnorm(xp, yp, sets, ref, gpu, xdtype, wdtype, flags=0):
     for b in range(len(sets)):
         assert rel_l2(x_got[b], _resnorm_ref(xp[b], yp[b], xdtype)) <= (
             5e-3 if xdtype == "bf16" else 1e-6)
-    # the pair of calls it replaces
+    # the pair of calls it replaces (equal up to the summation order of the mean square: a
+    # bf16 x_out may differ by one unit where r / rms falls next to a rounding boundary)
     x_pair = host_array(si.residual_rmsnorm(dev_tensor(xp), dev_tensor(yp)))
-    assert np.mean(xo_h == x_pair) > 0.99
+    if xdtype == "bf16":
+        assert np.mean(xo_h == x_pair) > 0.99
+    else:
+        assert max_rel_l2(xo_h, x_pair) <= 1e-6
     want = _oracle(xo_h, sets, ref)
     tol = ALARM_PER_TOKEN if wdtype == "bf16" else TOL["f32"]
     assert max_rel_l2(y_h, want) <= tol
@@ -318,7 +366,10 @@ def test_llama3_8b_stack_resnorm_fused():
 @pytest.mark.parametrize("B,d,wdtype,xdtype", [(1, 4104, "bf16", "bf16"), (2, 1000, "bf16", "bf16"),
                                                (3, 264, "f32", "f32"), (1, 8, "bf16", "bf16"),
                                                (2, 2052, "f32", "f32"), (2, 1000, "f32", "bf16"),
-                                               (4, 512, "bf16", "bf16")])
+                                               (4, 512, "bf16", "bf16"), (1, 5120, "bf16", "bf16"),
+                                               (2, 5120, "bf16", "f32"), (1, 8200, "bf16", "f32"),
+                                               (1, 12296, "bf16", "bf16"),
+                                               (1, 16384, "bf16", "bf16")])
 def test_selective_ffn_resnorm(B, d, wdtype, xdtype):
     """Per-token path with the prologue (B < 5; f32 weights at any B; SI_FLAG_PER_TOKEN), a
     token with an empty set (its x_out is still written), ragged d, and the union path (bf16
@@ -388,6 +439,18 @@ def test_check_flag_and_errors():
         with pytest.raises(si.SelectInferError) as e:
             si.selective_ffn(x, dev_tensor(off), dev_tensor(idx), gpu.gate_up_c, gpu.down_c,
                              flags=si.FLAG_CHECK)
+        assert e.value.status == code
+    # SI_FLAG_SORTED: ascending lists pass the check, others are refused
+    off, idx = csr_from_sets(good)
+    y = si.selective_ffn(x, dev_tensor(off), dev_tensor(idx), gpu.gate_up_c, gpu.down_c,
+                         flags=si.FLAG_CHECK | si.FLAG_SORTED)
+    assert max_rel_l2(host_array(y), _oracle(host_array(x), good, ref)) <= TOL["bf16"]
+    for code, sets in {1: [np.array([1, 9, 5], np.int32), np.array([2], np.int32)],
+                       3: [np.array([1, 5, 5], np.int32), np.array([2], np.int32)]}.items():
+        off, idx = csr_from_sets(sets)
+        with pytest.raises(si.SelectInferError) as e:
+            si.selective_ffn(x, dev_tensor(off), dev_tensor(idx), gpu.gate_up_c, gpu.down_c,
+                             flags=si.FLAG_CHECK | si.FLAG_SORTED)
         assert e.value.status == code
     bad_off = dev_tensor(np.array([0, 3, 2], np.int32))
     with pytest.raises(si.SelectInferError) as e:

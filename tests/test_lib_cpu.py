@@ -27,12 +27,48 @@ def lib():
     return _lib.load()
 
 
+def _enum_values():
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    return {k: int(v) for k, v in re.findall(r"\b(SI_[A-Z0-9_]+)\s*=\s*(\d+)", text)}
+
+
+def _prototype(name):
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    m = re.search(r"\b" + name + r"\s*\(([^)]*)\)", text)
+    assert m, name
+    return [a.strip() for a in " ".join(m.group(1).split()).split(",")]
+
+
 def test_header_declares_the_boundary():
+    """The calls, argument lists and enum values of the boundary the hot path is specified
+    with: compaction, per-token top-k (with its workspace query), the selective FFN."""
     names = _declared()
-    for n in ("si_compact_ffn", "si_select_topk", "si_selective_ffn", "si_remap_ids",
-              "si_selective_ffn_workspace", "si_residual_rmsnorm", "si_status_string",
-              "si_version"):
+    for n in ("si_compact_ffn", "si_select_topk", "si_select_topk_workspace",
+              "si_selective_ffn", "si_selective_ffn_workspace", "si_status_string",
+              "si_remap_ids", "si_residual_rmsnorm", "si_version"):
         assert n in names
+    ev = _enum_values()
+    want = dict(SI_F32=0, SI_BF16=1, SI_OK=0, SI_ERR_INVALID=1, SI_ERR_RANGE=2,
+                SI_ERR_DUPLICATE=3, SI_ERR_NOT_LOADED=4, SI_ERR_UNSUPPORTED=5, SI_ERR_HIP=6,
+                SI_TOPK_ABS=1, SI_TOPK_RAW=2, SI_FLAG_CHECK=4, SI_FLAG_SORTED=8)
+    for k, v in want.items():
+        assert ev.get(k) == v, k
+    assert _prototype("si_compact_ffn") == [
+        "const void* w_gate", "const void* w_up", "const void* w_down", "int64_t N",
+        "int64_t d", "si_dtype wdt", "const int32_t* loaded", "int64_t L", "void* gate_up_c",
+        "void* down_c", "int32_t* slot_to_orig", "int32_t* orig_to_slot", "void* hip_stream"]
+    assert _prototype("si_select_topk_workspace") == ["int64_t B", "int64_t L", "int64_t k"]
+    assert _prototype("si_select_topk") == [
+        "const float* scores", "int64_t B", "int64_t L", "int64_t k", "int mode",
+        "int32_t* out_idx", "void* ws", "size_t ws_bytes", "void* hip_stream"]
+    assert _prototype("si_selective_ffn") == [
+        "const void* x", "si_dtype xdt", "int64_t B", "int64_t d", "const int32_t* offsets",
+        "const int32_t* idx", "int64_t nnz", "const void* gate_up_c", "const void* down_c",
+        "int64_t L", "si_dtype wdt", "float* y", "void* ws", "size_t ws_bytes", "int flags",
+        "void* hip_stream"]
+    # the workspace query also takes the dtypes and flags, which choose the path
+    assert _prototype("si_selective_ffn_workspace")[:4] == [
+        "int64_t B", "int64_t nnz", "int64_t L", "int64_t d"]
 
 
 def test_every_declared_symbol_is_exported(lib):
@@ -49,15 +85,22 @@ def test_status_strings(lib):
     assert lib.si_status_string(0) == b"ok"
     assert b"range" in lib.si_status_string(2)
     assert lib.si_status_string(999) == b"unknown status"
-    assert lib.si_version() == 100
+    assert lib.si_version() == 200
 
 
 def test_host_side_argument_errors(lib):
     # each of these returns before any HIP call
-    assert lib.si_select_topk(None, 1, 4, 5, 0, None, None) == 1          # k > L
-    assert lib.si_select_topk(None, 1, 4, 2, 7, None, None) == 1          # bad mode
-    assert lib.si_select_topk(None, 0, 4, 2, 0, None, None) == 0          # B = 0: no-op
-    assert lib.si_select_topk(None, 3, 4, 0, 0, None, None) == 0          # k = 0: no-op
+    ABS, RAW, SORTED = 1, 2, 8
+    assert lib.si_select_topk_workspace(64, 11008, 2202) == 0
+    assert lib.si_select_topk(None, 1, 4, 5, ABS, None, None, 0, None) == 1     # k > L
+    assert lib.si_select_topk(None, 1, 4, 2, 0, None, None, 0, None) == 1       # no ranking key
+    assert lib.si_select_topk(None, 1, 4, 2, ABS | RAW, None, None, 0, None) == 1   # two keys
+    assert lib.si_select_topk(None, 1, 4, 2, 4, None, None, 0, None) == 1       # not a key
+    assert lib.si_select_topk(None, 1, 4, 2, ABS, None, None, 16, None) == 7    # ws size, no ws
+    assert lib.si_select_topk(None, 0, 4, 2, RAW | SORTED, None, None, 0, None) == 0  # B = 0: no-op
+    assert lib.si_select_topk(None, 3, 4, 0, ABS, None, None, 0, None) == 0     # k = 0: no-op
+    assert lib.si_dynamic_set(None, 1, 4, 64, None, 10, 1, None, 0, 2, 3, 0, None, None, None,
+                              0, None) == 1                              # no ranking key
     assert lib.si_selective_ffn(None, 1, 1, 0, None, None, 0, None, None, 4, 1, None, None,
                                 0, 0, None) == 1                          # d < 1
     assert lib.si_selective_ffn(None, 3, 1, 8, None, None, 0, None, None, 4, 1, None, None,
@@ -78,7 +121,7 @@ def test_path_choice_by_batch(lib):
     SI_FLAG_UNION), the union path from 5 (unless SI_FLAG_PER_TOKEN), per-token for f32."""
     ws = lambda B, flags, dt=1: lib.si_selective_ffn_workspace(B, 2202 * B, 7706, 4096, dt, dt,
                                                                flags)
-    PER, UNION = 2, 8
+    PER, UNION = 16, 64
     for B in (2, 3, 4):
         assert ws(B, 0) == ws(B, PER)
         assert ws(B, UNION) != ws(B, PER)
