@@ -6,18 +6,23 @@ N=11008, 70% of neurons loaded (L=7706), 20% active per token (k=2202), batch-1 
 1024-token sequence. One step = one token through one compacted layer, i.e. one
 si_selective_ffn call. Inputs are seeded synthetic data resident in HBM before timing starts.
 
-Reported: tokens/s per layer (whole job, one GPU), and for the main weight-streaming kernel the
+Reported: tokens/s per layer (whole job, one GPU); for the main weight-streaming kernel the
 achieved HBM bandwidth on the bytes the method touches (active rows x 3 matrices x d x 2 B),
-measured with HIP events around that kernel in every timed step, against the 8 TB/s peak.
-The oracle (fp64 NumPy, host) is timed on a bounded sample of the same workload.
+measured with HIP events stamped by that kernel's own dispatch, against the 8 TB/s peak; the
+same bytes over the whole call's step time (roofline.call). The oracle (fp64 NumPy, host) is
+timed first, before any HIP call, on one thread and then on forked worker processes over the
+host's cores, on a bounded sample of the same workload; its outputs for that sample are what
+the GPU's outputs are checked against.
 
-Other workloads (``--workload``) are available for measurement: tiny_f32, llama2_7b_b16
-(batch 16, union MFMA path), llama3_8b_stack (32 layers, residual RMSNorm between layers),
-llama2_13b_prefill (512 tokens, MFMA-bound union path); and the selection steps around the
-path: dynset_llama2_13b (dynamic-set construction for a 512-token prompt on the 13B-shape
-layer, si_dynamic_set), profile_llama3_8b (Eq. 1 scores of 512 tokens over a full
-8B-shape FFN layer, si_profile_scores) and load_llama2_7b (selective loading of the 7B-shape
-layer from host memory, si_load_selected).
+Other workloads (``--workload``): tiny_f32, llama2_7b_b16 (batch 16, union MFMA path),
+llama3_8b_stack (32 layers, residual RMSNorm between layers), llama2_13b_prefill (512 tokens,
+MFMA-bound union path); the selection steps around the path: dynset_llama2_13b (dynamic-set
+construction for a 512-token prompt on the 13B-shape layer, si_dynamic_set),
+profile_llama3_8b (Eq. 1 scores of 512 tokens over a full 8B-shape FFN layer,
+si_profile_scores) and load_llama2_7b (selective loading of the 7B-shape layer from host
+memory, si_load_selected); and the memory-system references of the decode step:
+stream_llama2_7b (a contiguous read of the step's bytes) and gather_llama2_7b (the step's own
+row gather without arithmetic).
 """
 from __future__ import annotations
 
@@ -48,7 +53,14 @@ def parse_args():
                     help="resident copies of the compacted layer, rotated per step so that a "
                          "repeated step cannot be served from the 256 MB Infinity Cache")
     ap.add_argument("--no-graph", action="store_true", help="launch steps eagerly")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="single-thread oracle time (the all-core run takes a sample that "
+                         "many times larger as there are workers)")
+    ap.add_argument("--cpu-workers", type=int, default=16,
+                    help="oracle worker processes for the all-core run (capped at the CPUs "
+                         "this process may run on)")
+    ap.add_argument("--ceiling-blocks", type=int, default=1024,
+                    help="work-groups of the contiguous-read reference")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--timed-launches", type=int, default=256,
                     help="steps whose main kernel is timed with HIP events")
@@ -213,6 +225,11 @@ class Workload:
         rows = self.union_rows[step % cfg.steps]
         return 2.0 * 3 * cfg.B * rows * cfg.d
 
+    def launch_useful_flops(self, step):
+        """Flops of the tokens' own active rows in one launch: 2 * 3 * d per (token, row)."""
+        cfg = self.cfg
+        return 2.0 * 3 * cfg.B * cfg.k * cfg.d
+
 
 # --------------------------------------------------------------------------------------------
 def run_gpu(work, steps, warmup, use_graph, timed_launches):
@@ -278,52 +295,154 @@ def run_gpu(work, steps, warmup, use_graph, timed_launches):
     return wall, kern_ms, graph is not None, list(range(warmup, warmup + n))
 
 
-def check_outputs(work, tokens):
-    """Recompute a few timed tokens with the oracle and return the worst relative L2."""
-    import numpy as np
+# --------------------------------------------------------------------------------------------
+# CPU leg: the oracle as it stands, timed on the host cores before the GPU is touched (its
+# worker processes are forked then, from a process that has made no HIP call). Its outputs for
+# the sampled tokens are the reference the GPU's outputs are checked against afterwards.
+# --------------------------------------------------------------------------------------------
+_CPU = {}          # inputs the forked workers inherit
 
+
+def _cpu_info():
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"cpu_model": model, "os_cpu_count": os.cpu_count(),
+            "affinity_cpus": len(os.sched_getaffinity(0))}
+
+
+def _one_thread():
+    from threadpoolctl import threadpool_limits
+    threadpool_limits(limits=1)
+
+
+def _oracle_token(t):
+    """One token of a one-layer workload: id remap + fp64 selective FFN."""
     import oracle
-
-    cfg = work.cfg
-    if cfg.layers > 1:
-        return None
-    wg, wu, wd, loaded = work.host[0]
-    ref = oracle.compact(wg, wu, wd, loaded)
-    y = work.y.cpu().numpy()
-    worst = 0.0
-    for t in tokens:
-        slots = oracle.remap(ref["orig_to_slot"], work.sets_host[0][t])
-        want = oracle.selective_ffn(work.x_host[t], slots, ref["gate_up_c"], ref["down_c"])
-        err = float(np.linalg.norm(y[t] - want) / max(np.linalg.norm(want), 1e-300))
-        worst = max(worst, err)
-    return worst, ref
+    st = _CPU
+    slots = oracle.remap(st["ref"]["orig_to_slot"], st["sets"][t])
+    return t, oracle.selective_ffn(st["x"][t], slots, st["ref"]["gate_up_c"],
+                                   st["ref"]["down_c"])
 
 
-def cpu_baseline(work, ref, seconds):
-    """Time the oracle (as is) on the host, one token at a time, for about `seconds`."""
+def _oracle_chain(t):
+    """One token through every layer of the stack, free-running: x_{l+1} = RMSNorm(x_l + y_l)
+    in bf16; returns the last layer's y."""
+    import oracle
+    st = _CPU
+    x = st["x"][t]
+    y = None
+    for lay, ref in enumerate(st["refs"]):
+        if lay > 0:
+            x = oracle.residual_rmsnorm_bf16(x, y)
+        slots = oracle.remap(ref["orig_to_slot"], st["sets"][lay][t])
+        y = oracle.selective_ffn(x, slots, ref["gate_up_c"], ref["down_c"])
+    return t, y
+
+
+# sample sizes: at least these many tokens (the stack: token chains through all layers)
+CPU_MIN_SAMPLE = {"tiny_f32": 64, "llama2_7b_decode": 32, "llama2_7b_b16": 32,
+                  "llama3_8b_stack": 4, "llama2_13b_prefill": 32}
+
+
+def cpu_leg(cfg, seconds, workers):
+    """Time the oracle on one thread (BLAS limited to one thread), in token order, for about
+    `seconds` (at least the minimum sample), then on `workers` forked processes of one thread
+    each over a sample that many times larger. Returns (cpu_baseline record, {token: y})."""
+    import multiprocessing as mp
+
     import numpy as np
     from threadpoolctl import threadpool_limits
 
     import oracle
+    from workloads import active_sets, layer_weights, loaded_ids, tokens_x
 
-    cfg = work.cfg
-    n = 0
+    T = cfg.steps * cfg.B
+    n_min = min(T, CPU_MIN_SAMPLE.get(cfg.name, 8))
+    t_prep = time.perf_counter()
+    if cfg.layers == 1:
+        wg, wu, wd = layer_weights(cfg, 0)
+        _CPU["ref"] = oracle.compact(wg, wu, wd, loaded_ids(cfg, 0))
+        del wg, wu, wd
+        fn, span = _oracle_token, T
+    else:
+        refs = []
+        for lay in range(cfg.layers):
+            wg, wu, wd = layer_weights(cfg, lay)
+            refs.append(oracle.compact(wg, wu, wd, loaded_ids(cfg, lay)))
+            del wg, wu, wd
+        _CPU["refs"] = refs
+        fn, span = _oracle_chain, min(T, max(n_min, 4 * workers))
+    n_cap = span if cfg.layers == 1 else n_min
+    _CPU["x"] = tokens_x(cfg, range(span))
+    _CPU["sets"] = (active_sets(cfg, range(span)) if cfg.layers == 1 else
+                    [active_sets(cfg, range(span), lay) for lay in range(cfg.layers)])
+    log(f"CPU leg: oracle inputs ready in {time.perf_counter() - t_prep:.1f}s")
+    outputs = {}
     with threadpool_limits(limits=1):
         t0 = time.perf_counter()
-        while n < work.T and time.perf_counter() - t0 < seconds:
-            slots = oracle.remap(ref["orig_to_slot"], work.sets_host[0][n])
-            oracle.selective_ffn(work.x_host[n], slots, ref["gate_up_c"], ref["down_c"])
-            n += 1
-        el = time.perf_counter() - t0
-    return {
-        "value": n / el,
-        "unit": "tokens/s/layer",
-        "cores": 1,
-        "kind": "oracle",
-        "sample": f"first {n} of the workload's {work.T} tokens, one si_selective_ffn-equivalent "
-                  f"oracle call each (id remap + fp64 NumPy selective FFN), single thread, "
-                  f"{el:.1f} s on {os.cpu_count()} visible host CPUs",
+        n1 = 0
+        while n1 < n_cap and (n1 < n_min or time.perf_counter() - t0 < seconds):
+            t, y = fn(n1)
+            outputs[t] = y
+            n1 += 1
+        el1 = time.perf_counter() - t0
+    rate1 = n1 * cfg.layers / el1
+    n_all = min(span, max(n_min, n1 * workers))
+    ctx = mp.get_context("fork")
+    with ctx.Pool(workers, initializer=_one_thread) as pool:
+        t0 = time.perf_counter()
+        res = pool.map(fn, range(n_all), chunksize=max(1, n_all // (4 * workers)))
+        el_all = time.perf_counter() - t0
+    for t, y in res:
+        if t in outputs and not np.array_equal(outputs[t], y):
+            raise RuntimeError(f"oracle is not deterministic on token {t}")
+        outputs[t] = y
+    _CPU.clear()
+    what = ("id remap + fp64 NumPy selective FFN per token" if cfg.layers == 1 else
+            f"one token through all {cfg.layers} layers (id remap, fp64 selective FFN, "
+            "residual RMSNorm to bf16), free-running")
+    unit = "tokens/s/layer"
+    info = _cpu_info()
+    rec = {
+        "value": n_all * cfg.layers / el_all, "unit": unit, "cores": workers, "kind": "oracle",
+        "sample": f"tokens 0..{n_all - 1} of the workload's {T}: {what}; {workers} forked "
+                  f"processes with one BLAS thread each, {el_all:.1f} s wall",
+        "single_thread": {"value": rate1, "unit": unit, "cores": 1,
+                          "sample": f"tokens 0..{n1 - 1}, one thread, {el1:.1f} s"},
+        **info,
     }
+    log(f"CPU leg: oracle {rate1:.1f} {unit} on one thread, {rec['value']:.1f} on {workers}")
+    return rec, outputs
+
+
+def parity_from_oracle(work, outputs, tol):
+    """The GPU's outputs of the tokens the CPU leg computed against the oracle's."""
+    import numpy as np
+
+    cfg = work.cfg
+    y = work.y.cpu().numpy()
+    worst = 0.0
+    for t, want in outputs.items():
+        if t >= y.shape[0]:
+            continue
+        n = np.linalg.norm(want)
+        err = float(np.linalg.norm(y[t] - want) / n) if n > 0 else float(np.linalg.norm(y[t]))
+        worst = max(worst, err)
+    rec = {"tokens_checked": len(outputs), "max_rel_l2": worst, "tol": tol}
+    if cfg.layers > 1:
+        # free-running through the stack: reported for information, not held to a bound
+        rec = {"tokens_checked": len(outputs), "free_running_last_layer_rel_l2": worst,
+               "layers": cfg.layers,
+               "note": "the oracle's chain takes its own bf16 x at every layer; per-layer "
+                       "parity (teacher-forced) is held to the tolerance in the tests"}
+    return rec
 
 
 def traffic_record(workload):
@@ -408,7 +527,7 @@ class SelectWork:
             need = int(si._lib.load().si_dynamic_set_workspace(self.T, self.L, self.alpha,
                                                                 self.n_total))
         else:
-            self.scores = torch.zeros(N, dtype=torch.float32, device=dev)
+            self.scores = torch.zeros(N, dtype=torch.float64, device=dev)
             need = int(si._lib.load().si_profile_scores_workspace(self.T, N, d, si.BF16,
                                                                    si.BF16))
         self.ws = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
@@ -431,7 +550,9 @@ class SelectWork:
         """MFMA flops of the activation GEMM: gate and up rows of every slot, every token."""
         return 2.0 * self.T * 2 * self.L * self.d
 
-    def check(self):
+    def check(self, ref=None):
+        """Dynamic set: validity of the result against its own counts. Scores: the GPU's
+        scores of the tokens the CPU leg scored (ref = (n, oracle scores)) against them."""
         np = self.np
         if self.kind == "dynset":
             out = self.out.cpu().numpy()
@@ -447,16 +568,16 @@ class SelectWork:
                     ok = min((cnt[j], -j) for j in dyn) > max((cnt[j], -j) for j in rest)
             return {"valid": bool(ok), "checks": "size, ascending, static included, counts sum "
                     "to T*alpha, dynamic slots the most frequent (ties to the lower slot)"}
-        # scores of a 16-token sample against the oracle
-        import oracle
-        wg, wu, wd, loaded = self.host
-        ref = oracle.compact(wg, wu, wd, loaded)
-        want, _ = oracle.profile_scores(self.x_host[:16], ref["gate_up_c"])
-        got = self.si.profile_scores(self.x[:16], self.gu[0]).cpu().numpy().astype(np.float64)
+        if ref is None:
+            return None
+        n, want = ref
+        got = self.si.profile_scores(self.x[:n], self.gu[0]).cpu().numpy()
         err = float(np.linalg.norm(got - want) / np.linalg.norm(want))
-        return {"tokens_checked": 16, "max_rel_l2": err, "tol": 1e-5, "valid": err <= 1e-5}
+        return {"tokens_checked": n, "max_rel_l2": err, "tol": 1e-5, "valid": err <= 1e-5}
 
     def cpu_baseline(self, seconds):
+        """The oracle on one thread over the first n prompt tokens (n doubling until about a
+        third of `seconds`); returns (record, (n, its Eq. 1 scores) or None)."""
         from threadpoolctl import threadpool_limits
 
         import oracle
@@ -469,8 +590,9 @@ class SelectWork:
                 if self.kind == "dynset":
                     oracle.dynamic_set(self.x_host[:n], ref["gate_up_c"], self.static_host,
                                        self.alpha, self.n_total)
+                    out = None
                 else:
-                    oracle.profile_scores(self.x_host[:n], ref["gate_up_c"])
+                    out = (n, oracle.profile_scores(self.x_host[:n], ref["gate_up_c"])[0])
                 el = time.perf_counter() - t0
                 if el >= seconds / 3 or n >= self.T:
                     break
@@ -478,8 +600,7 @@ class SelectWork:
         what = "si_dynamic_set-equivalent" if self.kind == "dynset" else "Eq. 1 scores"
         return {"value": n / el, "unit": "prompt tokens/s/layer", "cores": 1, "kind": "oracle",
                 "sample": f"first {n} of the {self.T} prompt tokens, one {what} oracle call "
-                          f"(fp64 NumPy), single thread, {el:.1f} s on {os.cpu_count()} "
-                          f"visible host CPUs"}
+                          f"(fp64 NumPy), single thread, {el:.1f} s", **_cpu_info()}, out
 
 
 def main_select(args):
@@ -502,11 +623,11 @@ def main_select(args):
             "kernel_ms_mean": float(kern_ms.mean()), "kernel_ms_p50": float(np.median(kern_ms)),
             "kernel_launches_timed": int(len(kern_ms)), "flops_per_launch": flops}
     torch.cuda.synchronize()
-    parity = work.check()
-    if not parity["valid"]:
+    cpu, ref = (None, None) if args.no_cpu_baseline else work.cpu_baseline(args.cpu_seconds)
+    parity = work.check(ref)
+    if parity is not None and not parity["valid"]:
         log(f"PARITY FAILURE: {parity}")
         sys.exit(1)
-    cpu = None if args.no_cpu_baseline else work.cpu_baseline(args.cpu_seconds)
     out = {
         "metric": ("dynamic-set construction prompt tokens/s per layer" if work.kind == "dynset"
                    else "profiler scoring (Eq. 1) tokens/s per layer"),
@@ -573,25 +694,25 @@ def main_load(args):
         dst.copy_(src, non_blocking=True)
     torch.cuda.synchronize()
     ceil = 3 * moved / (time.perf_counter() - t0) / 1e9
-    # parity: the loaded layer against the oracle's compaction, bit for bit
-    import oracle
-    ref = oracle.compact(wg, wu, wd, loaded)
-    layer = si.load_selected(wg, wu, wd, loaded)
-    ok = all(np.array_equal(a, b) for a, b in (
-        (layer.gate_up_c.view(torch.int16).cpu().numpy().view(np.uint16), ref["gate_up_c"]),
-        (layer.down_c.view(torch.int16).cpu().numpy().view(np.uint16), ref["down_c"]),
-        (layer.slot_to_orig.cpu().numpy(), ref["slot_to_orig"])))
-    if not ok:
-        log("PARITY FAILURE: loaded layer differs from the oracle's compaction")
-        sys.exit(1)
-    cpu = None
+    # CPU leg: the oracle's compaction, timed; then the loaded layer against it, bit for bit
+    cpu, parity = None, None
     if not args.no_cpu_baseline:
+        import oracle
         t0 = time.perf_counter()
-        oracle.compact(wg, wu, wd, loaded)
+        ref = oracle.compact(wg, wu, wd, loaded)
         el = time.perf_counter() - t0
         cpu = {"value": moved / el / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
-               "sample": f"one oracle compaction of the whole layer (Python loop over the {len(loaded)} "
-                         f"slots, host memory only), {el:.1f} s"}
+               "sample": f"one oracle compaction of the whole layer (Python loop over the "
+                         f"{len(loaded)} slots, host memory only), {el:.1f} s", **_cpu_info()}
+        layer = si.load_selected(wg, wu, wd, loaded)
+        ok = all(np.array_equal(a, b) for a, b in (
+            (layer.gate_up_c.view(torch.int16).cpu().numpy().view(np.uint16), ref["gate_up_c"]),
+            (layer.down_c.view(torch.int16).cpu().numpy().view(np.uint16), ref["down_c"]),
+            (layer.slot_to_orig.cpu().numpy(), ref["slot_to_orig"])))
+        if not ok:
+            log("PARITY FAILURE: loaded layer differs from the oracle's compaction")
+            sys.exit(1)
+        parity = {"bit_exact": True}
     out = {
         "metric": "selective loading of one FFN layer from host memory, compacted GB/s",
         "value": gbs, "unit": "GB/s", "n_gpus": 1, "steps": steps, "warmup": 2,
@@ -605,9 +726,106 @@ def main_load(args):
                      "frac": gbs / PCIE_PEAK_GBS, "traffic": None,
                      "measured_h2d_copy_gbs": ceil, "bytes_per_launch": moved},
         "cpu_baseline": cpu,
-        "parity": {"bit_exact": True},
+        "parity": parity,
     }
     print(json.dumps(out), flush=True)
+
+
+# --------------------------------------------------------------------------------------------
+# Memory-system references of the 7B decode step (measurement only)
+# --------------------------------------------------------------------------------------------
+CEILING_WORKLOADS = {
+    # a contiguous read of the bytes one decode step touches (k rows x 3 x d x 2 B)
+    "stream_llama2_7b": ("stream", "llama2_7b_decode"),
+    # the decode step's own row gather (same slots, same work-group split), no arithmetic
+    "gather_llama2_7b": ("gather", "llama2_7b_decode"),
+}
+
+
+class CeilingWork:
+    """Steps of a memory-system reference; rotates `copies` buffers (or layer copies) as the
+    decode workload does, so no step is served from the Infinity Cache."""
+
+    def __init__(self, kind, cfg, copies, dev, blocks):
+        import torch
+
+        import paper_2607_18081_amd as si
+        self.si, self.kind, self.cfg = si, kind, cfg
+        self.nbytes = cfg.k * 3 * cfg.d * (2 if cfg.wdtype == "bf16" else 4)
+        self.blocks = blocks
+        if kind == "stream":
+            self.bufs = [torch.zeros(self.nbytes, dtype=torch.uint8, device=dev)
+                         for _ in range(copies)]
+            nsink = blocks
+        else:
+            self.w = Workload(cfg, copies, dev)
+            self.P = min(cfg.k, torch.cuda.get_device_properties(dev).multi_processor_count)
+            nsink = self.P
+        self.sink = torch.empty(nsink * 512, dtype=torch.int32, device=dev)
+        self.copies = copies
+
+    def launch(self, step, timing=None):
+        si = self.si
+        if timing:
+            _settle()
+            si.set_timing_events(*timing[0])
+        if self.kind == "stream":
+            si.ceiling_stream(self.bufs[step % self.copies], self.blocks, self.sink)
+        else:
+            w = self.w
+            cp = w.layers[0][step % len(w.layers[0])]
+            si.ceiling_gather(cp.gate_up_c, cp.down_c, w._slots(0, step % self.cfg.steps), self.P,
+                              self.sink)
+        if timing:
+            si.set_timing_events(None, None)
+
+    def launch_bytes(self, step):
+        return self.nbytes
+
+
+def main_ceiling(args):
+    import numpy as np
+    import torch
+
+    from workloads import CONFIGS
+
+    kind, base = CEILING_WORKLOADS[args.workload]
+    cfg = CONFIGS[base]
+    steps = args.steps if args.steps is not None else cfg.steps
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    work = CeilingWork(kind, cfg, args.copies, dev, args.ceiling_blocks)
+    log(f"workload {args.workload}: {work.nbytes} bytes per step, {args.copies} copies")
+    wall, kern_ms, graphed, launches = run_gpu(work, steps, args.warmup, not args.no_graph,
+                                               args.timed_launches)
+    kern_ms = np.array(kern_ms)
+    achieved = work.nbytes / (kern_ms.mean() * 1e-3) / 1e9
+    step_s = wall / steps
+    out = {
+        "metric": "memory-system reference for the decode step: GB/s read",
+        "value": work.nbytes / step_s / 1e9, "unit": "GB/s", "n_gpus": 1, "steps": steps,
+        "warmup": args.warmup, "ms_per_step": step_s * 1e3, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "u8" if kind == "stream" else "bf16",
+        "data": "synthetic (the 7B decode workload's compacted layer copies and slots)"
+                if kind == "gather" else "zero-filled device buffers",
+        "config": {"workload": args.workload, "reference_for": base,
+                   "bytes_per_step": work.nbytes, "copies": args.copies,
+                   "work_groups": work.blocks if kind == "stream" else work.P,
+                   "hip_graph": graphed, "parallelism": "single GPU"},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "kernel_ms_mean": float(kern_ms.mean()),
+                     "kernel_ms_p50": float(np.median(kern_ms)),
+                     "kernel_launches_timed": int(len(kern_ms)),
+                     "bytes_per_launch": work.nbytes},
+        "cpu_baseline": None,
+        "parity": None,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def cpu_workers(args):
+    return max(1, min(args.cpu_workers, len(os.sched_getaffinity(0))))
 
 
 def main():
@@ -627,14 +845,19 @@ def main():
         return main_select(args)
     if args.workload in LOAD_WORKLOADS:
         return main_load(args)
+    if args.workload in CEILING_WORKLOADS:
+        return main_ceiling(args)
     cfg = CONFIGS[args.workload]
     steps = args.steps if args.steps is not None else (
         cfg.steps if cfg.B == 1 and cfg.layers == 1 else (64 if cfg.layers > 1 else
                                                           max(cfg.steps, 16)))
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
     log(f"workload {cfg.name}: d={cfg.d} N={cfg.N} L={cfg.L} k={cfg.k} B={cfg.B} "
         f"layers={cfg.layers} {cfg.wdtype}; steps={steps} warmup={args.warmup}")
+    # the CPU leg first: its worker processes are forked before any HIP call
+    cpu, ref_out = (None, None) if args.no_cpu_baseline else cpu_leg(
+        cfg, args.cpu_seconds, cpu_workers(args))
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
     work = Workload(cfg, args.copies, dev)
     wall, kern_ms, graphed, launches = run_gpu(work, steps, args.warmup, not args.no_graph,
                                                args.timed_launches)
@@ -642,40 +865,64 @@ def main():
     tokens = steps * cfg.B
     value = tokens * nlay / wall                     # tokens/s per layer
     ms_per_step = wall * 1e3 / steps
+    step_us = ms_per_step * 1e3 / nlay               # one call (one layer of a stack step)
     kern_ms = np.array(kern_ms)
+    traffic = traffic_record(cfg.name)
     # a union launch does 2*3*B flops per weight byte; above the MFMA/HBM ridge
     # (2500 TFLOP/s / 8 TB/s = 312) it is bound by the matrix cores
     if cfg.layers == 1 and cfg.B > MFMA_BF16_PEAK_TFLOPS / HBM_PEAK_GBS * 1e3:
         flops = np.mean([work.launch_flops(i) for i in launches])
         achieved = flops / (kern_ms.mean() * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": achieved, "peak": MFMA_BF16_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": achieved / MFMA_BF16_PEAK_TFLOPS,
-                "traffic": traffic_record(cfg.name)}
+                "unit": "TFLOP/s", "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": traffic}
+        call = flops / (step_us * 1e-6) / 1e12
+        roof["call"] = {"achieved": call, "frac": call / MFMA_BF16_PEAK_TFLOPS,
+                        "time_us": step_us,
+                        "what": "the whole si_selective_ffn call (bitmaps, union list, both "
+                                "GEMMs, reducer) per graph-replayed step, wall clock"}
     else:
         byts = np.mean([work.launch_bytes(i) for i in launches])
         achieved = byts / (kern_ms.mean() * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": achieved / HBM_PEAK_GBS, "traffic": traffic_record(cfg.name)}
+                "frac": achieved / HBM_PEAK_GBS, "traffic": traffic}
+        call = byts / (step_us * 1e-6) / 1e9
+        roof["call"] = {"achieved": call, "frac": call / HBM_PEAK_GBS, "time_us": step_us,
+                        "what": ("the whole si_selective_ffn call (gather-GEMV and reducer) "
+                                 if cfg.B == 1 else "the whole si_selective_ffn call (token "
+                                 "bitmaps, both union GEMMs, reducer) ") +
+                                ("per layer of a graph-replayed stack step (with its residual "
+                                 "RMSNorm), wall clock" if nlay > 1 else
+                                 "per graph-replayed step, wall clock")}
+    if traffic is not None:
+        roof["traffic_source"] = (f"stored rocprofv3 FETCH_SIZE x 2.0 + WRITE_SIZE record "
+                                  f"(profiles/traffic_{cfg.name}.json), taken with the "
+                                  "current kernel sources")
     roof["kernel_ms_mean"] = float(kern_ms.mean())
     roof["kernel_ms_p50"] = float(np.median(kern_ms))
     roof["kernel_launches_timed"] = int(len(kern_ms))
     roof["bytes_per_launch" if roof["bound"] == "hbm" else "flops_per_launch"] = float(
         np.mean([work.launch_bytes(i) if roof["bound"] == "hbm" else work.launch_flops(i)
                  for i in launches]))
+    if cfg.B > 1:
+        # MFMA work on the flops the tokens need (their own active rows) and on the
+        # dense-over-union flops the union GEMMs execute
+        useful = np.mean([work.launch_useful_flops(i) for i in launches])
+        dense = np.mean([work.launch_flops(i) for i in launches])
+        kt = kern_ms.mean() * 1e-3
+        roof["mfma"] = {"useful_tflops": useful / kt / 1e12,
+                        "useful_frac": useful / kt / 1e12 / MFMA_BF16_PEAK_TFLOPS,
+                        "dense_over_union_tflops": dense / kt / 1e12,
+                        "dense_over_union_frac": dense / kt / 1e12 / MFMA_BF16_PEAK_TFLOPS,
+                        "useful_flops_per_launch": useful, "dense_flops_per_launch": dense}
 
     parity = None
-    cpu = None
-    if cfg.layers == 1:
-        last = (args.warmup + steps - 1) % cfg.steps
-        check_toks = sorted({last * cfg.B, last * cfg.B + cfg.B - 1})
-        worst, ref = check_outputs(work, check_toks)
+    if ref_out is not None:
+        torch.cuda.synchronize()
         tol = 5e-3 if cfg.wdtype == "bf16" else 1e-5
-        parity = {"tokens_checked": check_toks, "max_rel_l2": worst, "tol": tol}
-        if worst > tol:
-            log(f"PARITY FAILURE: rel L2 {worst:.3e} > {tol}")
+        parity = parity_from_oracle(work, ref_out, tol)
+        if cfg.layers == 1 and parity["max_rel_l2"] > tol:
+            log(f"PARITY FAILURE: rel L2 {parity['max_rel_l2']:.3e} > {tol}")
             sys.exit(1)
-        if not args.no_cpu_baseline:
-            cpu = cpu_baseline(work, ref, args.cpu_seconds)
 
     out = {
         "metric": METRIC,
