@@ -178,6 +178,24 @@ int si_selective_ffn(const void* x, si_dtype xdt, int64_t B, int64_t d,
                      float* y, void* ws, size_t ws_bytes, int flags, void* hip_stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph capture, serving loops
+ * or harnesses that forbid allocation): si_selective_ffn without the workspace arguments. Its
+ * kernels take their workspace from a static device array of SI_NOALLOC_SCRATCH_BYTES that the
+ * library holds on every device it runs on until the process ends; the call itself allocates
+ * nothing. Arguments, results, paths and errors are those of si_selective_ffn, plus
+ * SI_ERR_UNSUPPORTED when si_selective_ffn_workspace(...) for the same arguments exceeds
+ * SI_NOALLOC_SCRATCH_BYTES. All calls on one device share that array, so calls that overlap in
+ * time on one device (on different streams, or from several host threads) race and give
+ * undefined results; calls in one stream are ordered and safe. The array keeps the last call's
+ * contents: every kernel writes the workspace it reads, so nothing depends on them.
+ */
+#define SI_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+int si_selective_ffn_noalloc(const void* x, si_dtype xdt, int64_t B, int64_t d,
+                             const int32_t* offsets, const int32_t* idx, int64_t nnz,
+                             const void* gate_up_c, const void* down_c, int64_t L, si_dtype wdt,
+                             float* y, int flags, void* hip_stream);
+
+/*
  * Instrumentation: time the main kernel of si_selective_ffn with caller-owned HIP events.
  *
  *   start, stop: hipEvent_t handles (created with timing enabled), or both NULL to stop.

@@ -29,6 +29,7 @@ from .api import (  # noqa: F401
     residual_rmsnorm,
     select_topk,
     selective_ffn,
+    selective_ffn_noalloc,
     selective_ffn_resnorm,
     selective_ffn_workspace,
     set_timing_events,

@@ -27,6 +27,8 @@ SIGNATURES = {
     "si_selective_ffn_workspace": (c_size, [c_i64, c_i64, c_i64, c_i64, c_int, c_int, c_int]),
     "si_selective_ffn": (c_int, [c_vp, c_int, c_i64, c_i64, c_vp, c_vp, c_i64, c_vp, c_vp,
                                  c_i64, c_int, c_vp, c_vp, c_size, c_int, c_vp]),
+    "si_selective_ffn_noalloc": (c_int, [c_vp, c_int, c_i64, c_i64, c_vp, c_vp, c_i64, c_vp, c_vp,
+                                         c_i64, c_int, c_vp, c_int, c_vp]),
     "si_selective_ffn_resnorm": (c_int, [c_vp, c_vp, ctypes.c_float, c_vp, c_int, c_i64, c_i64,
                                          c_vp, c_vp, c_i64, c_vp, c_vp, c_i64, c_int, c_vp, c_vp,
                                          c_size, c_int, c_vp]),

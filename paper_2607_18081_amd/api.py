@@ -179,6 +179,34 @@ def selective_ffn(x: torch.Tensor, offsets: torch.Tensor, idx: torch.Tensor,
     return y
 
 
+NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def selective_ffn_noalloc(x: torch.Tensor, offsets: torch.Tensor, idx: torch.Tensor,
+                          gate_up_c: torch.Tensor, down_c: torch.Tensor, y: torch.Tensor,
+                          flags: int = 0) -> torch.Tensor:
+    """si_selective_ffn_noalloc: as selective_ffn, with the library's static device scratch as
+    the workspace; y [B][d] float32 is the caller's. Nothing is allocated."""
+    dev = _dev(x)
+    if x.dim() != 2:
+        raise ValueError("x must be [B][d]")
+    B, d = x.shape
+    L = gate_up_c.shape[0]
+    if gate_up_c.shape != (L, 2, d) or down_c.shape != (L, d):
+        raise ValueError("compacted weights must be [L][2][d] and [L][d]")
+    if offsets.dtype != torch.int32 or idx.dtype != torch.int32:
+        raise ValueError("offsets and idx must be int32")
+    if offsets.numel() < B + 1:
+        raise ValueError("offsets needs B + 1 entries")
+    if y.shape != (B, d) or y.dtype != torch.float32:
+        raise ValueError("y must be [B][d] float32")
+    st = load().si_selective_ffn_noalloc(_ptr(x), _dt(x), B, d, _ptr(offsets), _ptr(idx),
+                                         idx.numel(), _ptr(gate_up_c), _ptr(down_c), L,
+                                         _dt(gate_up_c), _ptr(y), flags, _stream(dev))
+    _check(st, "si_selective_ffn_noalloc")
+    return y
+
+
 def selective_ffn_resnorm(x_prev: torch.Tensor, y_prev: torch.Tensor, offsets: torch.Tensor,
                           idx: torch.Tensor, gate_up_c: torch.Tensor, down_c: torch.Tensor,
                           eps: float = 1e-5, flags: int = 0, x_out: torch.Tensor | None = None,

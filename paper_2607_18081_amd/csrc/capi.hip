@@ -17,6 +17,13 @@ std::mutex g_check_mu;
 int* g_status_ptr[kMaxDevices] = {};
 int g_num_cu[kMaxDevices] = {};
 
+// Workspace of si_selective_ffn_noalloc: a static array that each device holds for the life of
+// the process. In host code `scratch` names a host-side stand-in, not device memory: its device
+// address comes from hipGetSymbolAddress, once per device, and only that address is used.
+__device__ __align__(256) unsigned char scratch[SI_NOALLOC_SCRATCH_BYTES];
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
 int current_device() {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return -1;
@@ -31,6 +38,17 @@ int* status_word(int dev) {
         g_status_ptr[dev] = static_cast<int*>(p);
     }
     return g_status_ptr[dev];
+}
+
+// the device address of this device's copy of `scratch` (the device must be current)
+void* scratch_ptr(int dev) {
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return nullptr;
+        g_scratch_ptr[dev] = p;
+    }
+    return g_scratch_ptr[dev];
 }
 
 int num_cu(int dev) {
@@ -240,6 +258,22 @@ int si_selective_ffn(const void* x, si_dtype xdt, int64_t B, int64_t d, const in
                      void* hip_stream) {
     return selective_ffn(x, xdt, B, d, offsets, idx, nnz, gate_up_c, down_c, L, wdt, y, ws,
                          ws_bytes, flags, hip_stream, nullptr);
+}
+
+int si_selective_ffn_noalloc(const void* x, si_dtype xdt, int64_t B, int64_t d,
+                             const int32_t* offsets, const int32_t* idx, int64_t nnz,
+                             const void* gate_up_c, const void* down_c, int64_t L, si_dtype wdt,
+                             float* y, int flags, void* hip_stream) {
+    if (B < 0 || d < 1 || L < 1 || nnz < 0) return SI_ERR_INVALID;
+    if (B == 0) return SI_OK;
+    if (si_selective_ffn_workspace(B, nnz, L, d, xdt, wdt, flags) > SI_NOALLOC_SCRATCH_BYTES)
+        return SI_ERR_UNSUPPORTED;
+    const int dev = current_device();
+    if (dev < 0) return SI_ERR_HIP;
+    void* ws = scratch_ptr(dev);
+    if (!ws) return SI_ERR_HIP;
+    return selective_ffn(x, xdt, B, d, offsets, idx, nnz, gate_up_c, down_c, L, wdt, y, ws,
+                         SI_NOALLOC_SCRATCH_BYTES, flags, hip_stream, nullptr);
 }
 
 int si_selective_ffn_resnorm(const void* x_prev, const float* y_prev, float eps, void* x_out,
