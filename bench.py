@@ -331,12 +331,13 @@ def _oracle_token(t):
                                    st["ref"]["down_c"])
 
 
-def _oracle_chain(t):
+def _oracle_chain(t, x=None):
     """One token through every layer of the stack, free-running: x_{l+1} = RMSNorm(x_l + y_l)
-    in bf16; returns the last layer's y."""
+    in bf16; returns the last layer's y. x: the first layer's input in storage form (default:
+    the token's own)."""
     import oracle
     st = _CPU
-    x = st["x"][t]
+    x = st["x"][t] if x is None else x
     y = None
     for lay, ref in enumerate(st["refs"]):
         if lay > 0:
@@ -404,6 +405,17 @@ def cpu_leg(cfg, seconds, workers):
         if t in outputs and not np.array_equal(outputs[t], y):
             raise RuntimeError(f"oracle is not deterministic on token {t}")
         outputs[t] = y
+    sens = None
+    if cfg.layers > 1 and cfg.wdtype == "bf16":
+        # the oracle against itself: token 0 again with its first input element moved by one
+        # bf16 unit in the last place; how far the last layer's y moves after all layers is
+        # the scale a free-running comparison of two correct implementations can differ by
+        x1 = _CPU["x"][0].copy()
+        x1[0] ^= np.uint16(1)
+        with threadpool_limits(limits=1):
+            _, y1 = _oracle_chain(0, x1)
+        sens = float(np.linalg.norm(y1 - outputs[0]) / np.linalg.norm(outputs[0]))
+        log(f"CPU leg: oracle's own free-running change for a one-ulp input change: {sens:.3e}")
     _CPU.clear()
     what = ("id remap + fp64 NumPy selective FFN per token" if cfg.layers == 1 else
             f"one token through all {cfg.layers} layers (id remap, fp64 selective FFN, "
@@ -419,6 +431,8 @@ def cpu_leg(cfg, seconds, workers):
         **info,
     }
     log(f"CPU leg: oracle {rate1:.1f} {unit} on one thread, {rec['value']:.1f} on {workers}")
+    if sens is not None:
+        outputs["one_ulp_sensitivity"] = sens
     return rec, outputs
 
 
@@ -429,6 +443,7 @@ def parity_from_oracle(work, outputs, tol):
     cfg = work.cfg
     y = work.y.cpu().numpy()
     worst = 0.0
+    sens = outputs.pop("one_ulp_sensitivity", None)
     for t, want in outputs.items():
         if t >= y.shape[0]:
             continue
@@ -440,8 +455,11 @@ def parity_from_oracle(work, outputs, tol):
         # free-running through the stack: reported for information, not held to a bound
         rec = {"tokens_checked": len(outputs), "free_running_last_layer_rel_l2": worst,
                "layers": cfg.layers,
+               "oracle_one_ulp_sensitivity": sens,
                "note": "the oracle's chain takes its own bf16 x at every layer; per-layer "
-                       "parity (teacher-forced) is held to the tolerance in the tests"}
+                       "parity (teacher-forced) is held to the tolerance in the tests. "
+                       "oracle_one_ulp_sensitivity: the oracle's own last-layer change when "
+                       "token 0's first input element moves by one bf16 ulp"}
     return rec
 
 

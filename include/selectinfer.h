@@ -63,8 +63,12 @@ enum {
                                ascending, which they always are                                 */
     SI_FLAG_PER_TOKEN = 16, /* B > 1: use the per-token path even when the union path applies   */
     SI_FLAG_FAST_H = 32,    /* union path: feed SiLU(g)*u to the second MFMA GEMM as one 16-bit
-                               value instead of a hi + lo pair (faster, ~1e-3 rel. err)         */
-    SI_FLAG_UNION = 64      /* 2 <= B < 5: use the union path where the dtypes allow it         */
+                               value instead of a hi + lo pair (faster, ~1e-3 rel. err); the
+                               default from 128 tokens on (the compute-bound tiled GEMMs)       */
+    SI_FLAG_UNION = 64,     /* 2 <= B < 5: use the union path where the dtypes allow it         */
+    SI_FLAG_EXACT_H = 128   /* union path from 128 tokens on: feed SiLU(g)*u as the hi + lo
+                               pair (about 16 significant bits, twice the second GEMM's MFMA
+                               work); below 128 tokens the pair is the default. FAST_H wins   */
 };
 
 /* Library version (major * 10000 + minor * 100 + patch). */
@@ -158,11 +162,12 @@ size_t si_selective_ffn_workspace(int64_t B, int64_t nnz, int64_t L, int64_t d,
  *     the active rows with 16-byte loads and a fused SiLU*up epilogue, then accumulates the
  *     down rows into float32 partial sums that a second kernel adds in a fixed order;
  *   - union (B >= 5, or B >= 2 with SI_FLAG_UNION; x and weights both bf16 or both half): the
- *     union of the B active sets
- *     is built on the device and both projections run as MFMA gather-GEMMs over the union
- *     rows, with
- *     each token's h masked to its own set; below 128 tokens the union rows are streamed
- *     once (bandwidth bound), from 128 tokens on the products are LDS-tiled (compute bound).
+ *     union of the B active sets is built on the device and both projections run as MFMA
+ *     gather-GEMMs over the union rows, with each token's h masked to its own set; below 128
+ *     tokens the union rows are streamed once (bandwidth bound) and h enters the second GEMM
+ *     as a 16-bit hi + lo pair (about 16 significant bits), from 128 tokens on the products
+ *     are LDS-tiled (compute bound) and h enters as one 16-bit value (about 8 significant bits
+ *     for bf16, a relative error near 1e-3; SI_FLAG_EXACT_H: the pair).
  * Requirements: d % 8 == 0 for 16-bit data, d % 4 == 0 for f32; d <= 16384 (16-bit weights)
  * or 8192 (f32 weights), else SI_ERR_UNSUPPORTED; 16-byte aligned x, gate_up_c, down_c, y and
  * ws; B >= 0; nnz >= 0; L >= 1.

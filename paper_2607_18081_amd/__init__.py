@@ -8,6 +8,7 @@ from .api import (  # noqa: F401
     F16,
     F32,
     FLAG_CHECK,
+    FLAG_EXACT_H,
     FLAG_FAST_H,
     FLAG_PER_TOKEN,
     FLAG_SORTED,

@@ -15,6 +15,7 @@ from ._lib import load
 F32, BF16, F16 = 0, 1, 2
 TOPK_ABS, TOPK_RAW = 1, 2
 FLAG_CHECK, FLAG_SORTED, FLAG_PER_TOKEN, FLAG_FAST_H, FLAG_UNION = 4, 8, 16, 32, 64
+FLAG_EXACT_H = 128
 _MODES = {"abs": TOPK_ABS, "raw": TOPK_RAW}
 
 _DT = {torch.float32: F32, torch.bfloat16: BF16, torch.float16: F16}

@@ -248,7 +248,7 @@ size_t si_selective_ffn_workspace(int64_t B, int64_t nnz, int64_t L, int64_t d, 
     if (B <= 0 || d <= 0 || L <= 0 || nnz < 0) return 0;
     const int dev = current_device();
     const int ncu = dev < 0 ? 256 : num_cu(dev);
-    if (use_union(B, L, d, xdt, wdt, flags)) return si::union_workspace(B, L, d, ncu);
+    if (use_union(B, L, d, xdt, wdt, flags)) return si::union_workspace(B, L, d, ncu, flags);
     return si::decode_workspace(B, nnz, d, ncu);
 }
 

@@ -9,7 +9,8 @@
 //    of 512 threads deal a token's k active slots as the gather-GEMV kernel does (work-group p
 //    takes rows [floor(k p / P), floor(k (p + 1) / P))), and for each batch of up to 16 rows
 //    issue every gate and up row load, then every down row load, 16 bytes per lane per row,
-//    non-temporal. Its time is the floor of that kernel's on the same rows.
+//    non-temporal; a batch issues loads for the rows it has only. Its time is the floor of
+//    that kernel's on the same rows.
 #include <hip/hip_ext.h>
 
 #include "common.h"
@@ -46,6 +47,50 @@ __global__ __launch_bounds__(kCeilThreads) void ceiling_stream(const void* __res
     sink[(int64_t)blockIdx.x * kCeilThreads + threadIdx.x] = acc;
 }
 
+// One batch of N rows (N a compile-time constant, as in the gather-GEMV kernel): every gate and
+// up load of the N rows, then every down load, then the fold. Only the N rows issue loads, so
+// a work-group whose share ends inside a batch spends no load issue slots on rows it does not
+// have.
+template <int N>
+__device__ __forceinline__ void gather_batch(__amdgpu_buffer_rsrc_t rg, __amdgpu_buffer_rsrc_t rd,
+                                             const int32_t (&sl)[kCeilRows], int64_t L,
+                                             int64_t row_bytes, uint32_t& acc) {
+    for (int64_t c = (int64_t)threadIdx.x * 16; c < row_bytes + 15; c += kCeilThreads * 16) {
+        const int col = c < row_bytes ? (int)c : kOOB;
+        V16 g[N], u[N], dn[N];
+#pragma unroll
+        for (int q = 0; q < N; ++q) {
+            const bool ok = sl[q] >= 0 && sl[q] < L && col != kOOB;
+            const int og = ok ? (int)(sl[q] * 2 * row_bytes) + col : kOOB;
+            g[q] = bload16nt(rg, og);
+            u[q] = bload16nt(rg, ok ? og + (int)row_bytes : kOOB);
+        }
+#pragma unroll
+        for (int q = 0; q < N; ++q) {
+            const bool ok = sl[q] >= 0 && sl[q] < L && col != kOOB;
+            dn[q] = bload16nt(rd, ok ? (int)(sl[q] * row_bytes) + col : kOOB);
+        }
+#pragma unroll
+        for (int q = 0; q < N; ++q)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc ^= g[q].w[e] + 3u * u[q].w[e] + 7u * dn[q].w[e];
+    }
+}
+
+// gather_batch<n> for a run-time n in [N, kCeilRows], through a chain of uniform compares
+template <int N>
+__device__ __forceinline__ void gather_rows(int n, __amdgpu_buffer_rsrc_t rg,
+                                            __amdgpu_buffer_rsrc_t rd,
+                                            const int32_t (&sl)[kCeilRows], int64_t L,
+                                            int64_t row_bytes, uint32_t& acc) {
+    if constexpr (N <= kCeilRows) {
+        if (n == N)
+            gather_batch<N>(rg, rd, sl, L, row_bytes, acc);
+        else
+            gather_rows<N + 1>(n, rg, rd, sl, L, row_bytes, acc);
+    }
+}
+
 __global__ __launch_bounds__(kCeilThreads) void ceiling_gather(
     const void* __restrict__ gate_up_c, const void* __restrict__ down_c, int64_t L,
     int64_t row_bytes, const int32_t* __restrict__ idx, int64_t k,
@@ -58,30 +103,11 @@ __global__ __launch_bounds__(kCeilThreads) void ceiling_gather(
     const int64_t r1 = (int64_t)((uint32_t)k * (uint32_t)(p + 1) / (uint32_t)P);
     uint32_t acc = 0;
     for (int64_t rb = r0; rb < r1; rb += kCeilRows) {
+        const int n = (int)(r1 - rb < kCeilRows ? r1 - rb : kCeilRows);
         int32_t sl[kCeilRows];
 #pragma unroll
-        for (int q = 0; q < kCeilRows; ++q) sl[q] = rb + q < r1 ? idx[rb + q] : -1;
-        // every group of the row: lanes beyond the row read nothing (out-of-range offset)
-        for (int64_t c = (int64_t)threadIdx.x * 16; c < row_bytes + 15; c += kCeilThreads * 16) {
-            const int col = c < row_bytes ? (int)c : kOOB;
-            V16 g[kCeilRows], u[kCeilRows], dn[kCeilRows];
-#pragma unroll
-            for (int q = 0; q < kCeilRows; ++q) {
-                const bool ok = sl[q] >= 0 && sl[q] < L && col != kOOB;
-                const int og = ok ? (int)(sl[q] * 2 * row_bytes) + col : kOOB;
-                g[q] = bload16nt(rg, og);
-                u[q] = bload16nt(rg, ok ? og + (int)row_bytes : kOOB);
-            }
-#pragma unroll
-            for (int q = 0; q < kCeilRows; ++q) {
-                const bool ok = sl[q] >= 0 && sl[q] < L && col != kOOB;
-                dn[q] = bload16nt(rd, ok ? (int)(sl[q] * row_bytes) + col : kOOB);
-            }
-#pragma unroll
-            for (int q = 0; q < kCeilRows; ++q)
-#pragma unroll
-                for (int e = 0; e < 4; ++e) acc ^= g[q].w[e] + 3u * u[q].w[e] + 7u * dn[q].w[e];
-        }
+        for (int q = 0; q < kCeilRows; ++q) sl[q] = q < n ? idx[rb + q] : -1;
+        gather_rows<1>(n, rg, rd, sl, L, row_bytes, acc);
     }
     sink[(int64_t)p * kCeilThreads + threadIdx.x] = acc;
 }

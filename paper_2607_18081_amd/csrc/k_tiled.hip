@@ -17,12 +17,16 @@
 //    neighbouring MFMA tiles and the SiLU*up*mask epilogue needs no data exchange. Both
 //    operands are K-contiguous rows (token rows of x, neuron rows of gate_up_c) staged in LDS
 //    with a 144-byte pitch, which keeps the 16 rows read by one ds_read_b128 in distinct banks.
-//    H is written as two bf16 planes, hi = bf16(h) and lo = bf16(h - hi).
-//  - gemm2_tiled: Y partials for 256 tokens x 128 columns over one of KS chunks of the union,
-//    K = union position in steps of 64. H rows are K-contiguous; the down rows are staged as
-//    row segments and read back transposed into the MFMA B layout with ds_read_b64_tr_b16.
-//    hi and lo both enter the MFMA (about 16 significant bits of h) unless SI_FLAG_FAST_H.
-//    The KS partials are added in a fixed order by the shared partial reducer.
+//    H is written as bf16(h), and with SI_FLAG_EXACT_H also lo = bf16(h - hi) as a second
+//    plane.
+//  - gemm2_tiled: Y partials for 256 tokens x 128-256 columns over one of KS chunks of the
+//    union, K = union position in steps of 64. H rows are K-contiguous; the down rows are
+//    staged as row segments and read back transposed into the MFMA B layout with
+//    ds_read_b64_tr_b16. Each XCD takes whole (token tile, K chunk) pairs, so the H slice of
+//    a pair is fetched into one XCD's L2 only. The products are compute bound, so H enters
+//    the MFMA as one 16-bit value (about 8 significant bits of h for bf16) unless
+//    SI_FLAG_EXACT_H asks for the hi + lo pair (about 16 bits, twice the MFMA work). The KS
+//    partials are added in a fixed order by the shared partial reducer.
 // Tiles are loaded with range-checked buffer loads (zeros outside), staged through registers
 // while the previous tile is multiplied out of LDS.
 #include <hip/hip_ext.h>
@@ -45,9 +49,7 @@ constexpr int kKP = kBK + 8;     // LDS pitch (bf16) of K-contiguous tiles: 144 
 constexpr int kT1S = 80;         // GEMM1 union slots per work-group (5 groups of 16)
 constexpr int kT1N = 2 * kT1S;   // GEMM1 weight rows per work-group
 constexpr int kT2M = 256;        // GEMM2 tokens per work-group (4 waves x 64)
-constexpr int kT2N = 128;        // GEMM2 columns per work-group (2 waves x 64)
 constexpr int kT2T = 512;        // GEMM2 threads per work-group (8 waves, two per SIMD)
-constexpr int kT2P = kT2N + 16;  // LDS pitch (bf16) of the down-row tile
 
 // part[c][w] = OR of bits[b][w] over the 64 tokens b of block c. Work-group (wx, c): 64 words
 // x 64 tokens; each wave ORs 16 tokens of the 64 words, then the 4 waves meet in LDS.
@@ -71,26 +73,40 @@ __global__ __launch_bounds__(256) void or_blocks(const uint32_t* __restrict__ bi
 }
 
 // One work-group: the union of the nb block bitmaps part[0..nb)[W], its set bits in ascending
-// order -> ulist, their number -> *ucount. Thread t owns a contiguous run of words; an
-// exclusive scan of the runs' counts (wave scans, then the 16 wave totals) gives each run its
-// first position.
+// order -> ulist, their number -> *ucount. The union words are formed once into LDS (thread t
+// takes words t, t + 1024, ...; the block rows of a word are read eight at a time with
+// range-checked loads issued together, so a word costs one memory round trip per eight
+// blocks). Thread t then owns a contiguous run of words; an exclusive scan of the runs' counts
+// (wave scans, then the 16 wave totals) gives each run its first position. Dynamic LDS: W
+// words (W <= 16368).
 __global__ __launch_bounds__(1024) void union_scan(const uint32_t* __restrict__ part, int64_t nb,
                                                    int64_t W, int32_t* __restrict__ ulist,
                                                    int* __restrict__ ucount) {
+    extern __shared__ uint32_t uw[];
     __shared__ int wtot[16];
     const int t = threadIdx.x;
     const int lane = t & 63;
     const int wv = t >> 6;
+    const __amdgpu_buffer_rsrc_t rp = make_rsrc(part, nb * W * 4);
+    for (int64_t w = t; w < W; w += 1024) {
+        uint32_t u = 0u;
+        for (int64_t c0 = 0; c0 < nb; c0 += 8) {
+            uint32_t v[8];
+#pragma unroll
+            for (int c = 0; c < 8; ++c)
+                v[c] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(
+                    rp, c0 + c < nb ? (int)(((c0 + c) * W + w) * 4) : kOOB, 0, 0);
+#pragma unroll
+            for (int c = 0; c < 8; ++c) u |= v[c];
+        }
+        uw[w] = u;
+    }
+    __syncthreads();
     const int64_t per = (W + 1023) / 1024;
     const int64_t w0 = (int64_t)t * per;
     const int64_t w1 = (w0 + per < W) ? w0 + per : W;
-    auto word = [&](int64_t w) {
-        uint32_t u = 0u;
-        for (int64_t c = 0; c < nb; ++c) u |= part[c * W + w];
-        return u;
-    };
     int c = 0;
-    for (int64_t w = w0; w < w1; ++w) c += __popc(word(w));
+    for (int64_t w = w0; w < w1; ++w) c += __popc(uw[w]);
     const int incl = wave_incl_scan(c);
     if (lane == kWave - 1) wtot[wv] = incl;
     __syncthreads();
@@ -102,7 +118,7 @@ __global__ __launch_bounds__(1024) void union_scan(const uint32_t* __restrict__ 
     }
     int pos = before + incl - c;
     for (int64_t w = w0; w < w1; ++w) {
-        uint32_t u = word(w);
+        uint32_t u = uw[w];
         while (u) {
             const int j = __ffs(u) - 1;
             ulist[pos++] = (int32_t)(w * 32 + j);
@@ -268,7 +284,8 @@ __global__ __launch_bounds__(2 * TM) void gemm1_tiled(
                             act ? silu_f32(acc[mi][2 * q][i]) * acc[mi][2 * q + 1][i] : 0.0f;
                         const uint32_t hb = Mfma<ET>::rne(h);
                         Hhi[tok * Up + u] = (uint16_t)hb;
-                        Hlo[tok * Up + u] = (uint16_t)Mfma<ET>::rne(h - Mfma<ET>::widen(hb));
+                        if (Hlo)  // the lo plane exists only for SI_FLAG_EXACT_H
+                            Hlo[tok * Up + u] = (uint16_t)Mfma<ET>::rne(h - Mfma<ET>::widen(hb));
                     }
                 }
             }
@@ -276,20 +293,48 @@ __global__ __launch_bounds__(2 * TM) void gemm1_tiled(
 }
 
 // ---- GEMM2 ---------------------------------------------------------------------------------
-// Grid: (ceil(d / 128), ceil(B / 256), KS), 512 threads: wave w computes tokens 64 (w / 2) ..
-// and columns 64 (w % 2) .. of the tile. Partials in the chunked layout.
-template <typename ET>
+// Work-group: 256 tokens x 32 NJ columns over one of KS chunks of the union, 512 threads:
+// wave w computes tokens 64 (w / 2) .. and columns 16 NJ (w % 2) .. of the tile. Partials in
+// the chunked layout. A (token tile, K chunk) pair is a combo: combo c is token tile c % ntm
+// of K chunk c / ntm.
+// XCD (xcd = 1): the hardware deals work-groups to the 8 XCDs in turn, so in the grid
+// (8, ntn, combos / 8) work-group (x, y, z) runs on XCD x and takes column tile y of combo
+// x + 8 z: each XCD takes whole combos, and the H slice of a combo (256 tokens x its chunk) is
+// read by the work-groups of one XCD only and stays in that XCD's L2. Otherwise the grid is
+// (ntn, combos), column tile fastest.
+// The two divisions by run-time sizes use host-computed reciprocals (n / q = mulhi(n, m),
+// m = ceil(2^32 / q), exact for n q < 2^32): the compiler lowers an integer division through
+// the vector unit, and the K range derived from one sizes a buffer descriptor, which would
+// then be a vector value and put every load through it in a loop over the lanes.
+// FAST: H enters the MFMA as one 16-bit value (no lo plane, and half the H tile in LDS).
+struct G2Grid {
+    int KS, ntm, xcd;
+    uint32_t ks_m, ntm_m;  // ceil(2^32 / KS), ceil(2^32 / ntm)
+};
+
+template <typename ET, int NJ, bool FAST>
 __global__ __launch_bounds__(kT2T) void gemm2_tiled(
     const uint16_t* __restrict__ Hhi, const uint16_t* __restrict__ Hlo, int64_t Up, int64_t B,
     const uint16_t* __restrict__ dc, int64_t d, int64_t L, const int32_t* __restrict__ ulist,
-    const int* __restrict__ ucount, float* __restrict__ part, int KS, int fast) {
+    const int* __restrict__ ucount, float* __restrict__ part, G2Grid gg) {
+    constexpr int kCols = 32 * NJ;                        // columns per work-group
+    constexpr int kPitch = kCols + 16;                    // LDS pitch (bf16) of the down tile
+    constexpr int kCpr = kCols / 8;                       // 16-byte chunks per row segment
+    constexpr int kDJ = (kBK * kCpr + kT2T - 1) / kT2T;   // staging passes of the down rows
+    constexpr int kPlanes = FAST ? 1 : 2;
+    const int KS = gg.KS;
+    const uint32_t combo = gg.xcd ? blockIdx.x + 8 * blockIdx.z : blockIdx.y;
+    const uint32_t ct = gg.xcd ? blockIdx.y : blockIdx.x;
+    // (a divisor of 1 has no 32-bit reciprocal: taken apart)
+    const uint32_t ks = gg.ntm == 1 ? combo : __umulhi(combo, gg.ntm_m);
+    const uint32_t tmi = combo - ks * (uint32_t)gg.ntm;
     const int nU = *ucount;
-    const int ks = blockIdx.z;
-    const int64_t kper = (((int64_t)nU + KS - 1) / KS + kBK - 1) / kBK * kBK;
-    const int64_t kb = (int64_t)ks * kper;
-    const int64_t ke = (kb + kper < nU) ? kb + kper : nU;
-    const int64_t n0 = (int64_t)blockIdx.x * kT2N;
-    const int64_t m0 = (int64_t)blockIdx.y * kT2M;
+    const uint32_t nk = (uint32_t)(nU + KS - 1);
+    const int kper = (int)((KS == 1 ? nk : __umulhi(nk, gg.ks_m)) + kBK - 1) / kBK * kBK;
+    const int kb = (int)ks * kper;
+    const int ke = kb + kper < nU ? kb + kper : nU;
+    const int64_t n0 = (int64_t)ct * kCols;
+    const int64_t m0 = (int64_t)tmi * kT2M;
     const int t = threadIdx.x;
     const int lane = t & 63;
     const int w = t >> 6;
@@ -298,38 +343,44 @@ __global__ __launch_bounds__(kT2T) void gemm2_tiled(
     const int nn = lane & 15;
     const int g = lane >> 4;
 
-    __shared__ __align__(16) uint16_t sH[2][kT2M][kKP];
-    __shared__ __align__(16) uint16_t sD[kBK][kT2P];
+    __shared__ __align__(16) uint16_t sH[kPlanes][kT2M][kKP];
+    __shared__ __align__(16) uint16_t sD[kBK][kPitch];
 
-    // staging of H: chunk t % 8 of rows t / 8 + 64 j; of the down rows: 16-byte chunk t % 16
-    // of union positions t / 16 + 32 j
+    // staging of H: chunk t % 8 of rows t / 8 + 64 j; of the down rows: 16-byte chunk
+    // q % kCpr of union position q / kCpr, q = t + 512 j (q past the tile: nothing)
     const int ch = t & 7;
     const int r0 = t >> 3;
-    const int dch = t & 15;
-    const int dr0 = t >> 4;
     const __amdgpu_buffer_rsrc_t rh = make_rsrc(Hhi, B * Up * 2);
     const __amdgpu_buffer_rsrc_t rl = make_rsrc(Hlo, B * Up * 2);
     const __amdgpu_buffer_rsrc_t rd = make_rsrc(dc, L * d * 2);
-    constexpr int kHJ = kT2M / 64, kDJ = kBK / 32;
+    constexpr int kHJ = kT2M / 64;
     int hoff[kHJ];
 #pragma unroll
     for (int j = 0; j < kHJ; ++j) {
         const int64_t tok = m0 + r0 + 64 * j;
         hoff[j] = tok < B ? (int)(tok * Up * 2) : kOOB;
     }
-    const int64_t dcol = n0 + 8 * dch;
-    const bool dcol_in = dcol < d;  // d % 8 == 0
+    int drow[kDJ], dcol[kDJ];  // staged position and element column; dcol < 0: no chunk
+#pragma unroll
+    for (int j = 0; j < kDJ; ++j) {
+        const int q = t + kT2T * j;
+        drow[j] = q / kCpr;
+        const int64_t c = n0 + 8 * (q % kCpr);
+        dcol[j] = (q < kBK * kCpr && c < d) ? (int)c : -1;  // d % 8 == 0
+    }
     V16 ph[kHJ], pl[kHJ], pd[kDJ];
     // slot ids of the down rows of the next fetch, loaded one K step ahead of their use so
-    // the row loads do not wait on them (union positions past the chunk read as -1)
+    // the row loads do not wait on them. The loads are unconditional (a union position past
+    // the chunk has an out-of-range offset and reads nothing): validity is applied where the
+    // ids are used, so no branch or select makes the compiler wait for them early.
     const __amdgpu_buffer_rsrc_t ru = make_rsrc(ulist, ke * 4);
     int32_t sl[kDJ];
     auto load_slots = [&](int64_t k0) {
 #pragma unroll
         for (int j = 0; j < kDJ; ++j) {
-            const int64_t u = k0 + dr0 + 32 * j;
-            sl[j] = u < ke ? (int32_t)__builtin_amdgcn_raw_buffer_load_b32(ru, (int)(u * 4), 0, 0)
-                           : -1;
+            const int64_t u = k0 + drow[j];
+            sl[j] = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(
+                ru, (u < ke && dcol[j] >= 0) ? (int)(u * 4) : kOOB, 0, 0);
         }
     };
     auto fetch = [&](int64_t k0) {
@@ -344,26 +395,26 @@ __global__ __launch_bounds__(kT2T) void gemm2_tiled(
         for (int j = 0; j < kHJ; ++j) {
             const int off = (nv > 0 && hoff[j] != kOOB) ? hoff[j] + (int)(k * 2) : kOOB;
             ph[j] = bload16(rh, off);
-            pl[j] = bload16(rl, fast ? kOOB : off);
+            if constexpr (!FAST) pl[j] = bload16(rl, off);
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 ph[j].w[e] &= keep[e];
-                pl[j].w[e] &= keep[e];
+                if constexpr (!FAST) pl[j].w[e] &= keep[e];
             }
         }
 #pragma unroll
-        for (int j = 0; j < kDJ; ++j)
-            pd[j] = bload16(rd, (sl[j] >= 0 && sl[j] < L && dcol_in)
-                                    ? (int)(((int64_t)sl[j] * d + dcol) * 2)
-                                    : kOOB);
+        for (int j = 0; j < kDJ; ++j) {
+            const bool ok = k0 + drow[j] < ke && dcol[j] >= 0 && sl[j] >= 0 && sl[j] < L;
+            pd[j] = bload16(rd, ok ? (int)(((int64_t)sl[j] * d + dcol[j]) * 2) : kOOB);
+        }
         load_slots(k0 + kBK);
     };
 
-    f32x4_t acc[4][4];
+    f32x4_t acc[4][NJ];
 #pragma unroll
     for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
-        for (int nj = 0; nj < 4; ++nj) acc[mi][nj] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int nj = 0; nj < NJ; ++nj) acc[mi][nj] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
     if (kb < ke) {
         load_slots(kb);
@@ -374,10 +425,11 @@ __global__ __launch_bounds__(kT2T) void gemm2_tiled(
 #pragma unroll
         for (int j = 0; j < kHJ; ++j) {
             st16(&sH[0][r0 + 64 * j][8 * ch], ph[j]);
-            st16(&sH[1][r0 + 64 * j][8 * ch], pl[j]);
+            if constexpr (!FAST) st16(&sH[kPlanes - 1][r0 + 64 * j][8 * ch], pl[j]);
         }
 #pragma unroll
-        for (int j = 0; j < kDJ; ++j) st16(&sD[dr0 + 32 * j][8 * dch], pd[j]);
+        for (int j = 0; j < kDJ; ++j)
+            if (dcol[j] >= 0) st16(&sD[drow[j]][dcol[j] - n0], pd[j]);
         __syncthreads();
         fetch(k0 + kBK);  // past the end of the chunk: reads nothing
         __builtin_amdgcn_sched_barrier(0);  // the prefetch stays ahead of the MFMAs
@@ -387,10 +439,10 @@ __global__ __launch_bounds__(kT2T) void gemm2_tiled(
             // 16-column subtile; ds_read_b64_tr_b16 hands lane i of a 16-lane group element
             // i % 4 of the 8-byte pieces addressed by lanes i / 4 + 4 j, so lane nn addresses
             // position 8 g + nn / 4 (and + 4), columns 4 (nn % 4) .. + 3 of the subtile.
-            typename Mfma<ET>::vec8 bop[4];
+            typename Mfma<ET>::vec8 bop[NJ];
 #pragma unroll
-            for (int nj = 0; nj < 4; ++nj) {
-                const int col = 64 * wn + 16 * nj + 4 * (nn & 3);
+            for (int nj = 0; nj < NJ; ++nj) {
+                const int col = 16 * NJ * wn + 16 * nj + 4 * (nn & 3);
                 const int row = 32 * ks2 + 8 * g + (nn >> 2);
                 const s16x4_t lo4 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
                     (__attribute__((address_space(3))) s16x4_t*)&sD[row][col]);
@@ -405,20 +457,23 @@ __global__ __launch_bounds__(kT2T) void gemm2_tiled(
             // A fragments (hi, lo) one row-tile ahead of their MFMAs
             typename Mfma<ET>::vec8 ah[2], al[2];
             ah[0] = Mfma<ET>::vec(ld16(&sH[0][64 * wm + nn][32 * ks2 + 8 * g]));
-            al[0] = Mfma<ET>::vec(ld16(&sH[1][64 * wm + nn][32 * ks2 + 8 * g]));
+            if constexpr (!FAST)
+                al[0] = Mfma<ET>::vec(ld16(&sH[kPlanes - 1][64 * wm + nn][32 * ks2 + 8 * g]));
 #pragma unroll
             for (int mi = 0; mi < 4; ++mi) {
                 if (mi + 1 < 4) {
                     const int row = 64 * wm + 16 * (mi + 1) + nn;
                     ah[(mi + 1) & 1] = Mfma<ET>::vec(ld16(&sH[0][row][32 * ks2 + 8 * g]));
-                    al[(mi + 1) & 1] = Mfma<ET>::vec(ld16(&sH[1][row][32 * ks2 + 8 * g]));
+                    if constexpr (!FAST)
+                        al[(mi + 1) & 1] =
+                            Mfma<ET>::vec(ld16(&sH[kPlanes - 1][row][32 * ks2 + 8 * g]));
                 }
 #pragma unroll
-                for (int nj = 0; nj < 4; ++nj)
+                for (int nj = 0; nj < NJ; ++nj)
                     acc[mi][nj] = Mfma<ET>::mma(ah[mi & 1], bop[nj], acc[mi][nj]);
-                if (!fast) {
+                if constexpr (!FAST) {
 #pragma unroll
-                    for (int nj = 0; nj < 4; ++nj)
+                    for (int nj = 0; nj < NJ; ++nj)
                         acc[mi][nj] = Mfma<ET>::mma(al[mi & 1], bop[nj], acc[mi][nj]);
                 }
             }
@@ -426,16 +481,16 @@ __global__ __launch_bounds__(kT2T) void gemm2_tiled(
     }
 
     // register i of lane l of tile (mi, nj): token 64 wm + 16 mi + 4 g + i, column
-    // 64 wn + 16 nj + nn; the 16 lanes of a row write 64 contiguous bytes
+    // 16 NJ wn + 16 nj + nn; the 16 lanes of a row write 64 contiguous bytes
     const int64_t nch = part_chunks(d);
 #pragma unroll
     for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
-        for (int nj = 0; nj < 4; ++nj)
+        for (int nj = 0; nj < NJ; ++nj)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int64_t tok = m0 + 64 * wm + 16 * mi + 4 * g + i;
-                const int64_t col = n0 + 64 * wn + 16 * nj + nn;
+                const int64_t col = n0 + 16 * NJ * wn + 16 * nj + nn;
                 if (tok < B && col < d) part[part_off(tok, ks, col, KS, nch)] = acc[mi][nj][i];
             }
 }
@@ -443,13 +498,16 @@ __global__ __launch_bounds__(kT2T) void gemm2_tiled(
 struct TPlan {
     int64_t W, Lp, Up;
     int tm1, ntm1, nst, ntm2, ntn2, KS;  // tm1: GEMM1 token tile (gemm1_tm)
+    int nj2;     // GEMM2 column tile: 32 nj2 columns
+    int xcd2;    // GEMM2 grid: combos dealt to XCDs (see gemm2_tiled)
     int64_t nb;  // blocks of 64 tokens
     size_t off_bits, off_words, off_ulist, off_count, off_hhi, off_hlo, off_part, total;
 };
 
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
-TPlan make_tplan(int64_t B, int64_t L, int64_t d, int num_cu) {
+// exact: H as a hi + lo pair (SI_FLAG_EXACT_H), else one 16-bit value (no lo plane)
+TPlan make_tplan(int64_t B, int64_t L, int64_t d, int num_cu, bool exact) {
     TPlan p;
     p.W = (L + 31) / 32;
     p.Lp = p.W * 32;
@@ -458,14 +516,20 @@ TPlan make_tplan(int64_t B, int64_t L, int64_t d, int num_cu) {
     p.ntm1 = (int)((B + p.tm1 - 1) / p.tm1);
     p.nst = (int)((L + kT1S - 1) / kT1S);
     p.ntm2 = (int)((B + kT2M - 1) / kT2M);
-    p.ntn2 = (int)((d + kT2N - 1) / kT2N);
-    const int64_t tiles = (int64_t)p.ntm2 * p.ntn2;
-    int64_t ks = num_cu / tiles;  // whole rounds only: one wave of work-groups per CU
+    // GEMM2 column tile: the narrowest of 128, 160 and 192 columns that splits d into at most
+    // 32 tiles (one per CU of an XCD), else 192
+    p.nj2 = 4;
+    while (p.nj2 < 6 && (d + 32 * p.nj2 - 1) / (32 * p.nj2) > 32) ++p.nj2;
+    p.ntn2 = (int)((d + 32 * p.nj2 - 1) / (32 * p.nj2));
+    // split K so that the combos (token tile x K chunk) fill the CUs' column tiles in whole
+    // rounds: num_cu / ntn2 combos in all
+    int64_t ks = num_cu / ((int64_t)p.ntm2 * p.ntn2);
     if (ks < 1) ks = 1;
     const int64_t kmax = (L + kBK - 1) / kBK;
     if (ks > kmax) ks = kmax;
     if (ks > 64) ks = 64;
     p.KS = (int)ks;
+    p.xcd2 = (p.ntm2 * p.KS) % 8 == 0 ? 1 : 0;
     size_t o = 0;
     p.off_bits = o;
     o = align256(o + (size_t)B * p.W * 4);
@@ -479,7 +543,7 @@ TPlan make_tplan(int64_t B, int64_t L, int64_t d, int num_cu) {
     p.off_hhi = o;
     o = align256(o + (size_t)B * p.Up * 2);
     p.off_hlo = o;
-    o = align256(o + (size_t)B * p.Up * 2);
+    if (exact) o = align256(o + (size_t)B * p.Up * 2);
     p.off_part = o;
     o = align256(o + (size_t)p.KS * B * part_chunks(d) * kChunk * 4);
     p.total = o;
@@ -490,7 +554,8 @@ TPlan make_tplan(int64_t B, int64_t L, int64_t d, int num_cu) {
 
 hipError_t launch_bits_to_list(const uint32_t* bits, int64_t W, int32_t* list, int* count,
                                hipStream_t s) {
-    hipLaunchKernelGGL(union_scan, dim3(1), dim3(1024), 0, s, bits, (int64_t)1, W, list, count);
+    hipLaunchKernelGGL(union_scan, dim3(1), dim3(1024), (unsigned)(W * 4), s, bits, (int64_t)1, W,
+                       list, count);
     return hipGetLastError();
 }
 
@@ -524,12 +589,18 @@ int activation_tiles_max(int64_t T) { return (int)((T + 127) / 128); }
 bool tiled_supported(int64_t B, int64_t L, int64_t d) {
     const int64_t Up = (L + kBK - 1) / kBK * kBK;
     const int64_t lim = (int64_t)1 << 31;
-    // 32-bit buffer offsets; the token bitmaps are built in LDS (at most 64 KB)
-    return L * 2 * d * 2 < lim && B * d * 2 < lim && B * Up * 2 < lim && L <= 524288;
+    // 32-bit buffer offsets; the token bitmaps are built in LDS (at most 64 KB), and the union
+    // scan keeps the union words and its 16 wave totals there (W * 4 + 64 <= 64 KB)
+    return L * 2 * d * 2 < lim && B * d * 2 < lim && B * Up * 2 < lim && L <= 523776;
 }
 
-size_t tiled_workspace(int64_t B, int64_t L, int64_t d, int num_cu) {
-    return make_tplan(B, L, d, num_cu).total;
+// The tiled path is compute bound: by default H enters GEMM2 as one 16-bit value (about 8
+// significant bits for bf16; GEMM2 then does half the MFMA work); SI_FLAG_EXACT_H asks for the
+// hi + lo pair, SI_FLAG_FAST_H for the single value explicitly.
+bool tiled_exact_h(int flags) { return (flags & SI_FLAG_EXACT_H) && !(flags & SI_FLAG_FAST_H); }
+
+size_t tiled_workspace(int64_t B, int64_t L, int64_t d, int num_cu, int flags) {
+    return make_tplan(B, L, d, num_cu, tiled_exact_h(flags)).total;
 }
 
 template <typename ET>
@@ -537,14 +608,15 @@ hipError_t launch_union_tiled_t(const void* x, int64_t B, int64_t d, const int32
                                 const int32_t* idx, int64_t nnz, const void* gate_up_c,
                                 const void* down_c, int64_t L, float* y, void* ws, int flags,
                                 int num_cu, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
-    const TPlan p = make_tplan(B, L, d, num_cu);
+    const bool fast = !tiled_exact_h(flags);
+    const TPlan p = make_tplan(B, L, d, num_cu, !fast);
     uint8_t* base = static_cast<uint8_t*>(ws);
     uint32_t* bits = reinterpret_cast<uint32_t*>(base + p.off_bits);
     uint32_t* words = reinterpret_cast<uint32_t*>(base + p.off_words);
     int32_t* ulist = reinterpret_cast<int32_t*>(base + p.off_ulist);
     int* ucount = reinterpret_cast<int*>(base + p.off_count);
     uint16_t* hhi = reinterpret_cast<uint16_t*>(base + p.off_hhi);
-    uint16_t* hlo = reinterpret_cast<uint16_t*>(base + p.off_hlo);
+    uint16_t* hlo = fast ? nullptr : reinterpret_cast<uint16_t*>(base + p.off_hlo);
     float* part = reinterpret_cast<float*>(base + p.off_part);
     const uint16_t* xx = static_cast<const uint16_t*>(x);
     const uint16_t* gu = static_cast<const uint16_t*>(gate_up_c);
@@ -554,7 +626,8 @@ hipError_t launch_union_tiled_t(const void* x, int64_t B, int64_t d, const int32
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(or_blocks, dim3((unsigned)((p.W + 63) / 64), (unsigned)p.nb), dim3(256), 0,
                        s, bits, B, p.W, words);
-    hipLaunchKernelGGL(union_scan, dim3(1), dim3(1024), 0, s, words, p.nb, p.W, ulist, ucount);
+    hipLaunchKernelGGL(union_scan, dim3(1), dim3(1024), (unsigned)(p.W * 4), s, words, p.nb, p.W,
+                       ulist, ucount);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int nst8 = (p.nst + 7) / 8 * 8;
@@ -566,10 +639,27 @@ hipError_t launch_union_tiled_t(const void* x, int64_t B, int64_t d, const int32
         hipExtLaunchKernelGGL((gemm1_tiled<ET, kUnion, 128>), dim3((unsigned)(nst8 * p.ntm1)),
                               dim3(256), 0, s, ev0, nullptr, 0, xx, B, d, gu, L, ulist, ucount,
                               bits, p.W, hhi, hlo, p.Up, p.ntm1, nullptr);
-    const int fast = (flags & SI_FLAG_FAST_H) ? 1 : 0;
-    hipExtLaunchKernelGGL((gemm2_tiled<ET>), dim3((unsigned)p.ntn2, (unsigned)p.ntm2, (unsigned)p.KS),
-                          dim3(kT2T), 0, s, nullptr, ev1, 0, hhi, hlo, p.Up, B, dc, d, L, ulist,
-                          ucount, part, p.KS, fast);
+    const unsigned ncombo = (unsigned)(p.ntm2 * p.KS);
+    const dim3 g2 = p.xcd2 ? dim3(8, (unsigned)p.ntn2, ncombo / 8) : dim3((unsigned)p.ntn2, ncombo);
+    G2Grid gg;
+    gg.KS = p.KS;
+    gg.ntm = p.ntm2;
+    gg.xcd = p.xcd2;
+    // reciprocals ceil(2^32 / q); q = 1 (2^32) is not used by the kernel
+    gg.ks_m = (uint32_t)((((uint64_t)1 << 32) + (uint64_t)p.KS - 1) / (uint64_t)p.KS);
+    gg.ntm_m = (uint32_t)((((uint64_t)1 << 32) + (uint64_t)p.ntm2 - 1) / (uint64_t)p.ntm2);
+#define SI_G2T(NJ, F)                                                                           \
+    hipExtLaunchKernelGGL((gemm2_tiled<ET, NJ, F>), g2, dim3(kT2T), 0, s, nullptr, ev1, 0, hhi,  \
+                          hlo, p.Up, B, dc, d, L, ulist, ucount, part, gg)
+#define SI_G2NJ(NJ)                                                                             \
+    if (fast) SI_G2T(NJ, true); else SI_G2T(NJ, false);
+    switch (p.nj2) {
+        case 4: SI_G2NJ(4) break;
+        case 5: SI_G2NJ(5) break;
+        default: SI_G2NJ(6) break;
+    }
+#undef SI_G2NJ
+#undef SI_G2T
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     return launch_reduce_partials(part, p.KS, B, d, y, s);

@@ -557,8 +557,8 @@ bool union_supported(int64_t B, int64_t L, int64_t d) {
            L <= 524288 && B * ((L + 31) / 32) * 4 < ((int64_t)1 << 31);
 }
 
-size_t union_workspace(int64_t B, int64_t L, int64_t d, int num_cu) {
-    if (use_tiled(B, L, d)) return tiled_workspace(B, L, d, num_cu);
+size_t union_workspace(int64_t B, int64_t L, int64_t d, int num_cu, int flags) {
+    if (use_tiled(B, L, d)) return tiled_workspace(B, L, d, num_cu, flags);
     return make_plan(B, L, d, num_cu).total;
 }
 

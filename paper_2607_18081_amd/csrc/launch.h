@@ -35,7 +35,7 @@ hipError_t launch_decode(const void* x, int xdt, int64_t B, int64_t d, const int
 // ---- k_union.hip: union (MFMA) path -----------------------------------------------------
 // sizes the union kernels handle (their buffer loads take 32-bit byte offsets)
 bool union_supported(int64_t B, int64_t L, int64_t d);
-size_t union_workspace(int64_t B, int64_t L, int64_t d, int num_cu);
+size_t union_workspace(int64_t B, int64_t L, int64_t d, int num_cu, int flags);
 // et: the 16-bit element type of x and the weights (1 = bf16, 2 = IEEE half)
 hipError_t launch_union(const void* x, int64_t B, int64_t d, const int32_t* offsets,
                         const int32_t* idx, int64_t nnz, const void* gate_up_c,
@@ -49,7 +49,7 @@ hipError_t launch_token_bitmaps(const int32_t* offsets, const int32_t* idx, int6
 
 // ---- k_tiled.hip: union path for large batches (LDS-tiled MFMA GEMMs) ----------------------
 bool tiled_supported(int64_t B, int64_t L, int64_t d);
-size_t tiled_workspace(int64_t B, int64_t L, int64_t d, int num_cu);
+size_t tiled_workspace(int64_t B, int64_t L, int64_t d, int num_cu, int flags);
 hipError_t launch_union_tiled(const void* x, int64_t B, int64_t d, const int32_t* offsets,
                               const int32_t* idx, int64_t nnz, const void* gate_up_c,
                               const void* down_c, int64_t L, int et, float* y, void* ws,

@@ -131,6 +131,21 @@ def test_path_choice_by_batch(lib):
     assert ws(16, 0, dt=0) == ws(16, PER, dt=0)                          # f32: per-token
 
 
+def test_h_form_workspace(lib):
+    """From 128 tokens (the tiled GEMMs) h is one 16-bit value unless SI_FLAG_EXACT_H, whose
+    workspace adds the lo plane of H; FAST_H names the default and wins over EXACT_H; below
+    128 tokens the H flags do not change the workspace. The 13B-shape 512-token prefill fits
+    the no-allocation entry point's scratch either way."""
+    ws = lambda B, flags, L=9677, d=5120: lib.si_selective_ffn_workspace(
+        B, 3456 * B, L, d, 1, 1, flags)
+    EXACT, FAST = 128, 32
+    up = (9677 + 63) // 64 * 64
+    assert ws(512, EXACT) - ws(512, 0) == (512 * up * 2 + 255) // 256 * 256
+    assert ws(512, FAST) == ws(512, 0) == ws(512, FAST | EXACT)
+    assert ws(16, EXACT) == ws(16, 0) == ws(16, FAST)
+    assert ws(512, EXACT) <= 64 << 20
+
+
 def test_lib_exports_resnorm_entry(lib):
     # x_out overlapping x_prev is refused before anything is enqueued
     buf = ctypes.create_string_buffer(1024)

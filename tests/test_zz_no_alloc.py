@@ -40,7 +40,8 @@ def _pair(x, sets, gpu, flags=0):
 
 
 @pytest.mark.parametrize("B1,B2,flags", [(1, 1, 0), (16, 6, 0), (4, 2, si.FLAG_UNION),
-                                          (160, 130, 0), (3, 1, si.FLAG_PER_TOKEN)])
+                                          (160, 130, 0), (160, 130, si.FLAG_EXACT_H),
+                                          (3, 1, si.FLAG_PER_TOKEN)])
 def test_noalloc_matches_selective_ffn(B1, B2, flags):
     N, d, L = 3000, 2048, 2100
     say(f"noalloc: B={B1} then B={B2}, flags={flags}")
