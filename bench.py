@@ -15,8 +15,10 @@ host's cores, on a bounded sample of the same workload; its outputs for that sam
 the GPU's outputs are checked against.
 
 Other workloads (``--workload``): tiny_f32, llama2_7b_b16 (batch 16, union MFMA path),
-llama3_8b_stack (32 layers, residual RMSNorm between layers), llama2_13b_prefill (512 tokens,
-MFMA-bound union path); the selection steps around the path: dynset_llama2_13b (dynamic-set
+llama3_8b_stack (32 layers, residual RMSNorm between layers), llama3_8b_stack_table1 (the same
+stack with Table 1's layer range: layers 0-4 and the last two keep the whole FFN),
+llama2_13b_prefill (512 tokens, MFMA-bound union path); the selection steps around the path:
+dynset_llama2_13b (dynamic-set
 construction for a 512-token prompt on the 13B-shape layer, si_dynamic_set),
 profile_llama3_8b (Eq. 1 scores of 512 tokens over a full 8B-shape FFN layer,
 si_profile_scores) and load_llama2_7b (selective loading of the 7B-shape layer from host
@@ -213,10 +215,11 @@ class Workload:
     def row_bytes(self):
         return 3 * self.cfg.d * (2 if self.cfg.wdtype == "bf16" else 4)
 
-    def launch_bytes(self, step):
-        """Algorithmic HBM bytes of the main kernel(s) of one launch: rows read x 3 x d x s."""
+    def launch_bytes(self, step, layer=0):
+        """Algorithmic HBM bytes of the main kernel(s) of one launch: rows read x 3 x d x s (a
+        dense layer of a stack reads all N rows)."""
         cfg = self.cfg
-        rows = cfg.k if cfg.B == 1 else self.union_rows[step % cfg.steps]
+        rows = cfg.k_of(layer) if cfg.B == 1 else self.union_rows[step % cfg.steps]
         return rows * self.row_bytes()
 
     def launch_flops(self, step):
@@ -349,7 +352,7 @@ def _oracle_chain(t, x=None):
 
 # sample sizes: at least these many tokens (the stack: token chains through all layers)
 CPU_MIN_SAMPLE = {"tiny_f32": 64, "llama2_7b_decode": 32, "llama2_7b_b16": 32,
-                  "llama3_8b_stack": 4, "llama2_13b_prefill": 32}
+                  "llama3_8b_stack": 4, "llama3_8b_stack_table1": 4, "llama2_13b_prefill": 32}
 
 
 def cpu_leg(cfg, seconds, workers):
@@ -874,6 +877,13 @@ def main():
     # the CPU leg first: its worker processes are forked before any HIP call
     cpu, ref_out = (None, None) if args.no_cpu_baseline else cpu_leg(
         cfg, args.cpu_seconds, cpu_workers(args))
+    if cfg.dense_layers:  # (after the CPU leg: its workers fork before the library loads)
+        # the workload's whole layers are those outside Table 1's range, by the library's rule
+        import paper_2607_18081_amd as si
+        sel = si.selective_layers(cfg.layers)
+        if sorted(cfg.dense_layers) != np.flatnonzero(~sel).tolist():
+            sys.exit(f"dense layers {cfg.dense_layers} are not those si_selective_layers leaves "
+                     "whole")
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     work = Workload(cfg, args.copies, dev)
@@ -899,7 +909,9 @@ def main():
                         "what": "the whole si_selective_ffn call (bitmaps, union list, both "
                                 "GEMMs, reducer) per graph-replayed step, wall clock"}
     else:
-        byts = np.mean([work.launch_bytes(i) for i in launches])
+        # per layer of a stack step: the mean bytes of its layers over their mean kernel time
+        # (the layers of a stack with dense layers read different row counts)
+        byts = np.mean([work.launch_bytes(i, lay) for i in launches for lay in range(nlay)])
         achieved = byts / (kern_ms.mean() * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": achieved / HBM_PEAK_GBS, "traffic": traffic}
@@ -919,8 +931,8 @@ def main():
     roof["kernel_ms_p50"] = float(np.median(kern_ms))
     roof["kernel_launches_timed"] = int(len(kern_ms))
     roof["bytes_per_launch" if roof["bound"] == "hbm" else "flops_per_launch"] = float(
-        np.mean([work.launch_bytes(i) if roof["bound"] == "hbm" else work.launch_flops(i)
-                 for i in launches]))
+        np.mean([work.launch_bytes(i, lay) if roof["bound"] == "hbm" else work.launch_flops(i)
+                 for i in launches for lay in range(nlay)]))
     if cfg.B > 1:
         # MFMA work on the flops the tokens need (their own active rows) and on the
         # dense-over-union flops the union GEMMs execute
@@ -957,6 +969,8 @@ def main():
         "data": "synthetic (seeded; weights N(0,0.02), x N(0,1), Zipf(1.1) popularity)",
         "config": {"workload": cfg.name, "d": cfg.d, "N": cfg.N, "loaded": cfg.L,
                    "active": cfg.k, "batch": cfg.B, "layers": cfg.layers,
+                   **({"dense_layers": list(cfg.dense_layers),
+                       "dense_layer_rows": cfg.N} if cfg.dense_layers else {}),
                    "tokens_per_step": cfg.B, "sequence_tokens": cfg.steps * cfg.B,
                    "weight_copies": len(work.layers[0]), "hip_graph": graphed,
                    "parallelism": "single GPU"},

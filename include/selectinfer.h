@@ -360,6 +360,21 @@ int si_build_loaded_set(const int32_t* task_rank, const int32_t* model_rank, int
                         int64_t n_base, int64_t n_loaded, int32_t* loaded);
 
 /*
+ * Layer range of selective loading and computation (Evaluation, Table 1: first layer 5, last
+ * layer -2, i.e. the last two layers skipped; Memory Footprint section: r_layer is the
+ * fraction of layers selected): mask[i] = 1 for the layers first <= i < n_layers + last, 0 for
+ * the others, whose FFN stays whole (every neuron loaded and computed).
+ *
+ *   mask  [n_layers] uint8 out, HOST memory (may be NULL when n_layers = 0)
+ *   count (optional)  HOST int64 out: the number of selected layers
+ *
+ * Host only. SI_ERR_INVALID for n_layers < 0, first < 0, last > 0, or a NULL mask with
+ * n_layers > 0. A range that is empty (first >= n_layers + last) selects no layer.
+ */
+int si_selective_layers(int64_t n_layers, int64_t first, int64_t last, uint8_t* mask,
+                        int64_t* count);
+
+/*
  * Selective loading from host memory (Selective Loading section): the same outputs as
  * si_compact_ffn, but the full layer stays in host memory (any host buffer, e.g. a weight file
  * mapped into memory) and only the loaded neurons' slices are read and moved to the device:

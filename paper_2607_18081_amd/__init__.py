@@ -33,6 +33,7 @@ from .api import (  # noqa: F401
     selective_ffn_noalloc,
     selective_ffn_resnorm,
     selective_ffn_workspace,
+    selective_layers,
     set_timing_events,
     version,
 )

@@ -47,6 +47,7 @@ SIGNATURES = {
     "si_merge_scores": (c_int, [c_vp, c_vp, c_i64, c_i64, c_vp, c_vp]),
     "si_rank_neurons": (c_int, [c_vp, c_i64, c_vp, c_vp]),
     "si_build_loaded_set": (c_int, [c_vp, c_vp, c_i64, c_i64, c_i64, c_vp]),
+    "si_selective_layers": (c_int, [c_i64, c_i64, c_i64, c_vp, c_vp]),
     "si_load_selected": (c_int, [c_vp, c_vp, c_vp, c_i64, c_i64, c_int, c_vp, c_i64, c_vp, c_vp,
                                  c_vp, c_vp, c_vp]),
 }

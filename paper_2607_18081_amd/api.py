@@ -6,6 +6,7 @@ follow the C entry points without their ``si_`` prefix.
 """
 from __future__ import annotations
 
+import ctypes
 from dataclasses import dataclass
 
 import torch
@@ -391,6 +392,20 @@ def build_loaded_set(task_rank, model_rank, n_base: int, n_loaded: int):
                                     out.ctypes.data if out.size else None)
     _check(st, "si_build_loaded_set")
     return out
+
+
+def selective_layers(n_layers: int, first: int = 5, last: int = -2):
+    """si_selective_layers (host only): boolean mask of the layers whose FFN is loaded and
+    computed selectively, first <= i < n_layers + last (Table 1: 5 and -2)."""
+    import numpy as np
+
+    mask = np.zeros(max(int(n_layers), 0), dtype=np.uint8)
+    cnt = ctypes.c_int64(0)
+    st = load().si_selective_layers(n_layers, first, last,
+                                    mask.ctypes.data if mask.size else None, ctypes.byref(cnt))
+    _check(st, "si_selective_layers")
+    assert int(cnt.value) == int(mask.sum())
+    return mask.astype(bool)
 
 
 def load_selected(w_gate, w_up, w_down, loaded, device=None) -> CompactLayer:

@@ -186,6 +186,18 @@ int si_build_loaded_set(const int32_t* task_rank, const int32_t* model_rank, int
     return SI_OK;
 }
 
+int si_selective_layers(int64_t n_layers, int64_t first, int64_t last, uint8_t* mask,
+                        int64_t* count) {
+    if (n_layers < 0 || first < 0 || last > 0 || (n_layers > 0 && !mask)) return SI_ERR_INVALID;
+    int64_t c = 0;
+    for (int64_t i = 0; i < n_layers; ++i) {
+        mask[i] = (i >= first && i < n_layers + last) ? 1 : 0;
+        c += mask[i];
+    }
+    if (count) *count = c;
+    return SI_OK;
+}
+
 int si_load_selected(const void* w_gate, const void* w_up, const void* w_down, int64_t N,
                      int64_t d, si_dtype wdt, const int32_t* loaded, int64_t L, void* gate_up_c,
                      void* down_c, int32_t* slot_to_orig, int32_t* orig_to_slot,

@@ -503,9 +503,11 @@ __global__ __launch_bounds__(kThreads) void sffn_rows(
 }
 
 // y[b][c] = sum_{p = 0..P-1} of the partials of column c, in a fixed order. One (token, chunk)
-// pair per WPP waves: its P x 16 floats are contiguous; thread t adds the float4 groups
-// t, t + 64 WPP, ... (all of column quarter t % 4) in ascending order, then a fixed shuffle tree
-// over the lanes of one quarter and, for WPP = 4, a fixed-order sum of the waves through LDS.
+// pair per WPP waves: its P x kChunk floats are contiguous; thread t adds the float4 groups
+// t, t + 64 WPP, ... (all of column group t % kG, kG = kChunk / 4) in ascending order, then a
+// fixed shuffle tree over the lanes of one group and, for WPP = 4, a fixed-order sum of the
+// waves through LDS.
+constexpr int kG = kChunk / 4;  // float4 groups of a chunk
 template <int WPP>
 __global__ __launch_bounds__(256) void reduce_chunks(const float* __restrict__ partials, int P,
                                                      int64_t pairs, int64_t nch, int64_t d,
@@ -517,7 +519,7 @@ __global__ __launch_bounds__(256) void reduce_chunks(const float* __restrict__ p
     if (pair >= pairs) return;  // uniform per work-group when WPP = 4
     const int t = (w % WPP) * kWave + lane;
     const float4* base = reinterpret_cast<const float4*>(partials + pair * (int64_t)P * kChunk);
-    const int n4 = P * (kChunk / 4);
+    const int n4 = P * kG;
     float s[4] = {0.f, 0.f, 0.f, 0.f};
     int i = t;
     for (; i + 3 * NT < n4; i += 4 * NT) {
@@ -540,18 +542,18 @@ __global__ __launch_bounds__(256) void reduce_chunks(const float* __restrict__ p
         s[3] += v.w;
     }
 #pragma unroll
-    for (int m = 4; m < kWave; m <<= 1)
+    for (int m = kG; m < kWave; m <<= 1)
 #pragma unroll
         for (int e = 0; e < 4; ++e) s[e] += __shfl_xor(s[e], m, kWave);
     const int64_t b = pair / nch;
     const int64_t c0 = (pair % nch) * kChunk;
     if (WPP == 1) {
         const int64_t c = c0 + 4 * lane;
-        if (lane < 4 && c < d)  // d is a multiple of 4: the float4 is all in range
+        if (lane < kG && c < d)  // d is a multiple of 4: the float4 is all in range
             *reinterpret_cast<float4*>(y + b * d + c) = make_float4(s[0], s[1], s[2], s[3]);
     } else {
         __shared__ float red[WPP][kChunk];
-        if (lane < 4) {
+        if (lane < kG) {
 #pragma unroll
             for (int e = 0; e < 4; ++e) red[w][lane * 4 + e] = s[e];
         }
@@ -565,19 +567,19 @@ __global__ __launch_bounds__(256) void reduce_chunks(const float* __restrict__ p
     }
 }
 
-// The same sum for few partials (P < 16): thread i owns float4 group i % 4 of chunk i / 4 (over
-// tokens and chunks) and adds its P float4 values in ascending p.
+// The same sum for few partials (P < 16): thread i owns float4 group i % kG of chunk i / kG
+// (over tokens and chunks) and adds its P float4 values in ascending p.
 __global__ __launch_bounds__(256) void reduce_few(const float* __restrict__ partials, int P,
                                                   int64_t n4, int64_t nch, int64_t d,
                                                   float* __restrict__ y) {
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i >= n4) return;
-    const int64_t pair = i >> 2;  // (token, chunk)
-    const int q = (int)(i & 3);
+    const int64_t pair = i / kG;  // (token, chunk)
+    const int q = (int)(i % kG);
     const float4* base = reinterpret_cast<const float4*>(partials + pair * (int64_t)P * kChunk) + q;
     float4 s = base[0];
     for (int p = 1; p < P; ++p) {
-        const float4 v = base[p * (kChunk / 4)];
+        const float4 v = base[p * kG];
         s.x += v.x;
         s.y += v.y;
         s.z += v.z;
@@ -701,7 +703,7 @@ hipError_t launch_reduce_partials(const float* partials, int P, int64_t B, int64
     const int64_t nch = part_chunks(d);
     const int64_t pairs = B * nch;
     if (P < 16) {  // one thread per float4 of y: a wave reads 16 chunks' partials contiguously
-        const int64_t n4 = B * nch * (kChunk / 4);
+        const int64_t n4 = B * nch * kG;
         hipLaunchKernelGGL(reduce_few, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s,
                            partials, P, n4, nch, d, y);
     } else if (P >= 64) {  // four waves per (token, chunk) pair

@@ -386,6 +386,28 @@ def test_llama3_8b_stack_resnorm_fused():
                    gpu1, "bf16", "bf16")
 
 
+def test_llama3_8b_table1_dense_to_selective():
+    """Table 1's layer range on the 8B stack: layer 4, the last whole layer (all 14336 neurons
+    loaded and active), then layer 5, the first selective one, through the fused residual
+    RMSNorm call; both teacher-forced against the oracle."""
+    name = "llama3_8b_stack_table1"
+    cfg = CONFIGS[name]
+    assert not si.selective_layers(cfg.layers)[4] and si.selective_layers(cfg.layers)[5]
+    toks = [5, 6]
+    say(f"8B stack, Table 1 range: whole layer 4 into selective layer 5, tokens {toks}")
+    x4 = tokens_x(cfg, toks)
+    c, ref4, gpu4 = _layer(name, 4)
+    sets4 = _slots(ref4, active_sets(cfg, toks, 4))
+    assert all(len(s) == cfg.N for s in sets4)
+    y4 = _run(x4, sets4, gpu4)
+    want4 = _oracle(x4, sets4, ref4)
+    assert max_rel_l2(y4, want4) <= ALARM_PER_TOKEN and max_elem_err(y4, want4) <= ELEM
+    c, ref5, gpu5 = _layer(name, 5)
+    sets5 = _slots(ref5, active_sets(cfg, toks, 5))
+    assert all(len(s) == cfg.k for s in sets5)
+    _check_resnorm(x4, y4.astype(np.float32), sets5, ref5, gpu5, "bf16", "bf16")
+
+
 @pytest.mark.parametrize("B,d,wdtype,xdtype", [(1, 4104, "bf16", "bf16"), (2, 1000, "bf16", "bf16"),
                                                (3, 264, "f32", "f32"), (1, 8, "bf16", "bf16"),
                                                (2, 2052, "f32", "f32"), (2, 1000, "f32", "bf16"),

@@ -37,3 +37,28 @@ def test_build_loaded_set_errors():
         si.build_loaded_set(t, t, 3, 2)                                     # n_loaded < n_base
     with pytest.raises(si.SelectInferError):
         si.build_loaded_set(t, t, 0, 6)                                     # n_loaded > N
+
+
+def test_selective_layers_table1():
+    """si_selective_layers against the oracle's layer range and Table 1's counts: layers 5 to
+    the second-last (exclusive) of 28 and of 16 layers (21 and 9, the Memory Footprint
+    section's 9 of 16 for the 1B model)."""
+    import json
+    import os
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "table1_parameters.json")))
+    first, last = g["first_layer"], g["last_layer"]
+    for n in (0, 1, 5, 6, 7, 8, 16, 28, 32, 80):
+        got = si.selective_layers(n, first, last)
+        assert np.flatnonzero(got).tolist() == oracle.selective_layers(n, first, last)
+    assert int(si.selective_layers(g["n_layers_llama32_1b"], first, last).sum()) == \
+        g["selected_layers_llama32_1b"]
+    assert int(si.selective_layers(g["n_layers_llama32_3b"], first, last).sum()) == 21
+    m32 = si.selective_layers(32)                      # the defaults are Table 1's
+    assert np.flatnonzero(~m32).tolist() == [0, 1, 2, 3, 4, 30, 31]
+
+
+def test_selective_layers_errors():
+    for args in ((-1, 5, -2), (8, -1, -2), (8, 5, 1)):
+        with pytest.raises(si.SelectInferError):
+            si.selective_layers(*args)
+    assert not si.selective_layers(4, 5, -2).any()      # range past the end: no layer

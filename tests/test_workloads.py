@@ -72,3 +72,18 @@ def test_hot_core_overlap_statistics():
 def test_csr():
     off, ids = csr_from_sets([np.array([1, 2]), np.array([], np.int32), np.array([7])])
     assert off.tolist() == [0, 2, 2, 3] and ids.tolist() == [1, 2, 7]
+
+
+def test_table1_stack_dense_layers():
+    """The Table 1 stack: its selective layers are the 8B stack's own (same seeds); a dense
+    layer loads and activates every neuron."""
+    a, b = CONFIGS["llama3_8b_stack"], CONFIGS["llama3_8b_stack_table1"]
+    small = dict(d=64, N=300, L=180, k=45)
+    a, b = a.with_(**small), b.with_(**small)
+    assert np.array_equal(loaded_ids(a, 7), loaded_ids(b, 7))
+    for x, y in zip(active_sets(a, range(3), 7), active_sets(b, range(3), 7)):
+        assert np.array_equal(x, y)
+    assert b.L_of(0) == b.k_of(31) == 300 and b.L_of(5) == 180 and b.k_of(29) == 45
+    assert np.array_equal(np.sort(loaded_ids(b, 0)), np.arange(300))
+    for s in active_sets(b, range(2), 31):
+        assert np.array_equal(s, np.arange(300))

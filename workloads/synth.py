@@ -54,9 +54,18 @@ class FFNConfig:
     layers: int     # FFN layers (stack workload)
     wdtype: str     # 'f32' or 'bf16' (weights and x)
     hot: int = 0    # size of the shared hot core forced into every token's set
+    # layers whose FFN stays whole: every neuron loaded (L = N) and active in every token's
+    # set (k = N); the others load L and compute k neurons
+    dense_layers: tuple = ()
 
     def with_(self, **kw) -> "FFNConfig":
         return replace(self, **kw)
+
+    def L_of(self, layer: int) -> int:
+        return self.N if layer in self.dense_layers else self.L
+
+    def k_of(self, layer: int) -> int:
+        return self.N if layer in self.dense_layers else self.k
 
 
 def _r(frac: float, n: int) -> int:
@@ -74,6 +83,13 @@ CONFIGS = {
                                hot=_r(0.1, 11008)),
     "llama3_8b_stack": FFNConfig("llama3_8b_stack", 3, d=4096, N=14336, L=_r(0.6, 14336),
                                  k=_r(0.15, 14336), B=1, steps=512, layers=32, wdtype="bf16"),
+    # the 8B-shape stack with the layer range of the paper's Table 1: selective from layer 5 to
+    # the second-last (exclusive); the first five and the last two layers keep the whole FFN.
+    # Same seeds as llama3_8b_stack, so its selective layers are that workload's layers.
+    "llama3_8b_stack_table1": FFNConfig("llama3_8b_stack_table1", 3, d=4096, N=14336,
+                                        L=_r(0.6, 14336), k=_r(0.15, 14336), B=1, steps=512,
+                                        layers=32, wdtype="bf16",
+                                        dense_layers=(0, 1, 2, 3, 4, 30, 31)),
     "llama2_13b_prefill": FFNConfig("llama2_13b_prefill", 4, d=5120, N=13824,
                                     L=_r(0.7, 13824), k=_r(0.25, 13824), B=512, steps=1,
                                     layers=1, wdtype="bf16"),
@@ -134,9 +150,10 @@ def popularity(cfg: FFNConfig, layer: int = 0) -> tuple[np.ndarray, np.ndarray]:
 
 
 def loaded_ids(cfg: FFNConfig, layer: int = 0) -> np.ndarray:
-    """The L most popular neurons, in popularity order (int32, not sorted by id)."""
+    """The L most popular neurons, in popularity order (int32, not sorted by id); every neuron
+    for a dense layer."""
     pi, _ = popularity(cfg, layer)
-    return pi[: cfg.L].astype(np.int32)
+    return pi[: cfg.L_of(layer)].astype(np.int32)
 
 
 def layer_weights(cfg: FFNConfig, layer: int = 0):
@@ -170,15 +187,16 @@ def es_keys(cfg: FFNConfig, tokens, layer: int = 0) -> np.ndarray:
     """
     tokens = list(tokens)
     ids = _loaded_sorted(cfg, layer)
+    L = len(ids)
     pi, w = popularity(cfg, layer)
     wl = w[ids]
     hot = np.zeros(cfg.N, dtype=bool)
     if cfg.hot:
         hot[pi[: cfg.hot]] = True
     hot_l = hot[ids]
-    out = np.empty((len(tokens), cfg.L), dtype=np.float32)
+    out = np.empty((len(tokens), L), dtype=np.float32)
     for i, t in enumerate(tokens):
-        u = _rng(cfg.cfg_id, layer, P_KEYS, t).random(cfg.L)
+        u = _rng(cfg.cfg_id, layer, P_KEYS, t).random(L)
         u = np.maximum(u, np.finfo(np.float64).tiny)
         key = np.log(u) / wl
         key[hot_l] = np.inf
@@ -190,9 +208,12 @@ def active_sets(cfg: FFNConfig, tokens, layer: int = 0) -> list[np.ndarray]:
     """Per-token active sets as original neuron ids (int32, ascending).
 
     The k members with the largest sampling keys; keys are continuous, so ties do not occur.
+    A dense layer's set is every neuron.
     """
-    keys = es_keys(cfg, tokens, layer)
     ids = _loaded_sorted(cfg, layer)
+    if layer in cfg.dense_layers:
+        return [ids.astype(np.int32) for _ in tokens]
+    keys = es_keys(cfg, tokens, layer)
     out = []
     for row in keys:
         pick = np.argpartition(-row.astype(np.float64), cfg.k - 1)[: cfg.k] if cfg.k else []
