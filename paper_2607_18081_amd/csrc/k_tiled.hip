@@ -59,12 +59,17 @@ __global__ __launch_bounds__(256) void or_blocks(const uint32_t* __restrict__ bi
     const int wv = threadIdx.x >> 6;
     const int64_t w = (int64_t)blockIdx.x * 64 + lane;
     const int64_t b0 = (int64_t)blockIdx.y * 64 + 16 * wv;
-    uint32_t u = 0u;
-    if (w < W) {
+    // range-checked buffer loads, issued together (a load behind each token's condition made
+    // the compiler wait for it before the next)
+    const __amdgpu_buffer_rsrc_t rb = make_rsrc(bits, B * W * 4);
+    uint32_t v[16];
 #pragma unroll
-        for (int i = 0; i < 16; ++i)
-            if (b0 + i < B) u |= bits[(b0 + i) * W + w];
-    }
+    for (int i = 0; i < 16; ++i)
+        v[i] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(
+            rb, (w < W && b0 + i < B) ? (int)(((b0 + i) * W + w) * 4) : kOOB, 0, 0);
+    uint32_t u = 0u;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) u |= v[i];
     __shared__ uint32_t red[4][64];
     red[wv][lane] = u;
     __syncthreads();
@@ -177,12 +182,28 @@ __global__ __launch_bounds__(2 * TM) void gemm1_tiled(
         const int64_t tok = m0 + r0 + kRP * j;
         aoff[j] = tok < B ? (int)(tok * d * 2) : kOOB;
     }
+    // Union slot ids (the union list in kUnion mode, the union position itself otherwise) are
+    // read with range-checked buffer loads, issued together: behind a per-lane condition each
+    // load made the compiler wait for it before the next (one memory round trip apiece).
+    const __amdgpu_buffer_rsrc_t rul = make_rsrc(ulist, MODE == kUnion ? (int64_t)nU * 4 : 0);
+    auto union_slot = [&](int64_t u, bool ok) -> int32_t {
+        if constexpr (MODE == kUnion)
+            return ok ? (int32_t)__builtin_amdgcn_raw_buffer_load_b32(rul, (int)(u * 4), 0, 0)
+                      : -1;
+        else
+            return ok ? (int32_t)u : -1;
+    };
+    int32_t bslot[kBJ];
 #pragma unroll
     for (int j = 0; j < kBJ; ++j) {
         const int r = r0 + kRP * j;             // weight row of the tile
         const int64_t u = u0 + 16 * (r / 32) + (r % 16);
-        const int plane = (r % 32) / 16;        // 0 gate, 1 up
-        const int32_t slot = (r < kT1N && u < nU) ? (MODE == kUnion ? ulist[u] : (int32_t)u) : -1;
+        bslot[j] = union_slot(u, r < kT1N && u < nU);
+    }
+#pragma unroll
+    for (int j = 0; j < kBJ; ++j) {
+        const int plane = ((r0 + kRP * j) % 32) / 16;  // 0 gate, 1 up
+        const int32_t slot = bslot[j];
         boff[j] = (slot >= 0 && slot < L) ? (int)(((int64_t)slot * 2 + plane) * d * 2) : kOOB;
     }
     V16 pa[kAJ], pb[kBJ];
@@ -266,10 +287,36 @@ __global__ __launch_bounds__(2 * TM) void gemm1_tiled(
         }
         return;
     }
+    // The lane's 5 slots, then (kUnion) the bitmap word of each of its 8 tokens at each slot:
+    // all loads issued together, range-checked (an invalid pair reads nothing, as zero), then
+    // used. Loaded under the per-element condition they cost one memory round trip each, 40
+    // per work-group at the end of the kernel.
+    int32_t eslot[5];
 #pragma unroll
     for (int q = 0; q < 5; ++q) {
         const int64_t u = u0 + 16 * q + nn;
-        const int32_t slot = u < nU ? (MODE == kUnion ? ulist[u] : (int32_t)u) : -1;
+        eslot[q] = union_slot(u, u < nU);
+    }
+    uint32_t tword[5][2][4];
+    if constexpr (MODE == kUnion) {
+        const __amdgpu_buffer_rsrc_t rbm = make_rsrc(bits, B * W * 4);
+#pragma unroll
+        for (int q = 0; q < 5; ++q)
+#pragma unroll
+            for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int64_t tok = m0 + 32 * w + 16 * mi + 4 * g + i;
+                    const int32_t sl = eslot[q];
+                    const bool ok = tok < B && sl >= 0 && sl < L;
+                    tword[q][mi][i] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(
+                        rbm, ok ? (int)((tok * W + sl / 32) * 4) : kOOB, 0, 0);
+                }
+    }
+#pragma unroll
+    for (int q = 0; q < 5; ++q) {
+        const int64_t u = u0 + 16 * q + nn;
+        const int32_t slot = eslot[q];
 #pragma unroll
         for (int mi = 0; mi < 2; ++mi)
 #pragma unroll
@@ -279,7 +326,7 @@ __global__ __launch_bounds__(2 * TM) void gemm1_tiled(
                     if (MODE == kAct) {
                         out[tok * Up + u] = silu_f32(acc[mi][2 * q][i]) * acc[mi][2 * q + 1][i];
                     } else {
-                        const bool act = (bits[tok * W + slot / 32] >> (slot % 32)) & 1u;
+                        const bool act = (tword[q][mi][i] >> (slot % 32)) & 1u;
                         const float h =
                             act ? silu_f32(acc[mi][2 * q][i]) * acc[mi][2 * q + 1][i] : 0.0f;
                         const uint32_t hb = Mfma<ET>::rne(h);
