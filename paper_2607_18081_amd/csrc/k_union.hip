@@ -42,8 +42,10 @@ typedef __attribute__((ext_vector_type(4))) short s16x4_t;
 
 namespace {
 
-constexpr int kG2Cols = 256;               // GEMM2 columns per work-group
+constexpr int kG2Waves = 4;                // GEMM2 waves per work-group, 64 columns each
+constexpr int kG2Cols = 64 * kG2Waves;     // GEMM2 columns per work-group
 constexpr int kG2Pitch = kG2Cols + 16;     // LDS row pitch (bf16): rows 32 bytes apart in bank
+constexpr int kG2Tpr = kG2Cols / 32;       // staging threads per tile row (4 x 8 columns each)
 constexpr int kGemm1Waves = 8;
 constexpr int kWordRegs = 4;               // GEMM2 chunks span at most 64 kWordRegs words
 
@@ -355,11 +357,12 @@ __global__ __launch_bounds__(64 * kGemm1Waves) void union_gemm1(
         }
 }
 
-// GEMM2 (see the file comment). Grid: (ceil(d/256), ceil(B/(16*MT)), KS); 4 waves.
+// GEMM2 (see the file comment). Grid: (ceil(d / kG2Cols), ceil(B/(16*MT)), KS); kG2Waves waves,
+// wave w taking columns 64 w .. 64 w + 63 of the tile.
 // FAST: H enters the MFMA as its bf16 (or half) rounding alone, without the low part.
 // NT: one token tile, so each down row is read once: non-temporal loads.
 template <typename ET, int MT, bool FAST, bool NT>
-__global__ __launch_bounds__(256) void union_gemm2(const float* __restrict__ H, int64_t Lp,
+__global__ __launch_bounds__(64 * kG2Waves) void union_gemm2(const float* __restrict__ H, int64_t Lp,
                                                    int64_t B, const uint16_t* __restrict__ dc,
                                                    int64_t d, int64_t L,
                                                    const uint32_t* __restrict__ words, int64_t W,
@@ -383,10 +386,11 @@ __global__ __launch_bounds__(256) void union_gemm2(const float* __restrict__ H, 
         for (int j = 0; j < 4; ++j) acc[mt][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
     const __amdgpu_buffer_rsrc_t rd = make_rsrc(dc, L * d * 2);
-    const int sr = threadIdx.x >> 3;         // staging: tile row (slot 32 wd + sr)
-    // staging: the 8 lanes of a tile row take 16 contiguous bytes each of one 128-byte line
-    // per load (columns 64 e + 8 (t % 8) .. + 7 in load e), so a load reads whole lines
-    const int sc = (threadIdx.x & 7) * 8;
+    const int sr = threadIdx.x / kG2Tpr;     // staging: tile row (slot 32 wd + sr)
+    // staging: the kG2Tpr lanes of a tile row take 16 contiguous bytes each of kG2Cols / 4
+    // columns per load (columns kG2Cols / 4 * e + 8 (t % kG2Tpr) .. + 7 in load e), so a load
+    // reads whole 128-byte lines
+    const int sc = (threadIdx.x % kG2Tpr) * 8;
     // words of down rows in flight in registers ahead of the LDS tile being consumed: deeper
     // for few tokens, where the kernel only streams rows and register room is plentiful
     constexpr int kDepth = MT == 1 ? 8 : (MT == 2 ? 6 : 3);
@@ -419,7 +423,7 @@ __global__ __launch_bounds__(256) void union_gemm2(const float* __restrict__ H, 
         const int64_t slot = wd * 32 + sr;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const int64_t col = c0 + e * 64 + sc;
+            const int64_t col = c0 + e * (kG2Cols / 4) + sc;
             const int off = (rok && col < d) ? (int)((slot * d + col) * 2) : kOOB;
             v[e] = NT ? bload16nt(rd, off) : bload16(rd, off);
         }
@@ -500,7 +504,7 @@ __global__ __launch_bounds__(256) void union_gemm2(const float* __restrict__ H, 
         for (int q = 0; q < kDepth; ++q) {
             const int64_t wd = wg + q;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) st16(&tile[buf][sr][e * 64 + sc], nxt[q][e]);
+            for (int e = 0; e < 4; ++e) st16(&tile[buf][sr][e * (kG2Cols / 4) + sc], nxt[q][e]);
             const uint32_t word = word_at(wd);
             AV ahi[MT], alo[MT];
             a_ops(nh[q], ahi, alo);
@@ -600,7 +604,8 @@ hipError_t launch_union_t(const void* x, int64_t B, int64_t d, const int32_t* of
     dim3 g2((unsigned)((d + kG2Cols - 1) / kG2Cols),
             (unsigned)((B + 16 * p.MT - 1) / (16 * p.MT)), (unsigned)p.KS);
 #define SI_G2F(MTV, F, N)                                                                       \
-    hipExtLaunchKernelGGL((union_gemm2<ET, MTV, F, N>), g2, dim3(256), 0, s, nullptr, ev1, 0,     \
+    hipExtLaunchKernelGGL((union_gemm2<ET, MTV, F, N>), g2, dim3(64 * kG2Waves), 0, s, nullptr,  \
+                          ev1, 0,                                                             \
                           H, p.Lp, B, dc, d, L, words, p.W, part, p.KS)
 #define SI_G2(MTV)                                                                              \
     if (g2.y == 1) {                                                                            \

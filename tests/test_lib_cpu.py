@@ -165,3 +165,18 @@ def test_product_path_fails_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(_lib, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(_lib.LibraryMissing):
         _lib.load()
+
+
+def test_no_kernel_spills():
+    """Every kernel instance in the library keeps its state in registers: no scratch (register
+    spill) memory, by the compiler's per-kernel resource remarks recorded at build time."""
+    import json
+    import os
+    from paper_2607_18081_amd import build as b
+    if not os.path.exists(b.USAGE):
+        pytest.skip("the library was not built by build() in this tree (no resource record)")
+    usage = json.load(open(b.USAGE))
+    assert len(usage) > 50                   # every source's kernels were recorded
+    spilled = [(u["kernel"], u.get("scratch_bytes_per_lane")) for u in usage
+               if u.get("scratch_bytes_per_lane", 0) != 0]
+    assert not spilled, spilled
