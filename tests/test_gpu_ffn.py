@@ -165,10 +165,14 @@ def test_union_path_ragged(B, d, L):
 
 
 @pytest.mark.parametrize("B,d,L,sparse", [(128, 264, 613, False), (257, 1000, 300, False),
-                                           (300, 264, 613, True), (130, 64, 81, False)])
+                                           (300, 264, 613, True), (130, 64, 81, False),
+                                           (300, 4088, 1000, False), (140, 5112, 1000, True),
+                                           (160, 2048, 2100, False), (130, 6144, 700, False)])
 def test_union_tiled_ragged(B, d, L, sparse):
     """Batches of 128 tokens and more take the LDS-tiled GEMMs: ragged token, slot and K tiles,
-    a union much smaller than L (sparse), split-K tails, empty sets."""
+    a union much smaller than L (sparse), split-K tails, empty sets. The last four shapes run
+    GEMM2 on its XCD grid (combo counts 8, 8, 16, 8) with 128-, 160-, 128- and 192-column
+    tiles, the first two with a ragged last column tile."""
     N = L + 97
     say(f"union tiled B={B} d={d} L={L} sparse={sparse}")
     rng, draw, ref, gpu = _rand_problem(B * 7 + d + L, N, d, L, "bf16")
