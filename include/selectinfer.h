@@ -165,9 +165,11 @@ size_t si_selective_ffn_workspace(int64_t B, int64_t nnz, int64_t L, int64_t d,
  *     union of the B active sets is built on the device and both projections run as MFMA
  *     gather-GEMMs over the union rows, with each token's h masked to its own set; below 128
  *     tokens the union rows are streamed once (bandwidth bound) and h enters the second GEMM
- *     as a 16-bit hi + lo pair (about 16 significant bits), from 128 tokens on the products
- *     are LDS-tiled (compute bound) and h enters as one 16-bit value (about 8 significant bits
- *     for bf16, a relative error near 1e-3; SI_FLAG_EXACT_H: the pair).
+ *     as a 16-bit hi + lo pair (about 16 significant bits for bf16; for half 22 bits, but no
+ *     finer than 2^-25 absolute once |h| < 2^-3 and the low half is subnormal); from 128
+ *     tokens on the products are LDS-tiled (compute bound) and h enters as one 16-bit value
+ *     (about 8 significant bits for bf16, a relative error near 1e-3; SI_FLAG_EXACT_H: the
+ *     pair).
  * Requirements: d % 8 == 0 for 16-bit data, d % 4 == 0 for f32; d <= 16384 (16-bit weights)
  * or 8192 (f32 weights), else SI_ERR_UNSUPPORTED; 16-byte aligned x, gate_up_c, down_c, y and
  * ws; B >= 0; nnz >= 0; L >= 1.
