@@ -10,13 +10,14 @@
 //    work-group ORs the blocks and turns the union into the ascending list of its slots;
 //  - gemm1_tiled: a work-group computes TM tokens x 80 union slots, K = d in steps of 64,
 //    with TM / 32 waves of 32 tokens each. TM = 256 (two waves per SIMD) when that grid fits
-//    in one round of work-groups on the CUs; otherwise TM = 128, whose work-groups (41 KB of
+//    in one round of work-groups on the CUs; otherwise TM = 128, whose work-groups (46 KB of
 //    LDS) run two or three to a CU, so the grid's last round is not a partial one.
 //    The 160 weight rows of its tile are ordered per group of 16 slots as 16 gate rows then
 //    16 up rows, so gate and up of one (token, slot) land in the same lane and register of two
 //    neighbouring MFMA tiles and the SiLU*up*mask epilogue needs no data exchange. Both
 //    operands are K-contiguous rows (token rows of x, neuron rows of gate_up_c) staged in LDS
-//    with a 144-byte pitch, which keeps the 16 rows read by one ds_read_b128 in distinct banks.
+//    with a 160-byte pitch, at which neither the ds_read_b128 of 16 rows nor the staging
+//    stores meet bank conflicts.
 //    H is written as bf16(h), and with SI_FLAG_EXACT_H also lo = bf16(h - hi) as a second
 //    plane.
 //  - gemm2_tiled: Y partials for 256 tokens x 128-256 columns over one of KS chunks of the
@@ -45,7 +46,10 @@ namespace {
 typedef __attribute__((ext_vector_type(4))) short s16x4_t;
 
 constexpr int kBK = 64;          // K step (elements)
-constexpr int kKP = kBK + 8;     // LDS pitch (bf16) of K-contiguous tiles: 144 bytes
+// LDS pitch (bf16) of K-contiguous tiles: 160 bytes. Measured with the hardware's bank-conflict
+// counter on the fragment reads (16 rows at one 16-byte column, ds_read_b128) and the staging
+// writes: none at 160 bytes (or at 128 with an XOR swizzle), 3.6 cycles per read at 144.
+constexpr int kKP = kBK + 16;
 constexpr int kT1S = 80;         // GEMM1 union slots per work-group (5 groups of 16)
 constexpr int kT1N = 2 * kT1S;   // GEMM1 weight rows per work-group
 constexpr int kT2M = 256;        // GEMM2 tokens per work-group (4 waves x 64)
@@ -365,7 +369,10 @@ __global__ __launch_bounds__(kT2T) void gemm2_tiled(
     const uint16_t* __restrict__ dc, int64_t d, int64_t L, const int32_t* __restrict__ ulist,
     const int* __restrict__ ucount, float* __restrict__ part, G2Grid gg) {
     constexpr int kCols = 32 * NJ;                        // columns per work-group
-    constexpr int kPitch = kCols + 16;                    // LDS pitch (bf16) of the down tile
+    // LDS pitch (bf16) of the down tile: padded by 16 except for 160 columns, where the pad
+    // put the staging writes into bank conflicts (1.5 cycles per store, none unpadded); the
+    // transposing reads cost the same at either pitch
+    constexpr int kPitch = kCols + (NJ == 5 ? 0 : 16);
     constexpr int kCpr = kCols / 8;                       // 16-byte chunks per row segment
     constexpr int kDJ = (kBK * kCpr + kT2T - 1) / kT2T;   // staging passes of the down rows
     constexpr int kPlanes = FAST ? 1 : 2;
