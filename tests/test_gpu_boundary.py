@@ -146,6 +146,31 @@ def test_topk_ties_zeros_nan(L):
         si.select_topk(scores, L + 1)
 
 
+@pytest.mark.parametrize("seed", range(16))
+def test_topk_random_shapes(seed):
+    """Seeded random rows, lengths and k (including 0 and L), in both modes: integer-valued,
+    coarsely rounded (many ties), normal, and tiny (subnormal) keys, exact against the oracle."""
+    rng = np.random.default_rng(300 + seed)
+    B = int(rng.integers(1, 41))
+    L = int(rng.choice([int(rng.integers(1, 2000)), int(rng.integers(2000, 50000))]))
+    kind = seed % 4
+    if kind == 0:
+        rows = rng.integers(-20, 21, (B, L)).astype(np.float32)
+    elif kind == 1:
+        rows = rng.standard_normal((B, L)).astype(np.float32).round(2)
+    elif kind == 2:
+        rows = rng.standard_normal((B, L)).astype(np.float32)
+    else:
+        rows = (rng.standard_normal((B, L)) * 1e-39).astype(np.float32)
+    k = int(rng.choice([0, L, int(rng.integers(0, L + 1)), min(L, int(rng.integers(1, 64)))]))
+    mode = ("abs", "raw")[seed % 2]
+    say(f"topk random seed={seed}: B={B} L={L} k={k} {mode} kind={kind}")
+    got = host_array(si.select_topk(dev_tensor(rows), k, mode))
+    assert got.shape == (B, k)
+    for b in range(B):
+        assert np.array_equal(got[b], oracle.select_topk(rows[b], k, mode)), b
+
+
 @pytest.mark.parametrize("xdt,d", [("bf16", 4096), ("f32", 4096), ("bf16", 20000),
                                    ("f32", 100), ("bf16", 102), ("f32", 4098)])
 def test_residual_rmsnorm(xdt, d):
