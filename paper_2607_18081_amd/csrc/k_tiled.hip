@@ -210,8 +210,8 @@ __global__ __launch_bounds__(2 * TM) void gemm1_tiled(
         const int32_t slot = bslot[j];
         boff[j] = (slot >= 0 && slot < L) ? (int)(((int64_t)slot * 2 + plane) * d * 2) : kOOB;
     }
-    V16 pa[kAJ], pb[kBJ];
-    auto fetch = [&](int64_t k0) {
+    V16 pa0[kAJ], pb0[kBJ], pa1[kAJ], pb1[kBJ];
+    auto fetch = [&](int64_t k0, V16(&pa)[kAJ], V16(&pb)[kBJ]) {
         const int64_t k = k0 + 8 * ch;
         const bool kin = k < d;  // d % 8 == 0: a chunk is all in or all out
 #pragma unroll
@@ -228,8 +228,9 @@ __global__ __launch_bounds__(2 * TM) void gemm1_tiled(
 #pragma unroll
         for (int nj = 0; nj < 10; ++nj) acc[mi][nj] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-    fetch(0);
-    for (int64_t k0 = 0; k0 < d; k0 += kBK) {
+    // One K step: the staged tile (pa, pb) goes to LDS, the loads of a later tile are issued
+    // into the same registers, then the tile is multiplied out of LDS.
+    auto step = [&](int64_t k0, V16(&pa)[kAJ], V16(&pb)[kBJ]) {
         __syncthreads();  // the previous tile has been read
 #pragma unroll
         for (int j = 0; j < kAJ; ++j) st16(&sA[r0 + kRP * j][8 * ch], pa[j]);
@@ -237,10 +238,14 @@ __global__ __launch_bounds__(2 * TM) void gemm1_tiled(
         for (int j = 0; j < kBJ; ++j)
             if (r0 + kRP * j < kT1N) st16(&sB[r0 + kRP * j][8 * ch], pb[j]);
         __syncthreads();
-        fetch(k0 + kBK);  // in flight while this tile is used (past the end: reads nothing)
-        // keep the prefetch ahead of the MFMAs (the scheduler would otherwise sink the loads
-        // to the end of the iteration and expose their whole latency at the next LDS store)
-        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (TM == 256) {
+            fetch(k0 + 2 * kBK, pa, pb);  // two steps ahead (past the end: reads nothing)
+        } else {
+            fetch(k0 + kBK, pa, pb);  // one step ahead (past the end: reads nothing)
+            // keep the prefetch ahead of the MFMAs (the scheduler would otherwise sink the
+            // loads to the end of the step and expose their whole latency at the next LDS store)
+            __builtin_amdgcn_sched_barrier(0);
+        }
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
             typename Mfma<ET>::vec8 a[2];
@@ -260,6 +265,29 @@ __global__ __launch_bounds__(2 * TM) void gemm1_tiled(
                 for (int mi = 0; mi < 2; ++mi) acc[mi][nj] = Mfma<ET>::mma(a[mi], b, acc[mi][nj]);
             }
         }
+        if constexpr (TM == 256) {
+            // the loads spread over the step's MFMAs, one after every five
+#pragma unroll
+            for (int i = 0; i < kAJ + kBJ; ++i) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 5, 0);  // MFMA
+                __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // vector memory read
+            }
+        }
+    };
+    if constexpr (TM == 256) {
+        // Two tiles in flight, in alternating register sets: the loads of a tile have two
+        // steps to land, and go out spread over the MFMAs rather than in one burst (13B
+        // prefill GEMM1 128 -> 124 us). The 128-token form, which runs two or three work-groups
+        // to a CU, keeps one set: the second set's registers would cost it a work-group per CU.
+        fetch(0, pa0, pb0);
+        fetch(kBK, pa1, pb1);
+        for (int64_t k0 = 0; k0 < d; k0 += 2 * kBK) {  // an odd last step multiplies zeros
+            step(k0, pa0, pb0);
+            step(k0 + kBK, pa1, pb1);
+        }
+    } else {
+        fetch(0, pa0, pb0);
+        for (int64_t k0 = 0; k0 < d; k0 += kBK) step(k0, pa0, pb0);
     }
 
     // epilogue: register i of lane l of tile (mi, nj) is token 32 w + 16 mi + 4 g + i and
