@@ -468,21 +468,11 @@ __global__ __launch_bounds__(kT2T) void gemm2_tiled(
     auto fetch = [&](int64_t k0) {
         const int64_t k = k0 + 8 * ch;  // 8 union positions of one chunk
         const int64_t nv = ke - k;      // valid positions in the chunk, if below 8
-        // H past the chunk's K range is not part of this sum: zero it (branch-free)
-        uint32_t keep[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-            keep[e] = (2 * e + 1 < nv) ? 0xffffffffu : (2 * e < nv ? 0x0000ffffu : 0u);
 #pragma unroll
         for (int j = 0; j < kHJ; ++j) {
             const int off = (nv > 0 && hoff[j] != kOOB) ? hoff[j] + (int)(k * 2) : kOOB;
             ph[j] = bload16(rh, off);
             if constexpr (!FAST) pl[j] = bload16(rl, off);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                ph[j].w[e] &= keep[e];
-                if constexpr (!FAST) pl[j].w[e] &= keep[e];
-            }
         }
 #pragma unroll
         for (int j = 0; j < kDJ; ++j) {
@@ -503,9 +493,24 @@ __global__ __launch_bounds__(kT2T) void gemm2_tiled(
         fetch(kb);
     }
     for (int64_t k0 = kb; k0 < ke; k0 += kBK) {
+        // H past the chunk's K range is not part of this sum: zero it (branch-free). Applied
+        // here, where the tile is stored, and not where it is loaded: there it made the
+        // compiler wait for the loads before the step's MFMAs.
+        uint32_t keep[4];
+        {
+            const int64_t nv = ke - (k0 + 8 * ch);
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                keep[e] = (2 * e + 1 < nv) ? 0xffffffffu : (2 * e < nv ? 0x0000ffffu : 0u);
+        }
         __syncthreads();
 #pragma unroll
         for (int j = 0; j < kHJ; ++j) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                ph[j].w[e] &= keep[e];
+                if constexpr (!FAST) pl[j].w[e] &= keep[e];
+            }
             st16(&sH[0][r0 + 64 * j][8 * ch], ph[j]);
             if constexpr (!FAST) st16(&sH[kPlanes - 1][r0 + 64 * j][8 * ch], pl[j]);
         }
