@@ -404,6 +404,9 @@ __global__ __launch_bounds__(kT2T) void gemm2_tiled(
     constexpr int kCpr = kCols / 8;                       // 16-byte chunks per row segment
     constexpr int kDJ = (kBK * kCpr + kT2T - 1) / kT2T;   // staging passes of the down rows
     constexpr int kPlanes = FAST ? 1 : 2;
+    // two tiles in flight (alternating register sets) where the registers allow: one 16-bit h
+    // and at most 160 columns; the hi + lo form and 192 columns keep one set
+    constexpr bool kTwo = FAST && NJ <= 5;
     const int KS = gg.KS;
     const uint32_t combo = gg.xcd ? blockIdx.x + 8 * blockIdx.z : blockIdx.y;
     const uint32_t ct = gg.xcd ? blockIdx.y : blockIdx.x;
@@ -450,7 +453,7 @@ __global__ __launch_bounds__(kT2T) void gemm2_tiled(
         const int64_t c = n0 + 8 * (q % kCpr);
         dcol[j] = (q < kBK * kCpr && c < d) ? (int)c : -1;  // d % 8 == 0
     }
-    V16 ph[kHJ], pl[kHJ], pd[kDJ];
+    V16 ph0[kHJ], pl0[kHJ], pd0[kDJ], ph1[kHJ], pl1[kHJ], pd1[kDJ];
     // slot ids of the down rows of the next fetch, loaded one K step ahead of their use so
     // the row loads do not wait on them. The loads are unconditional (a union position past
     // the chunk has an out-of-range offset and reads nothing): validity is applied where the
@@ -465,7 +468,7 @@ __global__ __launch_bounds__(kT2T) void gemm2_tiled(
                 ru, (u < ke && dcol[j] >= 0) ? (int)(u * 4) : kOOB, 0, 0);
         }
     };
-    auto fetch = [&](int64_t k0) {
+    auto fetch = [&](int64_t k0, V16(&ph)[kHJ], V16(&pl)[kHJ], V16(&pd)[kDJ]) {
         const int64_t k = k0 + 8 * ch;  // 8 union positions of one chunk
         const int64_t nv = ke - k;      // valid positions in the chunk, if below 8
 #pragma unroll
@@ -488,11 +491,9 @@ __global__ __launch_bounds__(kT2T) void gemm2_tiled(
 #pragma unroll
         for (int nj = 0; nj < NJ; ++nj) acc[mi][nj] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-    if (kb < ke) {
-        load_slots(kb);
-        fetch(kb);
-    }
-    for (int64_t k0 = kb; k0 < ke; k0 += kBK) {
+    // One K step: the staged tile goes to LDS, the loads of a later tile are issued into the
+    // same registers, then the tile is multiplied out of LDS.
+    auto step = [&](int64_t k0, V16(&ph)[kHJ], V16(&pl)[kHJ], V16(&pd)[kDJ]) {
         // H past the chunk's K range is not part of this sum: zero it (branch-free). Applied
         // here, where the tile is stored, and not where it is loaded: there it made the
         // compiler wait for the loads before the step's MFMAs.
@@ -518,8 +519,12 @@ __global__ __launch_bounds__(kT2T) void gemm2_tiled(
         for (int j = 0; j < kDJ; ++j)
             if (dcol[j] >= 0) st16(&sD[drow[j]][dcol[j] - n0], pd[j]);
         __syncthreads();
-        fetch(k0 + kBK);  // past the end of the chunk: reads nothing
-        __builtin_amdgcn_sched_barrier(0);  // the prefetch stays ahead of the MFMAs
+        if constexpr (kTwo) {
+            fetch(k0 + 2 * kBK, ph, pl, pd);  // two steps ahead (past the chunk: nothing)
+        } else {
+            fetch(k0 + kBK, ph, pl, pd);  // one step ahead (past the chunk: reads nothing)
+            __builtin_amdgcn_sched_barrier(0);  // the prefetch stays ahead of the MFMAs
+        }
 #pragma unroll
         for (int ks2 = 0; ks2 < 2; ++ks2) {
             // B operand: lane (nn, g) needs union positions 8 g .. 8 g + 7 of column nn of a
@@ -565,6 +570,28 @@ __global__ __launch_bounds__(kT2T) void gemm2_tiled(
                 }
             }
         }
+        if constexpr (kTwo) {
+            // the loads spread over the step's MFMAs
+#pragma unroll
+            for (int i = 0; i < kHJ + 2 * kDJ; ++i) {
+                __builtin_amdgcn_sched_group_barrier(0x008, (8 * NJ) / (kHJ + 2 * kDJ), 0);
+                __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+            }
+        }
+    };
+    if (kb < ke) {
+        load_slots(kb);
+        fetch(kb, ph0, pl0, pd0);
+        if constexpr (kTwo) fetch(kb + kBK, ph1, pl1, pd1);
+    }
+    if constexpr (kTwo) {
+        // Two tiles in flight, in alternating register sets (as in GEMM1)
+        for (int64_t k0 = kb; k0 < ke; k0 += 2 * kBK) {  // an odd last step multiplies zeros
+            step(k0, ph0, pl0, pd0);
+            step(k0 + kBK, ph1, pl1, pd1);
+        }
+    } else {
+        for (int64_t k0 = kb; k0 < ke; k0 += kBK) step(k0, ph0, pl0, pd0);
     }
 
     // register i of lane l of tile (mi, nj): token 64 wm + 16 mi + 4 g + i, column
