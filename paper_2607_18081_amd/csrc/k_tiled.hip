@@ -210,7 +210,7 @@ __global__ __launch_bounds__(2 * TM) void gemm1_tiled(
         const int32_t slot = bslot[j];
         boff[j] = (slot >= 0 && slot < L) ? (int)(((int64_t)slot * 2 + plane) * d * 2) : kOOB;
     }
-    V16 pa0[kAJ], pb0[kBJ], pa1[kAJ], pb1[kBJ];
+    V16 pa0[kAJ], pb0[kBJ], pa1[kAJ], pb1[kBJ], pa2[kAJ], pb2[kBJ];
     auto fetch = [&](int64_t k0, V16(&pa)[kAJ], V16(&pb)[kBJ]) {
         const int64_t k = k0 + 8 * ch;
         const bool kin = k < d;  // d % 8 == 0: a chunk is all in or all out
@@ -239,7 +239,7 @@ __global__ __launch_bounds__(2 * TM) void gemm1_tiled(
             if (r0 + kRP * j < kT1N) st16(&sB[r0 + kRP * j][8 * ch], pb[j]);
         __syncthreads();
         if constexpr (TM == 256) {
-            fetch(k0 + 2 * kBK, pa, pb);  // two steps ahead (past the end: reads nothing)
+            fetch(k0 + 3 * kBK, pa, pb);  // three steps ahead (past the end: reads nothing)
         } else {
             fetch(k0 + kBK, pa, pb);  // one step ahead (past the end: reads nothing)
             // keep the prefetch ahead of the MFMAs (the scheduler would otherwise sink the
@@ -275,16 +275,23 @@ __global__ __launch_bounds__(2 * TM) void gemm1_tiled(
         }
     };
     if constexpr (TM == 256) {
-        // Two tiles in flight, in alternating register sets: the loads of a tile have two
+        // Three tiles in flight, in rotating register sets: the loads of a tile have three
         // steps to land, and go out spread over the MFMAs rather than in one burst (13B
-        // prefill GEMM1 128 -> 124 us). The 128-token form, which runs two or three work-groups
-        // to a CU, keeps one set: the second set's registers would cost it a work-group per CU.
+        // prefill GEMM1 128 -> 124 us with two sets, 119 us with three). The 128-token form,
+        // which runs two or three work-groups to a CU, keeps one set: a second set's registers
+        // would cost it a work-group per CU.
+        const int nks = (int)((d + kBK - 1) / kBK);
         fetch(0, pa0, pb0);
         fetch(kBK, pa1, pb1);
-        for (int64_t k0 = 0; k0 < d; k0 += 2 * kBK) {  // an odd last step multiplies zeros
-            step(k0, pa0, pb0);
-            step(k0 + kBK, pa1, pb1);
+        fetch(2 * kBK, pa2, pb2);
+        int ks0 = 0;
+        for (; ks0 + 3 <= nks; ks0 += 3) {
+            step((int64_t)ks0 * kBK, pa0, pb0);
+            step((int64_t)(ks0 + 1) * kBK, pa1, pb1);
+            step((int64_t)(ks0 + 2) * kBK, pa2, pb2);
         }
+        if (ks0 < nks) step((int64_t)ks0 * kBK, pa0, pb0);
+        if (ks0 + 1 < nks) step((int64_t)(ks0 + 1) * kBK, pa1, pb1);
     } else {
         fetch(0, pa0, pb0);
         for (int64_t k0 = 0; k0 < d; k0 += kBK) step(k0, pa0, pb0);
