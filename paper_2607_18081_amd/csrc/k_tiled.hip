@@ -592,11 +592,15 @@ __global__ __launch_bounds__(kT2T) void gemm2_tiled(
         if constexpr (kTwo) fetch(kb + kBK, ph1, pl1, pd1);
     }
     if constexpr (kTwo) {
-        // Two tiles in flight, in alternating register sets (as in GEMM1)
-        for (int64_t k0 = kb; k0 < ke; k0 += 2 * kBK) {  // an odd last step multiplies zeros
-            step(k0, ph0, pl0, pd0);
-            step(k0 + kBK, ph1, pl1, pd1);
+        // Two tiles in flight, in alternating register sets (as in GEMM1); the steps are
+        // counted, and an odd last one runs after the loop
+        const int ns = ke > kb ? (ke - kb + kBK - 1) / kBK : 0;
+        int s2 = 0;
+        for (; s2 + 2 <= ns; s2 += 2) {
+            step(kb + (int64_t)s2 * kBK, ph0, pl0, pd0);
+            step(kb + (int64_t)(s2 + 1) * kBK, ph1, pl1, pd1);
         }
+        if (s2 < ns) step(kb + (int64_t)s2 * kBK, ph0, pl0, pd0);
     } else {
         for (int64_t k0 = kb; k0 < ke; k0 += kBK) step(k0, ph0, pl0, pd0);
     }
