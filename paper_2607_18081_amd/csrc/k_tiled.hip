@@ -411,9 +411,9 @@ __global__ __launch_bounds__(kT2T) void gemm2_tiled(
     constexpr int kCpr = kCols / 8;                       // 16-byte chunks per row segment
     constexpr int kDJ = (kBK * kCpr + kT2T - 1) / kT2T;   // staging passes of the down rows
     constexpr int kPlanes = FAST ? 1 : 2;
-    // two tiles in flight (alternating register sets) where the registers allow: one 16-bit h
-    // and at most 160 columns; the hi + lo form and 192 columns keep one set
-    constexpr bool kTwo = FAST && NJ <= 5;
+    // tiles in flight (rotating register sets) as the registers allow: with one 16-bit h,
+    // three at 128 columns and two at 160; the hi + lo form and 192 columns keep one set
+    constexpr int kSets = !FAST ? 1 : (NJ <= 4 ? 3 : (NJ == 5 ? 2 : 1));
     const int KS = gg.KS;
     const uint32_t combo = gg.xcd ? blockIdx.x + 8 * blockIdx.z : blockIdx.y;
     const uint32_t ct = gg.xcd ? blockIdx.y : blockIdx.x;
@@ -460,7 +460,8 @@ __global__ __launch_bounds__(kT2T) void gemm2_tiled(
         const int64_t c = n0 + 8 * (q % kCpr);
         dcol[j] = (q < kBK * kCpr && c < d) ? (int)c : -1;  // d % 8 == 0
     }
-    V16 ph0[kHJ], pl0[kHJ], pd0[kDJ], ph1[kHJ], pl1[kHJ], pd1[kDJ];
+    V16 ph0[kHJ], pl0[kHJ], pd0[kDJ], ph1[kHJ], pl1[kHJ], pd1[kDJ], ph2[kHJ], pl2[kHJ],
+        pd2[kDJ];
     // slot ids of the down rows of the next fetch, loaded one K step ahead of their use so
     // the row loads do not wait on them. The loads are unconditional (a union position past
     // the chunk has an out-of-range offset and reads nothing): validity is applied where the
@@ -526,8 +527,8 @@ __global__ __launch_bounds__(kT2T) void gemm2_tiled(
         for (int j = 0; j < kDJ; ++j)
             if (dcol[j] >= 0) st16(&sD[drow[j]][dcol[j] - n0], pd[j]);
         __syncthreads();
-        if constexpr (kTwo) {
-            fetch(k0 + 2 * kBK, ph, pl, pd);  // two steps ahead (past the chunk: nothing)
+        if constexpr (kSets > 1) {
+            fetch(k0 + kSets * kBK, ph, pl, pd);  // kSets steps ahead (past the chunk: nothing)
         } else {
             fetch(k0 + kBK, ph, pl, pd);  // one step ahead (past the chunk: reads nothing)
             __builtin_amdgcn_sched_barrier(0);  // the prefetch stays ahead of the MFMAs
@@ -577,7 +578,7 @@ __global__ __launch_bounds__(kT2T) void gemm2_tiled(
                 }
             }
         }
-        if constexpr (kTwo) {
+        if constexpr (kSets > 1) {
             // the loads spread over the step's MFMAs
 #pragma unroll
             for (int i = 0; i < kHJ + 2 * kDJ; ++i) {
@@ -589,18 +590,21 @@ __global__ __launch_bounds__(kT2T) void gemm2_tiled(
     if (kb < ke) {
         load_slots(kb);
         fetch(kb, ph0, pl0, pd0);
-        if constexpr (kTwo) fetch(kb + kBK, ph1, pl1, pd1);
+        if constexpr (kSets > 1) fetch(kb + kBK, ph1, pl1, pd1);
+        if constexpr (kSets > 2) fetch(kb + 2 * kBK, ph2, pl2, pd2);
     }
-    if constexpr (kTwo) {
-        // Two tiles in flight, in alternating register sets (as in GEMM1); the steps are
-        // counted, and an odd last one runs after the loop
+    if constexpr (kSets > 1) {
+        // kSets tiles in flight, in rotating register sets (as in GEMM1); the steps are
+        // counted, and those left over run after the loop
         const int ns = ke > kb ? (ke - kb + kBK - 1) / kBK : 0;
         int s2 = 0;
-        for (; s2 + 2 <= ns; s2 += 2) {
+        for (; s2 + kSets <= ns; s2 += kSets) {
             step(kb + (int64_t)s2 * kBK, ph0, pl0, pd0);
             step(kb + (int64_t)(s2 + 1) * kBK, ph1, pl1, pd1);
+            if constexpr (kSets > 2) step(kb + (int64_t)(s2 + 2) * kBK, ph2, pl2, pd2);
         }
         if (s2 < ns) step(kb + (int64_t)s2 * kBK, ph0, pl0, pd0);
+        if (kSets > 2 && s2 + 1 < ns) step(kb + (int64_t)(s2 + 1) * kBK, ph1, pl1, pd1);
     } else {
         for (int64_t k0 = kb; k0 < ke; k0 += kBK) step(k0, ph0, pl0, pd0);
     }
