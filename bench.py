@@ -270,9 +270,9 @@ def run_gpu(work, steps, warmup, use_graph, timed_launches):
     main kernel of up to `timed_launches` steps with HIP events.
 
     Event records inside a replayed graph do not bracket kernels on ROCm, so the kernel
-    durations come from an eager pass over the same steps. That pass is queued behind a short
-    device-side sleep, so every launch is already queued when the GPU reaches it and the events
-    measure device time only.
+    durations come from an eager pass over the same steps. That pass is queued behind further
+    untimed replays of the graph (a device-side sleep without a graph), so every launch is
+    already queued when the GPU reaches it and the events measure device time only.
     """
     import torch
 
@@ -317,10 +317,17 @@ def run_gpu(work, steps, warmup, use_graph, timed_launches):
         b.record()
         evs.append((a, b))
     torch.cuda.synchronize()
-    try:
-        torch.cuda._sleep(int(50e6))  # ~20 ms: lets the host queue the whole pass first
-    except (AttributeError, RuntimeError):
-        log("no device sleep available: kernel timings may include launch latency")
+    if graph is not None:
+        # the timed steps again, untimed, for at least 20 ms: the host queues the whole pass
+        # behind them, and the GPU arrives at it busy (an idle wait let its clocks drop, and
+        # the MFMA-bound kernels then read up to 6% slow)
+        for _ in range(max(1, min(50, int(0.02 / max(wall, 1e-6)) + 1))):
+            graph.replay()
+    else:
+        try:
+            torch.cuda._sleep(int(50e6))  # ~20 ms: lets the host queue the whole pass first
+        except (AttributeError, RuntimeError):
+            log("no device sleep available: kernel timings may include launch latency")
     for i in range(n):
         work.launch(warmup + i, timing=evs[i * nlay:(i + 1) * nlay])
     torch.cuda.synchronize()
@@ -660,7 +667,7 @@ def main_select(args):
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    steps = args.steps if args.steps is not None else 16
+    steps = args.steps if args.steps is not None else 128   # about 20 ms: clocks settled
     copies = max(1, min(args.copies, 4))
     work = SelectWork(args.workload, copies, dev)
     log(f"workload {args.workload}: T={work.T} L={work.L} d={work.d}; steps={steps}")
@@ -899,9 +906,12 @@ def main():
     if args.workload in CEILING_WORKLOADS:
         return main_ceiling(args)
     cfg = CONFIGS[args.workload]
+    # prefill-sized batches are timed over 128 steps (about 25 ms): the GPU's clocks take some
+    # milliseconds of MFMA load to settle, and over 16 steps (4 ms) the 13B prefill read
+    # 234-250 us per step against 203 us over 128
     steps = args.steps if args.steps is not None else (
         cfg.steps if cfg.B == 1 and cfg.layers == 1 else (64 if cfg.layers > 1 else
-                                                          max(cfg.steps, 16)))
+                                                          max(cfg.steps, 128)))
     log(f"workload {cfg.name}: d={cfg.d} N={cfg.N} L={cfg.L} k={cfg.k} B={cfg.B} "
         f"layers={cfg.layers} {cfg.wdtype}; steps={steps} warmup={args.warmup}")
     # the CPU leg first: its worker processes are forked before any HIP call
