@@ -277,7 +277,7 @@ __global__ __launch_bounds__(2 * TM) void gemm1_tiled(
     if constexpr (TM == 256) {
         // Three tiles in flight, in rotating register sets: the loads of a tile have three
         // steps to land, and go out spread over the MFMAs rather than in one burst (13B
-        // prefill GEMM1 128 -> 124 us with two sets, 119 us with three). The 128-token form,
+        // prefill GEMM1 128 -> 124 us with two sets, 111 us with three). The 128-token form,
         // which runs two or three work-groups to a CU, keeps one set: a second set's registers
         // would cost it a work-group per CU.
         const int nks = (int)((d + kBK - 1) / kBK);
