@@ -213,6 +213,30 @@ def test_union_tiled_ragged(B, d, L, sparse):
     assert np.array_equal(_run(x, sets, gpu, flags=si.FLAG_EXACT_H), exact)
 
 
+@pytest.mark.parametrize("d", [64, 128, 192, 256, 320, 384, 448])
+def test_union_tiled_k_step_counts(d):
+    """The 256-token GEMM1 keeps three K tiles in flight in rotating register sets and runs the
+    one or two steps left over after its loop; GEMM2 keeps two or three. d = 64 .. 448 gives 1
+    to 7 K steps in GEMM1, and union sizes around multiples of 64 give GEMM2 chunks of every
+    remainder; each against the oracle and against the pair form of h."""
+    B, L = 200, 700
+    N = L + 50
+    say(f"tiled K steps d={d}")
+    rng, draw, ref, gpu = _rand_problem(9000 + d, N, d, L, "bf16", wscale=d ** -0.5)
+    for nU in (64, 130, 191, 257, L):
+        pool = rng.permutation(L)[:nU]
+        sets = [np.sort(rng.permutation(pool)[:int(rng.integers(1, nU + 1))]).astype(np.int32)
+                for _ in range(B)]
+        sets[0] = np.sort(pool).astype(np.int32)          # the union is the whole pool
+        x = draw(B, d, scale=1.0)
+        want = _oracle(x, sets, ref)
+        got = _run(x, sets, gpu)
+        err = max_rel_l2(got, want)
+        assert err <= TOL["bf16"] and max_elem_err(got, want) <= ELEM_ONE_H, (nU, err)
+        exact = _run(x, sets, gpu, flags=si.FLAG_EXACT_H)
+        assert max_rel_l2(exact, want) <= ALARM_PER_TOKEN, nU
+
+
 @pytest.mark.parametrize("seed", range(24))
 def test_random_shapes(seed):
     """Seeded random problems across the path boundaries: B from 1 to 300 (per-token below 5
