@@ -29,7 +29,9 @@
 //    SI_FLAG_EXACT_H asks for the hi + lo pair (about 16 bits, twice the MFMA work). The KS
 //    partials are added in a fixed order by the shared partial reducer.
 // Tiles are loaded with range-checked buffer loads (zeros outside), staged through registers
-// while the previous tile is multiplied out of LDS.
+// while the previous tile is multiplied out of LDS. Where the registers allow (GEMM1 with
+// 256-token tiles, GEMM2 with one 16-bit h and up to 160 columns) two or three tiles are in
+// flight in rotating register sets, and a step's loads are spread over its MFMAs.
 #include <hip/hip_ext.h>
 
 #include <atomic>
